@@ -1,0 +1,197 @@
+"""Seeded synthetic inputs shaped like the paper's workloads.
+
+This module holds no part of the method's arithmetic: it only draws keys,
+values, queries and per-page ranks, and rounds them to their storage type.
+Both the oracle side and the GPU side of every test receive the same arrays
+from here; neither imports the other.
+
+Recipe (every draw comes from numpy's PCG64 seeded by
+SeedSequence([seed, workload_id, tag, ...])):
+  * per page j of one (layer, batch, kv head), independently for K and V:
+    X_j = G_j W_j + 0.05 N_j with G_j (P x r0), W_j (r0 x d), N_j (P x d)
+    all i.i.d. N(0, 1) -- pages with low-rank structure plus noise, the
+    property the paper measures on real caches (Section 3.1);
+  * keys (not the tiny workload): 4 channels per (layer, kv head), drawn
+    without replacement, are scaled by 10 before RoPE; RoPE uses the
+    rotate-half convention at absolute position t = j P + row with base
+    5e5 (Llama-3-8B shape) or 1e6 (Qwen3-32B shape);
+  * queries: per (batch, query head) i.i.d. N(0, 1/d);
+  * ranks: fixed, or uniform over a set per (layer, batch, kv head, page);
+  * storage rounding: bf16 round-to-nearest-even, or none for fp32.
+"""
+from __future__ import annotations
+
+import dataclasses
+
+import numpy as np
+
+TAG_KEY, TAG_VALUE, TAG_OUTLIER, TAG_QUERY, TAG_RANK, TAG_FACTOR, TAG_TOKEN = range(7)
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    name: str
+    wid: int              # workload id used in the seed sequence
+    batch: int
+    kv_heads: int
+    q_heads: int
+    head_dim: int
+    page: int             # P
+    tokens: int           # T (prefill length)
+    sink: int             # S, tokens
+    window: int           # W, tokens
+    r0: int               # rank of the planted page structure
+    ranks: tuple          # rank choices for factorized pages
+    dtype: str            # "f32" or "bf16"
+    rope_base: float | None
+    outliers: int
+    layers: int = 1
+    decode_steps: int = 0
+
+    @property
+    def group(self) -> int:
+        return self.q_heads // self.kv_heads
+
+
+WORKLOADS = {
+    # 1 layer, 1 KV head, 1 query head, d=64, P=16, T=256, sink 16, window 32, r=4, fp32.
+    "tiny": Workload("tiny", 1, 1, 1, 1, 64, 16, 256, 16, 32, 4, (4,), "f32", None, 0),
+    # Llama-3-8B-shaped layer: 32 q / 8 kv heads, d=128, P=64, T=32K, batch 1, r=24, bf16.
+    "llama8b_32k": Workload("llama8b_32k", 2, 1, 8, 32, 128, 64, 32768, 64, 256, 24, (24,),
+                            "bf16", 5.0e5, 4),
+    # Qwen3-32B-shaped layer: 64 q / 8 kv heads, d=128, P=64, T=128K, batch 4,
+    # r uniform over {16, 24, 32}; a decode step runs 64 such layers.
+    "qwen32b_128k": Workload("qwen32b_128k", 3, 4, 8, 64, 128, 64, 131072, 64, 512, 24,
+                             (16, 24, 32), "bf16", 1.0e6, 4, layers=64),
+    # Incremental decode: Llama-3-8B heads, batch 32, prefill 16K then 512 steps, r=24.
+    "llama8b_incremental": Workload("llama8b_incremental", 4, 32, 8, 32, 128, 64, 16384, 64,
+                                    256, 24, (24,), "bf16", 5.0e5, 4, decode_steps=512),
+    # INT4 factors: Qwen3-32B heads, batch 8, T=128K.
+    "qwen32b_int4": Workload("qwen32b_int4", 5, 8, 8, 64, 128, 64, 131072, 64, 512, 24,
+                             (16, 24, 32), "bf16", 1.0e6, 4),
+}
+
+
+def rng(seed: int, wid: int, tag: int, *keys: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence(
+        [int(seed), int(wid), int(tag)] + [int(k) for k in keys])))
+
+
+# --------------------------------------------------------------------------
+# Storage rounding
+# --------------------------------------------------------------------------
+def bf16_bits(x: np.ndarray) -> np.ndarray:
+    """float32 -> bf16 bit patterns (uint16), round to nearest even."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
+    rounded = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    nan = np.isnan(np.asarray(x, dtype=np.float32))
+    out = rounded.astype(np.uint16)
+    out[nan] = 0x7FC0
+    return out
+
+
+def bf16_to_f32(bits: np.ndarray) -> np.ndarray:
+    return (np.asarray(bits, dtype=np.uint32) << 16).view(np.float32)
+
+
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """Values rounded to bf16 and returned as float32 (exactly representable)."""
+    return bf16_to_f32(bf16_bits(np.asarray(x, dtype=np.float32)))
+
+
+def round_storage(x: np.ndarray, dtype: str) -> np.ndarray:
+    return round_bf16(x) if dtype == "bf16" else np.asarray(x, dtype=np.float32)
+
+
+# --------------------------------------------------------------------------
+# Keys, values, queries, ranks
+# --------------------------------------------------------------------------
+def _rope(x: np.ndarray, positions: np.ndarray, base: float) -> np.ndarray:
+    """Rotate-half RoPE of rows of x (n x d) at the given absolute positions."""
+    d = x.shape[-1]
+    half = d // 2
+    inv = base ** (-np.arange(half, dtype=np.float64) * 2.0 / d)
+    ang = positions.astype(np.float64)[:, None] * inv[None, :]
+    c, s = np.cos(ang), np.sin(ang)
+    a = x[:, :half].astype(np.float64)
+    b = x[:, half:].astype(np.float64)
+    return np.concatenate([a * c - b * s, b * c + a * s], axis=1).astype(np.float32)
+
+
+def _low_rank_pages(g: np.random.Generator, n_pages: int, P: int, d: int, r0: int):
+    G = g.standard_normal((n_pages, P, r0), dtype=np.float32)
+    W = g.standard_normal((n_pages, r0, d), dtype=np.float32)
+    N = g.standard_normal((n_pages, P, d), dtype=np.float32)
+    return (np.matmul(G, W) + np.float32(0.05) * N).reshape(n_pages * P, d)
+
+
+def outlier_channels(wl: Workload, seed: int, layer: int, h: int) -> np.ndarray:
+    if wl.outliers <= 0:
+        return np.zeros(0, dtype=np.int64)
+    return rng(seed, wl.wid, TAG_OUTLIER, layer, h).choice(wl.head_dim, wl.outliers,
+                                                           replace=False)
+
+
+def kv_head(wl: Workload, seed: int, layer: int, b: int, h: int, tokens: int | None = None):
+    """K and V (tokens x d, float32 holding storage-rounded values) of one KV head."""
+    T = wl.tokens + wl.decode_steps if tokens is None else int(tokens)
+    P, d = wl.page, wl.head_dim
+    n_pages = -(-T // P)
+    K = _low_rank_pages(rng(seed, wl.wid, TAG_KEY, layer, b, h), n_pages, P, d, wl.r0)
+    V = _low_rank_pages(rng(seed, wl.wid, TAG_VALUE, layer, b, h), n_pages, P, d, wl.r0)
+    ch = outlier_channels(wl, seed, layer, h)
+    if ch.size:
+        K[:, ch] *= np.float32(10.0)
+    if wl.rope_base is not None:
+        K = _rope(K, np.arange(n_pages * P), wl.rope_base)
+    return round_storage(K[:T], wl.dtype), round_storage(V[:T], wl.dtype)
+
+
+def kv_layer(wl: Workload, seed: int, layer: int, tokens: int | None = None):
+    """K, V of a whole layer: (batch, kv_heads, tokens, d) float32."""
+    T = wl.tokens + wl.decode_steps if tokens is None else int(tokens)
+    K = np.empty((wl.batch, wl.kv_heads, T, wl.head_dim), dtype=np.float32)
+    V = np.empty_like(K)
+    for b in range(wl.batch):
+        for h in range(wl.kv_heads):
+            K[b, h], V[b, h] = kv_head(wl, seed, layer, b, h, T)
+    return K, V
+
+
+def queries(wl: Workload, seed: int, step: int = 0) -> np.ndarray:
+    """Decode queries (batch, q_heads, d), i.i.d. N(0, 1/d), storage-rounded."""
+    out = np.empty((wl.batch, wl.q_heads, wl.head_dim), dtype=np.float32)
+    for b in range(wl.batch):
+        g = rng(seed, wl.wid, TAG_QUERY, step, b)
+        out[b] = g.standard_normal((wl.q_heads, wl.head_dim)) / np.sqrt(wl.head_dim)
+    return round_storage(out, wl.dtype)
+
+
+def page_ranks(wl: Workload, seed: int, layer: int, n_pages: int) -> np.ndarray:
+    """Rank of every logical page, (batch, kv_heads, n_pages) uint8; uniform over
+    wl.ranks when it holds several choices."""
+    out = np.empty((wl.batch, wl.kv_heads, n_pages), dtype=np.uint8)
+    choices = np.asarray(wl.ranks, dtype=np.uint8)
+    for b in range(wl.batch):
+        for h in range(wl.kv_heads):
+            if len(choices) == 1:
+                out[b, h] = choices[0]
+            else:
+                out[b, h] = rng(seed, wl.wid, TAG_RANK, layer, b, h).choice(choices, n_pages)
+    return out
+
+
+def factor_page(wl: Workload, seed: int, layer: int, b: int, h: int, j: int, r_k: int,
+                r_v: int):
+    """Factor pairs drawn directly (not from a decomposition), storage-rounded:
+    L (P x r) ~ N(0, 1/P), R (r x d) ~ N(0, r0 P / r), so L R has the
+    per-element scale of the planted pages. Used where a test needs a full-size
+    cache whose factors must not come from the GPU decomposition."""
+    g = rng(seed, wl.wid, TAG_FACTOR, layer, b, h, j)
+    P, d = wl.page, wl.head_dim
+    out = []
+    for r in (r_k, r_v):
+        L = g.standard_normal((P, r)) / np.sqrt(P)
+        R = g.standard_normal((r, d)) * np.sqrt(wl.r0 * P / r)
+        out += [round_storage(L, wl.dtype), round_storage(R, wl.dtype)]
+    return tuple(out)
