@@ -1,0 +1,325 @@
+#!/usr/bin/env python3
+"""Benchmark of the PuzzleKV hot path on one MI355X.
+
+Workload (default qwen32b_128k): Qwen3-32B-shaped layer -- 64 query heads over
+8 KV heads, d=128, pages of 64 tokens, batch 4, 131072 cached tokens per
+sequence, 64-token sink and 512-token window dense, every other page stored as
+bf16 factors with a per-page rank drawn from {16, 24, 32}. A decode step runs
+64 layers, each with its own cache buffers: append the new token, factorize
+pages that leave the window (the host planner decides; none at this length
+inside a short run), and mixed-page decode attention.
+
+Setup (untimed): the seeded generator draws layer 0's prompt K/V, the GPU
+decomposition builds its hybrid cache (timed separately for pages/s), and the
+layer's buffers are copied into the 63 other layers. Inputs are resident in
+HBM when the timed region starts.
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attention_traffic.txt")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_23843_amd", "csrc", f)
+                  for f in ("attention.inl", "attention_mfma.inl", "attention_launch.inl")]
+
+
+def log(msg: str) -> None:
+    print("[bench %7.1fs] %s" % (time.time() - T0, msg), file=sys.stderr, flush=True)
+
+
+T0 = time.time()
+
+
+def kernel_hash() -> str:
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(workload: str):
+    """HBM bytes per attention launch from the committed rocprofv3 counter
+    summary, if it was taken on the current kernel source; else None."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    vals = {}
+    with open(TRAFFIC_FILE) as f:
+        for line in f:
+            if "=" in line and not line.startswith("#"):
+                k, v = line.split("=", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_hash") != kernel_hash() or vals.get("workload") != workload:
+        return None
+    try:
+        return float(vals["bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="qwen32b_128k")
+    ap.add_argument("--layers", type=int, default=0, help="layers per step (default: the workload's)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-seconds", type=float, default=12.0,
+                    help="CPU-baseline budget for the oracle (0 disables)")
+    ap.add_argument("--workers", type=int, default=16, help="host threads for input generation")
+    return ap.parse_args()
+
+
+def attention_bytes(pk_cache, ranks_np, seq_len, P, d, B, Hkv, Hq, S, W):
+    """Algorithmic bytes one attention launch must move: every stored byte of
+    every page it reads (factor pairs at their ranks, dense pages up to the
+    sequence length), the page-table entries, the queries, out and lse."""
+    total = 0
+    fpb = {}
+    for b in range(B):
+        T = int(seq_len[b])
+        n = -(-T // P)
+        sink_pages = -(-S // P)
+        jmax = (T - W) // P - 1 if T - W >= 0 else -1
+        for h in range(Hkv):
+            for j in range(n):
+                if sink_pages <= j <= jmax:
+                    r = int(ranks_np[b, h, j])
+                    if r not in fpb:
+                        fpb[r] = pk_cache.factor_page_bytes(r, r)
+                    total += fpb[r]
+                else:
+                    rows = min(P, T - j * P)
+                    total += 2 * rows * d * 2
+            total += n * 8
+    total += B * Hq * d * 2 + B * Hq * d * 4 + B * Hq * 4
+    return total
+
+
+def cpu_baseline(wl, seed, seq_T, K_dense, V_dense, q, budget_s, layers):
+    """The oracle on a bounded sample: whole (sequence, KV head) heads of one
+    layer at the full length, factor pages drawn by the generator, timed until
+    the budget is spent; extrapolated to the step (all heads, all layers)."""
+    import numpy as np
+    import oracle
+    import synth
+    P, d, g = wl.page, wl.head_dim, wl.group
+    kinds = oracle.plan_pages(seq_T, P, wl.sink, wl.window)
+    ranks = synth.page_ranks(wl, seed, 0, len(kinds))
+    times, heads = [], []
+    for b in range(wl.batch):
+        for h in range(wl.kv_heads):
+            pages = []
+            for j, kd in enumerate(kinds):
+                if kd == oracle.FACTOR:
+                    r = int(ranks[b, h, j])
+                    Lk, Rk, Lv, Rv = synth.factor_page(wl, seed, 0, b, h, j, r, r)
+                    pages.append(("factor", Lk, Rk, Lv, Rv))
+                else:
+                    Kp, Vp = K_dense[(b, h, j)], V_dense[(b, h, j)]
+                    pages.append(("dense", Kp, Vp))
+            head = oracle.HeadCache(seq_T, P, d, pages)
+            t = time.time()
+            oracle.attention(head, q[b, h * g:(h + 1) * g].astype(np.float64))
+            times.append(time.time() - t)
+            heads.append((b, h))
+            if sum(times) >= budget_s:
+                break
+        if sum(times) >= budget_s:
+            break
+    per_head = sum(times) / len(times)
+    n_heads = wl.batch * wl.kv_heads
+    us_step = per_head * n_heads * layers * 1e6
+    return {
+        "value": us_step, "unit": "us/step", "cores": oracle.num_threads(), "kind": "oracle",
+        "sample": "%d of %d (sequence, KV head) heads of one layer at T=%d (fp64 rebuild + softmax), "
+                  "%.2f s per head, extrapolated x%d heads x%d layers" % (len(times), n_heads, seq_T,
+                                                                          per_head, n_heads, layers),
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(asked for --gpus %d, WORLD_SIZE=%d)" % (args.gpus, world), file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2608_23843_amd as pk
+    import synth
+
+    pk.load_library()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        sys.exit(1)
+    torch.cuda.set_device(0)
+    wl = synth.WORKLOADS[args.workload]
+    layers = args.layers or wl.layers
+    B, Hkv, Hq, d, P, T = wl.batch, wl.kv_heads, wl.q_heads, wl.head_dim, wl.page, wl.tokens
+    S, W = wl.sink, wl.window
+    n_steps = args.warmup + args.steps
+    max_pages = -(-(T + n_steps + 1) // P) + 1
+    max_rank = max(wl.ranks)
+    log("workload %s: B=%d Hq=%d Hkv=%d d=%d P=%d T=%d layers=%d" % (wl.name, B, Hq, Hkv, d, P, T, layers))
+
+    # ---- inputs ----------------------------------------------------------------
+    K, V = synth.kv_layer(wl, args.seed, 0, T, workers=args.workers)
+    log("generated layer-0 K/V (%.1f GB fp32 on host)" % (2 * K.nbytes / 1e9))
+    kinds = pk.plan_pages(T, P, S, W)
+    dense_idx = [j for j, kd in enumerate(kinds) if kd == pk.PKV_DENSE]
+    K_dense = {(b, h, j): K[b, h, j * P:(j + 1) * P].astype(np.float64)
+               for b in range(B) for h in range(Hkv) for j in dense_idx}
+    V_dense = {(b, h, j): V[b, h, j * P:(j + 1) * P].astype(np.float64)
+               for b in range(B) for h in range(Hkv) for j in dense_idx}
+    bf = torch.bfloat16
+    kt = torch.from_numpy(K).to("cuda", bf)
+    del K
+    vt = torch.from_numpy(V).to("cuda", bf)
+    del V
+    ranks_np = synth.page_ranks(wl, args.seed, 0, max_pages)
+    ranks = torch.from_numpy(ranks_np).cuda().contiguous()
+
+    cache = pk.PuzzleKVCache(layers, B, Hkv, Hq, d, P, max_pages, max_rank, S, W, "bf16", "bf16")
+    log("cache: factor pool %.1f GB, dense pool %.2f GB" % (cache.factor_pool.numel() / 1e9,
+                                                            cache.dense_pool.numel() / 1e9))
+
+    # ---- batched page decomposition (prefill of layer 0) ----------------------
+    n_fact = int((kinds == pk.PKV_FACTOR).sum()) * B * Hkv
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    comp_ms = []
+    for rep in range(3):
+        torch.cuda.synchronize()
+        ev0.record()
+        cache.prefill(0, kt, vt, [T] * B, rank_k=ranks, rank_v=ranks)
+        ev1.record()
+        torch.cuda.synchronize()
+        comp_ms.append(ev0.elapsed_time(ev1))
+    status = cache.device_status()
+    comp_ms_best = min(comp_ms)
+    pages_per_s = n_fact / (comp_ms_best / 1e3)
+    log("prefill/decomposition: %d page pairs in %.2f ms (%.3g pairs/s), status %d"
+        % (n_fact, comp_ms_best, pages_per_s, status))
+    del kt, vt
+    torch.cuda.empty_cache()
+
+    # ---- replicate layer 0 into the other layers --------------------------------
+    per_d = cache.dense_pool.numel() // layers
+    per_f = cache.factor_pool.numel() // layers
+    per_t = cache.table.numel() // layers
+    for layer in range(1, layers):
+        cache.dense_pool[layer * per_d:(layer + 1) * per_d].copy_(cache.dense_pool[:per_d])
+        cache.factor_pool[layer * per_f:(layer + 1) * per_f].copy_(cache.factor_pool[:per_f])
+        cache.table[layer * per_t:(layer + 1) * per_t].copy_(cache.table[:per_t])
+    torch.cuda.synchronize()
+    log("replicated layer 0 into %d layers" % layers)
+
+    # ---- decode steps ------------------------------------------------------------
+    ws = cache.workspace(pk.PKV_OP_ATTENTION, T + n_steps + 1)
+    out = torch.empty((B, Hq, d), dtype=torch.float32, device="cuda")
+    lse = torch.empty((B, Hq), dtype=torch.float32, device="cuda")
+    qs = [torch.from_numpy(synth.queries(wl, args.seed, s)).to("cuda", bf).contiguous() for s in range(n_steps)]
+    toks = [tuple(torch.from_numpy(x).to("cuda", bf).contiguous() for x in synth.decode_kv(wl, args.seed, 0, T + s))
+            for s in range(n_steps)]
+    stream = torch.cuda.current_stream()
+    call_events = []
+    step_start = step_end = None
+    compress_calls = 0
+    for s in range(n_steps):
+        timed = s >= args.warmup
+        if s == args.warmup:
+            torch.cuda.synchronize()
+            step_start = torch.cuda.Event(enable_timing=True)
+            step_start.record(stream)
+        pos = T + s
+        new_pages = pk.eligible_pages(pos, pos + 1, P, S, W)
+        for layer in range(layers):
+            cache.append(layer, toks[s][0], toks[s][1], [pos] * B)
+            if len(new_pages):
+                bb, hh, jj = zip(*[(b, h, int(j)) for b in range(B) for h in range(Hkv) for j in new_pages])
+                rr = [int(ranks_np[b, h, j]) for b, h, j in zip(bb, hh, jj)]
+                cache.compress_pages(layer, bb, hh, jj, rr, rr)
+                compress_calls += 1
+            if timed:
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record(stream)
+            cache.attention(layer, qs[s], [pos + 1] * B, out=out, lse=lse, workspace=ws)
+            if timed:
+                e1.record(stream)
+                call_events.append((e0, e1))
+        if s == 0:
+            torch.cuda.synchronize()
+            log("first step done")
+    step_end = torch.cuda.Event(enable_timing=True)
+    step_end.record(stream)
+    torch.cuda.synchronize()
+    status |= cache.device_status()
+    ms_total = step_start.elapsed_time(step_end)
+    ms_per_step = ms_total / args.steps
+    call_ms = np.array([a.elapsed_time(b) for a, b in call_events])
+    attn_us = float(call_ms.mean() * 1e3)
+    log("decode: %.3f ms/step, attention %.1f us/layer (median %.1f), status %d"
+        % (ms_per_step, attn_us, float(np.median(call_ms) * 1e3), status))
+    if not np.isfinite(out.float().cpu().numpy()).all():
+        raise RuntimeError("non-finite attention output")
+
+    mid_T = T + args.warmup + args.steps // 2 + 1
+    abytes = attention_bytes(cache, ranks_np, [mid_T] * B, P, d, B, Hkv, Hq, S, W)
+    achieved = abytes / (attn_us * 1e-6) / 1e9
+    traffic = measured_traffic(wl.name)
+    roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                "frac": round(achieved / HBM_PEAK_GBPS, 4),
+                "traffic": traffic}
+
+    result = {
+        "metric": "mixed-page decode attention time per decode step (64 layers, Qwen3-32B heads, 128K context)"
+                  if wl.name == "qwen32b_128k" else "mixed-page decode attention time per decode step",
+        "value": round(ms_per_step * 1e3, 2),
+        "unit": "us/step",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "batch": B, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d,
+                   "page": P, "tokens": T, "sink": S, "window": W, "ranks": list(wl.ranks),
+                   "layers": layers, "step": "append + planner + compress-when-eligible + attention per layer"},
+        "attention_us_per_layer": round(attn_us, 2),
+        "attention_algorithmic_bytes": int(abytes),
+        "attention_gbps": round(achieved, 1),
+        "compress_page_pairs_per_s": round(pages_per_s, 1),
+        "compress_ms_per_layer_prefill": round(comp_ms_best, 3),
+        "compress_calls_in_run": compress_calls,
+        "device_status": status,
+        "roofline": roofline,
+    }
+    if args.cpu_seconds > 0:
+        log("CPU baseline (oracle), budget %.0f s" % args.cpu_seconds)
+        q0 = synth.queries(wl, args.seed, 0)
+        result["cpu_baseline"] = cpu_baseline(wl, args.seed, T, K_dense, V_dense, q0, args.cpu_seconds,
+                                              layers)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

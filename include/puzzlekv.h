@@ -1,0 +1,247 @@
+/*
+ * puzzlekv.h -- C ABI of the PuzzleKV hot path on MI355X (gfx950).
+ *
+ * PuzzleKV keeps every token of a KV cache: each (layer, KV head) is cut into
+ * pages of P tokens; a sink page and a local window stay dense, every other
+ * completed page is stored as an independent rank-r factor pair
+ * K_p ~ L_K R_K, V_p ~ L_V R_V (Section 3.3, Eq. (2)). Decode attention reads
+ * the mixed cache directly (Eq. (4), Eq. (5)); pages that leave the window are
+ * factorized during decoding (Section 3.3, "Incremental Cache Update").
+ *
+ * Conventions for every call:
+ *   - Ownership: the caller allocates and frees every buffer (pools, page
+ *     table, queries, outputs, workspace). The library allocates no device
+ *     memory. Pointers marked "device" are HIP device pointers, "host" are
+ *     ordinary host pointers; host arrays may be reused once the call returns.
+ *   - Streams: work is enqueued on the given stream (a hipStream_t; NULL is the
+ *     null stream) with no implicit synchronization, except where noted.
+ *   - Errors: every call returns a pkv_status. Argument and state errors that
+ *     the host can see are reported before anything is enqueued;
+ *     pkv_last_error() then holds a message (thread-local). Errors only the
+ *     device can see (for example, compressing a page that is not dense) set a
+ *     sticky per-device status word, read and cleared by pkv_device_status().
+ *   - Page-table entries, page kinds and eligible-page lists are integers and
+ *     are deterministic.
+ *   - Nothing here falls back to a CPU implementation.
+ */
+#ifndef PUZZLEKV_H
+#define PUZZLEKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef void *pkv_stream; /* hipStream_t */
+
+typedef enum {
+    PKV_OK = 0,
+    PKV_E_ARG = 1,         /* null pointer, bad enum value, negative count */
+    PKV_E_SHAPE = 2,       /* geometry inconsistent or out of the supported range */
+    PKV_E_RANK = 3,        /* rank 0 or above min(P, d, max_rank) */
+    PKV_E_STATE = 4,       /* page not in a state that allows the operation */
+    PKV_E_WORKSPACE = 5,   /* workspace pointer null or smaller than required */
+    PKV_E_UNSUPPORTED = 6, /* valid request that this build does not implement */
+    PKV_E_HIP = 7          /* HIP runtime error; pkv_last_error() has its text */
+} pkv_status;
+
+/* Element types. PKV_INT4 is a factor storage type only (reserved). */
+typedef enum { PKV_F32 = 0, PKV_BF16 = 1, PKV_INT4 = 2 } pkv_dtype;
+
+/* Kind of a logical page. */
+typedef enum { PKV_EMPTY = 0, PKV_DENSE = 1, PKV_FACTOR = 2 } pkv_kind;
+
+/* Device status bits (pkv_device_status). */
+#define PKV_DEV_NOT_DENSE     0x1u /* compress_pages found a page that is not dense   */
+#define PKV_DEV_BAD_PAGE      0x2u /* attention met an empty page below the length    */
+#define PKV_DEV_RING_OVERRUN  0x4u /* append would overwrite a page still dense       */
+#define PKV_DEV_NO_CONVERGE   0x8u /* a decomposition hit the sweep cap (result kept)  */
+#define PKV_DEV_BAD_RANK      0x10u /* prefill met a rank outside 1..max_rank (clamped) */
+
+/*
+ * Page-table entry, 8 bytes. slot is relative to the layer:
+ *   DENSE : index into the layer's dense slots
+ *           ((b * n_kv_heads + h) * dense_slots_per_head + ring position)
+ *   FACTOR: index into the layer's factor slots ((b * n_kv_heads + h) * max_pages + j)
+ * The page table is laid out [n_layers][batch][n_kv_heads][max_pages].
+ */
+typedef struct {
+    int32_t slot;
+    uint8_t kind;   /* pkv_kind */
+    uint8_t rank_k; /* factor pages: r_K, else 0 */
+    uint8_t rank_v; /* factor pages: r_V, else 0 */
+    uint8_t flags;  /* reserved, 0 */
+} pkv_page;
+
+/*
+ * Cache descriptor. Geometry plus three caller-owned device buffers whose
+ * sizes come from pkv_dense_pool_bytes / pkv_factor_pool_bytes /
+ * pkv_page_table_bytes.
+ *
+ * Dense pool: [n_layers][batch][n_kv_heads][dense_slots_per_head] slots of
+ * pkv_dense_slot_bytes. A slot holds K as P x d row-major, then V transposed
+ * (d x P row-major), both in dense_dtype. The first ceil(sink/P) slots of a
+ * head hold the sink pages; the rest form a ring of ceil(window/P) + 2 slots
+ * in which page j sits at position (j - sink_pages) mod ring length.
+ *
+ * Factor pool: [n_layers][batch][n_kv_heads][max_pages] slots of
+ * pkv_factor_slot_bytes (sized for max_rank). With e the factor element size
+ * and r4(x) = x rounded up to a multiple of 4, a slot holding ranks (rk, rv)
+ * stores, packed from its start:
+ *   A_K  = L_K          P  x r4(rk) row-major (columns >= rk are zero)
+ *   B_K  = R_K          rk x d      row-major
+ *   A_Vt = L_V^T        rv x P      row-major
+ *   B_Vt = R_V^T        d  x r4(rv) row-major (columns >= rv are zero)
+ * for e * (P r4(rk) + rk d + rv P + d r4(rv)) bytes (pkv_factor_page_bytes).
+ * Every operand is stored with its contraction index contiguous, the order
+ * the attention kernel streams it in.
+ */
+typedef struct {
+    int32_t n_layers;
+    int32_t batch;
+    int32_t n_kv_heads;
+    int32_t n_q_heads;     /* multiple of n_kv_heads; query head i reads KV head i / g */
+    int32_t head_dim;      /* d: multiple of 32, <= 256 */
+    int32_t page_size;     /* P: 16, 32 or 64 */
+    int32_t max_pages;     /* logical pages per (layer, b, kv head) */
+    int32_t max_rank;      /* 1 .. min(P, d) */
+    int32_t sink_tokens;   /* S >= 0 */
+    int32_t window_tokens; /* W >= 0 */
+    int32_t dense_dtype;   /* PKV_F32 or PKV_BF16 (also the query dtype) */
+    int32_t factor_dtype;  /* PKV_F32 or PKV_BF16 */
+    void *dense_pool;      /* device */
+    void *factor_pool;     /* device */
+    pkv_page *page_table;  /* device */
+} pkv_cache;
+
+/* ---- geometry and sizing (host only, no device work) -------------------- */
+
+/* Checks the descriptor's geometry and pointers. */
+pkv_status pkv_cache_check(const pkv_cache *c);
+int64_t pkv_dense_slots_per_head(const pkv_cache *c);
+size_t pkv_dense_slot_bytes(const pkv_cache *c);
+size_t pkv_factor_slot_bytes(const pkv_cache *c);
+size_t pkv_dense_pool_bytes(const pkv_cache *c);
+size_t pkv_factor_pool_bytes(const pkv_cache *c);
+size_t pkv_page_table_bytes(const pkv_cache *c);
+/* Bytes of one factor page pair at ranks (rk, rv): what attention reads for it. */
+size_t pkv_factor_page_bytes(const pkv_cache *c, int32_t rank_k, int32_t rank_v);
+
+/* Workspace sizes. op PKV_OP_ATTENTION: n = longest sequence length passed to
+ * pkv_mixed_decode_attention; PKV_OP_COMPRESS: n = pages per call;
+ * PKV_OP_PREFILL: n = longest prompt length. */
+enum { PKV_OP_ATTENTION = 0, PKV_OP_COMPRESS = 1, PKV_OP_PREFILL = 2, PKV_OP_IMPORT = 3 };
+size_t pkv_workspace_bytes(const pkv_cache *c, int32_t op, int64_t n);
+
+/* ---- page plan (host, integer; Section 3.3 and Section 4.1) ---------------
+ * Page j of a sequence of T tokens is FACTOR iff it is complete
+ * ((j+1) P <= T), outside the sink (j >= ceil(S / P)) and entirely older than
+ * the W-token window ((j+1) P <= T - W); pages holding a token but not
+ * factorized are DENSE; pages past the last token are EMPTY. With S = W = P
+ * this is the paper's default dense region: one sink page, the most recently
+ * completed page and the current incomplete page.
+ * pkv_plan_pages writes kind[0..n) and the page count ceil(T/P) to *n_pages.
+ * pkv_eligible_pages lists, ascending, the pages FACTOR at T_new but not at
+ * T_prev (at most cap of them; *count gets the full number). */
+pkv_status pkv_plan_pages(int64_t T, int32_t P, int32_t S, int32_t W, uint8_t *kind /*host*/,
+                          int64_t n, int64_t *n_pages);
+pkv_status pkv_eligible_pages(int64_t T_prev, int64_t T_new, int32_t P, int32_t S, int32_t W,
+                              int32_t *pages /*host*/, int64_t cap, int64_t *count);
+
+/* ---- cache construction and maintenance --------------------------------- */
+
+/* Marks every page of `layer` (all layers if layer < 0) EMPTY. */
+pkv_status pkv_cache_reset(const pkv_cache *c, int32_t layer, pkv_stream s);
+
+/* Builds one layer from the dense prompt cache (Section 3.3, steps 1-3 of the
+ * workflow: pages, dense sink/window, every other completed page factorized).
+ * k, v: device [batch][n_kv_heads][src_tokens][d] in dense_dtype.
+ * seq_len: host [batch], 0 <= seq_len[b] <= min(src_tokens, max_pages * P).
+ * rank_k, rank_v: device [batch][n_kv_heads][max_pages] ranks of factor pages,
+ * or NULL to use default_rank_k / default_rank_v for every page; a device rank
+ * outside 1..max_rank is clamped and raises PKV_DEV_BAD_RANK.
+ * Pages of the plan for seq_len[b] are written: dense pages copied, factor
+ * pages decomposed by the same kernel as pkv_compress_pages; pages past the
+ * sequence become EMPTY. Workspace: pkv_workspace_bytes(PKV_OP_PREFILL, max T). */
+pkv_status pkv_prefill(const pkv_cache *c, int32_t layer, const void *k, const void *v,
+                       int64_t src_tokens, const int32_t *seq_len, const uint8_t *rank_k,
+                       const uint8_t *rank_v, int32_t default_rank_k, int32_t default_rank_v,
+                       void *ws, size_t ws_bytes, pkv_stream s);
+
+/* Appends one token per sequence to `layer` (Section 3.3, "Incremental Cache
+ * Update": the new pair joins the most recent dense page).
+ * k_new, v_new: device [batch][n_kv_heads][d] in dense_dtype.
+ * pos: host [batch], the token index being written (the sequence length before
+ * the append); pos[b] < 0 skips sequence b. When pos[b] is a multiple of P a
+ * new dense page starts in the ring; if the ring position still holds a dense
+ * page the row is not written and PKV_DEV_RING_OVERRUN is raised. */
+pkv_status pkv_append_kv(const pkv_cache *c, int32_t layer, const void *k_new, const void *v_new,
+                         const int32_t *pos, pkv_stream s);
+
+/* Factorizes n dense pages of `layer` (Section 3.3: Gram matrix G = X X^T,
+ * L = its top-r eigenvectors, R = L^T X, which are the rank-r truncated-SVD
+ * factors of Eq. (2)); K and V of a page are decomposed independently.
+ * b, kv_head, page: host [n]; rank_k, rank_v: host [n], 1 <= r <= min(P, d,
+ * max_rank). Each page must be complete and DENSE; the entry becomes FACTOR
+ * with its ranks and its dense slot is free for reuse. A page found not dense
+ * is left untouched and PKV_DEV_NOT_DENSE is raised. Duplicate pages in one
+ * call are rejected (PKV_E_ARG). Workspace: pkv_workspace_bytes(PKV_OP_COMPRESS, n). */
+pkv_status pkv_compress_pages(const pkv_cache *c, int32_t layer, int32_t n, const int32_t *b,
+                              const int32_t *kv_head, const int32_t *page, const uint8_t *rank_k,
+                              const uint8_t *rank_v, void *ws, size_t ws_bytes, pkv_stream s);
+
+/* Single-query grouped-query decode attention over the mixed cache of `layer`
+ * (Eq. (4) per factor page, the same state from K and V on dense pages,
+ * merged by Eq. (5)); factor pages are never rebuilt into K or V.
+ * q: device [batch][n_q_heads][d] in dense_dtype. seq_len: host [batch], the
+ * tokens each sequence attends to (1 <= seq_len[b] <= max_pages * P; 0 gives
+ * out = 0 and lse = -inf). out: device fp32 [batch][n_q_heads][d], normalized.
+ * lse: device fp32 [batch][n_q_heads] log-sum-exp of the scaled scores, or NULL.
+ * Softmax scale 1/sqrt(d); query head i uses KV head i / (n_q_heads / n_kv_heads).
+ * Workspace: pkv_workspace_bytes(PKV_OP_ATTENTION, max seq_len) bytes holding
+ * per-chunk partial states and one counter per (sequence, KV head); it must be
+ * zero-filled before its first use, and every call leaves it ready for the
+ * next (the counters return to zero). Calls that share a workspace must not
+ * overlap. One kernel launch per call. */
+pkv_status pkv_mixed_decode_attention(const pkv_cache *c, int32_t layer, const void *q,
+                                      const int32_t *seq_len, float *out, float *lse, void *ws,
+                                      size_t ws_bytes, pkv_stream s);
+
+/* ---- import / export of pages in the logical layout ---------------------
+ * Logical page block, row-major:
+ *   DENSE : K (P x d), V (P x d)
+ *   FACTOR: L_K (P x rk), R_K (rk x d), L_V (P x rv), R_V (rv x d)
+ * pkv_import_pages writes n pages of `layer`: b, kv_head, page, kind, rank_k,
+ * rank_v, src_offset are host [n]; src is a device array in the destination
+ * dtype (dense_dtype for dense pages, factor_dtype for factor pages) and page
+ * i's block starts src_offset[i] elements into it. The page-table entry is set.
+ * Workspace: pkv_workspace_bytes(PKV_OP_IMPORT, n). */
+pkv_status pkv_import_pages(const pkv_cache *c, int32_t layer, int32_t n, const int32_t *b,
+                            const int32_t *kv_head, const int32_t *page, const uint8_t *kind,
+                            const uint8_t *rank_k, const uint8_t *rank_v, const void *src,
+                            const int64_t *src_offset, void *ws, size_t ws_bytes, pkv_stream s);
+
+/* pkv_export_pages reads n pages of `layer` as fp32 into dst (device), page i
+ * at dst + i * pkv_export_block_elems(c): DENSE as K, V (P x d each); FACTOR as
+ * L_K (P x max_rank), R_K (max_rank x d), L_V (P x max_rank), R_V (max_rank x d)
+ * with entries past the page's ranks zero; EMPTY as zeros. */
+int64_t pkv_export_block_elems(const pkv_cache *c);
+pkv_status pkv_export_pages(const pkv_cache *c, int32_t layer, int32_t n, const int32_t *b,
+                            const int32_t *kv_head, const int32_t *page, float *dst, void *ws,
+                            size_t ws_bytes, pkv_stream s);
+
+/* ---- diagnostics --------------------------------------------------------- */
+
+/* Synchronizes the stream, then returns (and clears) the current device's
+ * sticky status bits (PKV_DEV_*) in *bits. */
+pkv_status pkv_device_status(pkv_stream s, uint32_t *bits);
+/* Message of the last error on this thread ("" if none). */
+const char *pkv_last_error(void);
+const char *pkv_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PUZZLEKV_H */

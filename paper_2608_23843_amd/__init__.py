@@ -1,0 +1,224 @@
+"""PuzzleKV hot path on MI355X: Python binding of libpuzzlekv.so.
+
+Argument marshalling only. Every step of the path (page planning on the host,
+and on the device the decompositions, the append, the import / export copies
+and the mixed-page attention) runs inside the C ABI declared in
+include/puzzlekv.h. PyTorch supplies device memory and the current stream.
+If the library is not built the import fails; there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+
+import numpy as np
+
+from . import _lib
+from ._lib import (PKV_BF16, PKV_DENSE, PKV_EMPTY, PKV_F32, PKV_FACTOR, PKV_OP_ATTENTION,
+                   PKV_OP_COMPRESS, PKV_OP_IMPORT, PKV_OP_PREFILL, PuzzleKVError, check)
+
+__all__ = ["PuzzleKVCache", "plan_pages", "eligible_pages", "load_library", "PuzzleKVError",
+           "PKV_EMPTY", "PKV_DENSE", "PKV_FACTOR", "PKV_F32", "PKV_BF16"]
+
+_DTYPES = {"f32": PKV_F32, "fp32": PKV_F32, "float32": PKV_F32, "bf16": PKV_BF16, "bfloat16": PKV_BF16}
+
+
+def load_library():
+    return _lib.load()
+
+
+def _np_ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def plan_pages(T: int, P: int, S: int, W: int, n: int | None = None) -> np.ndarray:
+    """pkv_plan_pages: kind of each logical page (0 empty, 1 dense, 2 factor)."""
+    lib = _lib.load()
+    if n is None:
+        n = -(-T // P) if T > 0 else 0
+    kind = np.zeros(max(n, 1), dtype=np.uint8)
+    npg = ctypes.c_int64(0)
+    check(lib.pkv_plan_pages(T, P, S, W, _np_ptr(kind), n, ctypes.byref(npg)), "pkv_plan_pages")
+    return kind[:n]
+
+
+def eligible_pages(T_prev: int, T_new: int, P: int, S: int, W: int) -> np.ndarray:
+    """pkv_eligible_pages: pages that become factorized when T_prev grows to T_new."""
+    lib = _lib.load()
+    cap = max(1, -(-T_new // P))
+    out = np.zeros(cap, dtype=np.int32)
+    cnt = ctypes.c_int64(0)
+    check(lib.pkv_eligible_pages(T_prev, T_new, P, S, W, _np_ptr(out), cap, ctypes.byref(cnt)),
+          "pkv_eligible_pages")
+    return out[:cnt.value].copy()
+
+
+def _stream_handle(torch, stream=None):
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def _i32(x, n=None):
+    a = np.ascontiguousarray(np.asarray(x, dtype=np.int32).reshape(-1))
+    if n is not None and a.size != n:
+        raise ValueError("expected %d entries, got %d" % (n, a.size))
+    return a
+
+
+class PuzzleKVCache:
+    """A hybrid paged KV cache in device memory (pools allocated with torch).
+
+    Geometry follows pkv_cache: n_layers, batch, n_kv_heads, n_q_heads, head_dim
+    (d), page_size (P), max_pages per (layer, sequence, KV head), max_rank,
+    sink_tokens, window_tokens, dense and factor dtypes ("bf16" or "f32")."""
+
+    def __init__(self, n_layers, batch, n_kv_heads, n_q_heads, head_dim, page_size, max_pages,
+                 max_rank, sink_tokens, window_tokens, dense_dtype="bf16", factor_dtype="bf16",
+                 device="cuda"):
+        import torch
+        self.torch = torch
+        self.lib = _lib.load()
+        c = _lib.PkvCache()
+        c.n_layers, c.batch, c.n_kv_heads, c.n_q_heads = n_layers, batch, n_kv_heads, n_q_heads
+        c.head_dim, c.page_size, c.max_pages, c.max_rank = head_dim, page_size, max_pages, max_rank
+        c.sink_tokens, c.window_tokens = sink_tokens, window_tokens
+        c.dense_dtype, c.factor_dtype = _DTYPES[dense_dtype], _DTYPES[factor_dtype]
+        self.c = c
+        self.device = torch.device(device)
+        lib = self.lib
+        sizes = [lib.pkv_dense_pool_bytes(c), lib.pkv_factor_pool_bytes(c), lib.pkv_page_table_bytes(c)]
+        if 0 in sizes:
+            # report the geometry error the library found
+            check(lib.pkv_cache_check(ctypes.byref(c)), "PuzzleKVCache")
+        self.dense_pool = torch.empty(sizes[0], dtype=torch.uint8, device=self.device)
+        self.factor_pool = torch.empty(sizes[1], dtype=torch.uint8, device=self.device)
+        self.table = torch.empty(sizes[2], dtype=torch.uint8, device=self.device)
+        c.dense_pool = self.dense_pool.data_ptr()
+        c.factor_pool = self.factor_pool.data_ptr()
+        c.page_table = self.table.data_ptr()
+        check(lib.pkv_cache_check(ctypes.byref(c)), "PuzzleKVCache")
+        self.qdtype = torch.bfloat16 if c.dense_dtype == PKV_BF16 else torch.float32
+        self.fdtype = torch.bfloat16 if c.factor_dtype == PKV_BF16 else torch.float32
+        self.reset()
+
+    # ---- geometry ----------------------------------------------------------
+    @property
+    def group(self) -> int:
+        return self.c.n_q_heads // self.c.n_kv_heads
+
+    def factor_page_bytes(self, rank_k: int, rank_v: int) -> int:
+        return int(self.lib.pkv_factor_page_bytes(ctypes.byref(self.c), rank_k, rank_v))
+
+    def workspace_bytes(self, op: int, n: int) -> int:
+        return int(self.lib.pkv_workspace_bytes(ctypes.byref(self.c), op, n))
+
+    def workspace(self, op: int, n: int):
+        """A zero-filled workspace for `op` (see pkv_workspace_bytes)."""
+        nb = self.workspace_bytes(op, n)
+        return self.torch.zeros(max(nb, 1), dtype=self.torch.uint8, device=self.device)
+
+    def page_table(self, layer: int):
+        """Page-table entries of one layer as a (batch, n_kv_heads, max_pages, 8) uint8 tensor."""
+        c = self.c
+        per = c.batch * c.n_kv_heads * c.max_pages * 8
+        return self.table[layer * per:(layer + 1) * per].view(c.batch, c.n_kv_heads, c.max_pages, 8)
+
+    def page_table_host(self, layer: int):
+        """(slot int32, kind, rank_k, rank_v) numpy arrays of one layer."""
+        t = self.page_table(layer).cpu().numpy()
+        slot = t[..., :4].copy().view(np.int32)[..., 0]
+        return slot, t[..., 4].copy(), t[..., 5].copy(), t[..., 6].copy()
+
+    # ---- operations --------------------------------------------------------
+    def reset(self, layer: int = -1, stream=None):
+        check(self.lib.pkv_cache_reset(ctypes.byref(self.c), layer, _stream_handle(self.torch, stream)),
+              "pkv_cache_reset")
+
+    def prefill(self, layer, k, v, seq_len, rank_k=None, rank_v=None, default_rank=None, stream=None):
+        """k, v: device (batch, n_kv_heads, src_tokens, d). rank_k/rank_v: device uint8
+        (batch, n_kv_heads, max_pages) or None with default_rank=(r_k, r_v)."""
+        torch = self.torch
+        assert k.is_contiguous() and v.is_contiguous() and k.dtype == self.qdtype
+        seq = _i32(seq_len, self.c.batch)
+        if rank_k is None:
+            rk, rv = default_rank
+            pk = pv = None
+        else:
+            rk = rv = 0
+            for rt in (rank_k, rank_v):
+                assert rt.dtype == torch.uint8 and rt.is_contiguous() and rt.is_cuda
+                assert rt.numel() == self.c.batch * self.c.n_kv_heads * self.c.max_pages
+            pk, pv = rank_k.data_ptr(), rank_v.data_ptr()
+        check(self.lib.pkv_prefill(ctypes.byref(self.c), layer, k.data_ptr(), v.data_ptr(), k.shape[2],
+                                   _np_ptr(seq), pk, pv, rk, rv, None, 0,
+                                   _stream_handle(torch, stream)), "pkv_prefill")
+
+    def append(self, layer, k_new, v_new, pos, stream=None):
+        """k_new, v_new: device (batch, n_kv_heads, d); pos: host ints (token index per sequence)."""
+        assert k_new.is_contiguous() and v_new.is_contiguous() and k_new.dtype == self.qdtype
+        p = _i32(pos, self.c.batch)
+        check(self.lib.pkv_append_kv(ctypes.byref(self.c), layer, k_new.data_ptr(), v_new.data_ptr(),
+                                     _np_ptr(p), _stream_handle(self.torch, stream)), "pkv_append_kv")
+
+    def compress_pages(self, layer, b, h, page, rank_k, rank_v, stream=None):
+        b, h, page = _i32(b), _i32(h), _i32(page)
+        n = b.size
+        rk = np.ascontiguousarray(np.broadcast_to(np.asarray(rank_k, dtype=np.uint8), (n,)))
+        rv = np.ascontiguousarray(np.broadcast_to(np.asarray(rank_v, dtype=np.uint8), (n,)))
+        check(self.lib.pkv_compress_pages(ctypes.byref(self.c), layer, n, _np_ptr(b), _np_ptr(h),
+                                          _np_ptr(page), _np_ptr(rk), _np_ptr(rv), None, 0,
+                                          _stream_handle(self.torch, stream)), "pkv_compress_pages")
+
+    def attention(self, layer, q, seq_len, out=None, lse=None, workspace=None, stream=None):
+        """q: device (batch, n_q_heads, d) in the dense dtype. Returns (out, lse) fp32."""
+        torch = self.torch
+        c = self.c
+        assert q.is_contiguous() and q.dtype == self.qdtype and tuple(q.shape) == (c.batch, c.n_q_heads, c.head_dim)
+        seq = _i32(seq_len, c.batch)
+        if out is None:
+            out = torch.empty((c.batch, c.n_q_heads, c.head_dim), dtype=torch.float32, device=self.device)
+        if lse is None:
+            lse = torch.empty((c.batch, c.n_q_heads), dtype=torch.float32, device=self.device)
+        need = self.workspace_bytes(PKV_OP_ATTENTION, int(seq.max()) if seq.size else 0)
+        if workspace is None or workspace.numel() < need:
+            # zero-filled on first use (the merge counters live in it)
+            workspace = torch.zeros(max(need, 1), dtype=torch.uint8, device=self.device)
+        check(self.lib.pkv_mixed_decode_attention(ctypes.byref(c), layer, q.data_ptr(), _np_ptr(seq),
+                                                  out.data_ptr(), lse.data_ptr(), workspace.data_ptr(),
+                                                  workspace.numel(), _stream_handle(torch, stream)),
+              "pkv_mixed_decode_attention")
+        return out, lse
+
+    def import_pages(self, layer, b, h, page, kind, rank_k, rank_v, src, src_offset, stream=None):
+        """src: device 1-D tensor (dense dtype for dense pages, factor dtype for factors)."""
+        b, h, page = _i32(b), _i32(h), _i32(page)
+        n = b.size
+        kind = np.ascontiguousarray(np.asarray(kind, dtype=np.uint8).reshape(-1))
+        rk = np.ascontiguousarray(np.asarray(rank_k, dtype=np.uint8).reshape(-1))
+        rv = np.ascontiguousarray(np.asarray(rank_v, dtype=np.uint8).reshape(-1))
+        off = np.ascontiguousarray(np.asarray(src_offset, dtype=np.int64).reshape(-1))
+        assert src.is_contiguous() and kind.size == n and rk.size == n and rv.size == n and off.size == n
+        check(self.lib.pkv_import_pages(ctypes.byref(self.c), layer, n, _np_ptr(b), _np_ptr(h),
+                                        _np_ptr(page), _np_ptr(kind), _np_ptr(rk), _np_ptr(rv),
+                                        src.data_ptr(), _np_ptr(off), None, 0,
+                                        _stream_handle(self.torch, stream)), "pkv_import_pages")
+
+    def export_block_elems(self) -> int:
+        return int(self.lib.pkv_export_block_elems(ctypes.byref(self.c)))
+
+    def export_pages(self, layer, b, h, page, stream=None):
+        """Returns a device fp32 tensor (n, export_block_elems) of logical page blocks."""
+        torch = self.torch
+        b, h, page = _i32(b), _i32(h), _i32(page)
+        n = b.size
+        blk = self.export_block_elems()
+        dst = torch.empty((max(n, 1), blk), dtype=torch.float32, device=self.device)
+        check(self.lib.pkv_export_pages(ctypes.byref(self.c), layer, n, _np_ptr(b), _np_ptr(h),
+                                        _np_ptr(page), dst.data_ptr(), None, 0,
+                                        _stream_handle(torch, stream)), "pkv_export_pages")
+        return dst[:n]
+
+    def device_status(self, stream=None) -> int:
+        bits = ctypes.c_uint32(0)
+        check(self.lib.pkv_device_status(_stream_handle(self.torch, stream), ctypes.byref(bits)),
+              "pkv_device_status")
+        return int(bits.value)

@@ -1,0 +1,329 @@
+// Cache maintenance kernels: page-table reset, prefill of dense pages and
+// table entries, token append, page import / export, compress commit.
+// Included by pkv_kernels.hip (single device translation unit).
+
+namespace pkv {
+
+__device__ unsigned int g_status;
+__device__ inline void raise_status(unsigned int bits) { atomicOr(&g_status, bits); }
+
+hipError_t status_read_clear(unsigned int *bits) {
+    unsigned int zero = 0;
+    hipError_t e = hipMemcpyFromSymbol(bits, HIP_SYMBOL(g_status), sizeof(unsigned int), 0,
+                                       hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return e;
+    return hipMemcpyToSymbol(HIP_SYMBOL(g_status), &zero, sizeof(unsigned int), 0,
+                             hipMemcpyHostToDevice);
+}
+
+struct LayerPtrs {
+    pkv_page *table;  // this layer's entries
+    char *dense;      // this layer's dense slots
+    char *factor;     // this layer's factor slots
+};
+
+inline LayerPtrs layer_ptrs(const LaunchCtx &L) {
+    LayerPtrs p;
+    p.table = L.c->page_table + (int64_t)L.layer * L.geo.layer_entries;
+    p.dense = (char *)L.c->dense_pool + (int64_t)L.layer * L.geo.layer_dense_bytes;
+    p.factor = (char *)L.c->factor_pool + (int64_t)L.layer * L.geo.layer_factor_bytes;
+    return p;
+}
+
+__device__ inline void write_entry(pkv_page *e, int slot, int kind, int rk, int rv) {
+    pkv_page v;
+    v.slot = slot;
+    v.kind = (uint8_t)kind;
+    v.rank_k = (uint8_t)rk;
+    v.rank_v = (uint8_t)rv;
+    v.flags = 0;
+    *e = v;
+}
+
+// ---- reset ------------------------------------------------------------------
+
+__global__ void k_reset(pkv_page *table, int64_t n) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * blockDim.x)
+        write_entry(table + i, 0, PKV_EMPTY, 0, 0);
+}
+
+hipError_t launch_reset(const LaunchCtx &L, int64_t first_entry, int64_t n_entries) {
+    if (n_entries <= 0) return hipSuccess;
+    int blocks = (int)std::min<int64_t>(ceil_div(n_entries, 256), 4096);
+    hipLaunchKernelGGL(k_reset, dim3(blocks), dim3(256), 0, L.stream, L.c->page_table + first_entry,
+                       n_entries);
+    return hipGetLastError();
+}
+
+// ---- dense page copy: source rows (row-major) -> slot (K row-major, V^T) ----
+
+template <typename T>
+__device__ void copy_dense_page(const Geo &g, const T *srcK, const T *srcV, int64_t src_row_stride,
+                                int rows, T *slot) {
+    const int P = g.P, d = g.d;
+    T *K = slot;
+    T *Vt = slot + (int64_t)P * d;
+    for (int i = threadIdx.x; i < P * d; i += blockDim.x) {
+        int t = i / d, k = i % d;
+        K[i] = t < rows ? srcK[t * src_row_stride + k] : T(0);
+    }
+    for (int i = threadIdx.x; i < P * d; i += blockDim.x) {
+        int k = i / P, t = i % P;
+        Vt[i] = t < rows ? srcV[t * src_row_stride + k] : T(0);
+    }
+}
+
+// ---- prefill: table entries and dense pages --------------------------------
+
+template <typename TE>
+__global__ __launch_bounds__(256) void k_prefill_pages(Geo g, pkv_page *table, char *dense,
+                                                       const TE *k, const TE *v, int64_t src_tokens,
+                                                       SeqArgs seq, const uint8_t *rank_k,
+                                                       const uint8_t *rank_v, int def_rk, int def_rv) {
+    const int j = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
+    const int64_t T = seq.len[b];
+    const int64_t head = g.head_index(b, h);
+    pkv_page *e = table + head * g.max_pages + j;
+    const int kind = plan_kind(T, g.P, g.S, g.W, j);
+    if (kind == PKV_EMPTY) {
+        if (threadIdx.x == 0) write_entry(e, 0, PKV_EMPTY, 0, 0);
+        return;
+    }
+    if (kind == PKV_FACTOR) {
+        if (threadIdx.x == 0) {
+            const int rmax = min(g.max_rank, min(g.P, g.d));
+            int rk = def_rk, rv = def_rv;
+            if (rank_k) {
+                rk = rank_k[head * g.max_pages + j];
+                rv = rank_v[head * g.max_pages + j];
+                if (rk < 1 || rk > rmax || rv < 1 || rv > rmax) raise_status(PKV_DEV_BAD_RANK);
+                rk = max(1, min(rk, rmax));
+                rv = max(1, min(rv, rmax));
+            }
+            write_entry(e, (int)(head * g.max_pages + j), PKV_FACTOR, rk, rv);
+        }
+        return;
+    }
+    const int slot = (int)(head * g.dslots + g.dense_ring_slot(j));
+    const int64_t t0 = (int64_t)j * g.P;
+    const int rows = (int)min<int64_t>(g.P, T - t0);
+    const TE *sK = k + (head * src_tokens + t0) * g.d;
+    const TE *sV = v + (head * src_tokens + t0) * g.d;
+    copy_dense_page<TE>(g, sK, sV, g.d, rows, (TE *)(dense + slot * g.dense_slot_bytes));
+    if (threadIdx.x == 0) write_entry(e, slot, PKV_DENSE, 0, 0);
+}
+
+hipError_t launch_prefill_pages(const LaunchCtx &L, const void *k, const void *v, int64_t src_tokens,
+                                const SeqArgs &seq, const uint8_t *rank_k, const uint8_t *rank_v,
+                                int def_rk, int def_rv, int max_pages_in_batch) {
+    LayerPtrs p = layer_ptrs(L);
+    dim3 grid(max_pages_in_batch, L.geo.Hkv, L.geo.B);
+    if (L.geo.dense_dtype == PKV_BF16)
+        hipLaunchKernelGGL(k_prefill_pages<uint16_t>, grid, dim3(256), 0, L.stream, L.geo, p.table,
+                           p.dense, (const uint16_t *)k, (const uint16_t *)v, src_tokens, seq, rank_k,
+                           rank_v, def_rk, def_rv);
+    else
+        hipLaunchKernelGGL(k_prefill_pages<float>, grid, dim3(256), 0, L.stream, L.geo, p.table, p.dense,
+                           (const float *)k, (const float *)v, src_tokens, seq, rank_k, rank_v, def_rk,
+                           def_rv);
+    return hipGetLastError();
+}
+
+// ---- append ------------------------------------------------------------------
+
+template <typename T>
+__global__ void k_append(Geo g, pkv_page *table, char *dense, const T *k_new, const T *v_new,
+                         SeqArgs pos) {
+    const int h = blockIdx.x, b = blockIdx.y;
+    const int64_t p = pos.len[b];
+    if (p < 0) return;
+    const int64_t head = g.head_index(b, h);
+    const int j = (int)(p / g.P), row = (int)(p % g.P);
+    pkv_page *e = table + head * g.max_pages + j;
+    int slot;
+    if (row == 0) {
+        // a new page starts; its ring position must not hold a page still dense
+        const int jprev = j - g.ring_len;
+        if (j >= g.sink_pages && jprev >= g.sink_pages) {
+            pkv_page old = table[head * g.max_pages + jprev];
+            if (old.kind == PKV_DENSE) {
+                if (threadIdx.x == 0) raise_status(PKV_DEV_RING_OVERRUN);
+                return;
+            }
+        }
+        slot = (int)(head * g.dslots + g.dense_ring_slot(j));
+    } else {
+        pkv_page cur = *e;
+        if (cur.kind != PKV_DENSE) {
+            if (threadIdx.x == 0) raise_status(PKV_DEV_BAD_PAGE);
+            return;
+        }
+        slot = cur.slot;
+    }
+    T *K = (T *)(dense + slot * g.dense_slot_bytes);
+    T *Vt = K + (int64_t)g.P * g.d;
+    const T *kn = k_new + head * g.d;
+    const T *vn = v_new + head * g.d;
+    for (int i = threadIdx.x; i < g.d; i += blockDim.x) {
+        K[(int64_t)row * g.d + i] = kn[i];
+        Vt[(int64_t)i * g.P + row] = vn[i];
+    }
+    if (row == 0 && threadIdx.x == 0) write_entry(e, slot, PKV_DENSE, 0, 0);
+}
+
+hipError_t launch_append(const LaunchCtx &L, const void *k_new, const void *v_new, const SeqArgs &pos) {
+    LayerPtrs p = layer_ptrs(L);
+    dim3 grid(L.geo.Hkv, L.geo.B);
+    int threads = std::min(256, L.geo.d);
+    if (L.geo.dense_dtype == PKV_BF16)
+        hipLaunchKernelGGL(k_append<uint16_t>, grid, dim3(threads), 0, L.stream, L.geo, p.table, p.dense,
+                           (const uint16_t *)k_new, (const uint16_t *)v_new, pos);
+    else
+        hipLaunchKernelGGL(k_append<float>, grid, dim3(threads), 0, L.stream, L.geo, p.table, p.dense,
+                           (const float *)k_new, (const float *)v_new, pos);
+    return hipGetLastError();
+}
+
+// ---- compress commit: DENSE -> FACTOR entries after the decompositions ------
+
+__global__ void k_compress_commit(Geo g, pkv_page *table, CompressItems items) {
+    const int i = threadIdx.x + blockIdx.x * blockDim.x;
+    if (i >= items.n) return;
+    const CompressItem it = items.it[i];
+    const int64_t idx = g.head_index(it.b, it.h) * g.max_pages + it.j;
+    if (table[idx].kind == PKV_DENSE) write_entry(table + idx, (int)idx, PKV_FACTOR, it.rk, it.rv);
+}
+
+hipError_t launch_compress_commit(const LaunchCtx &L, const CompressItems &items) {
+    LayerPtrs p = layer_ptrs(L);
+    hipLaunchKernelGGL(k_compress_commit, dim3(1), dim3(128), 0, L.stream, L.geo, p.table, items);
+    return hipGetLastError();
+}
+
+// ---- import (logical layout -> slots) ---------------------------------------
+
+template <typename TD, typename TF>
+__global__ __launch_bounds__(256) void k_import(Geo g, pkv_page *table, char *dense, char *factor,
+                                                const char *src, CopyItems items) {
+    const CopyItem it = items.it[blockIdx.x];
+    const int64_t head = g.head_index(it.b, it.h);
+    pkv_page *e = table + head * g.max_pages + it.j;
+    const int P = g.P, d = g.d;
+    if (it.kind == PKV_DENSE) {
+        const TD *s = (const TD *)src + it.src_off;
+        const int slot = (int)(head * g.dslots + g.dense_ring_slot(it.j));
+        copy_dense_page<TD>(g, s, s + (int64_t)P * d, d, P, (TD *)(dense + slot * g.dense_slot_bytes));
+        if (threadIdx.x == 0) write_entry(e, slot, PKV_DENSE, 0, 0);
+        return;
+    }
+    const int rk = it.rk, rv = it.rv, rk4 = r4(rk), rv4 = r4(rv);
+    const TF *Lk = (const TF *)src + it.src_off;
+    const TF *Rk = Lk + (int64_t)P * rk;
+    const TF *Lv = Rk + (int64_t)rk * d;
+    const TF *Rv = Lv + (int64_t)P * rv;
+    const int slot = (int)(head * g.max_pages + it.j);
+    TF *Ak = (TF *)(factor + slot * g.factor_slot_bytes);
+    TF *Bk = Ak + (int64_t)P * rk4;
+    TF *Avt = Bk + (int64_t)rk * d;
+    TF *Bvt = Avt + (int64_t)rv * P;
+    for (int i = threadIdx.x; i < P * rk4; i += blockDim.x) {
+        int t = i / rk4, a = i % rk4;
+        Ak[i] = a < rk ? Lk[t * rk + a] : TF(0);
+    }
+    for (int i = threadIdx.x; i < rk * d; i += blockDim.x) Bk[i] = Rk[i];
+    for (int i = threadIdx.x; i < rv * P; i += blockDim.x) {
+        int a = i / P, t = i % P;
+        Avt[i] = Lv[t * rv + a];
+    }
+    for (int i = threadIdx.x; i < d * rv4; i += blockDim.x) {
+        int k = i / rv4, a = i % rv4;
+        Bvt[i] = a < rv ? Rv[(int64_t)a * d + k] : TF(0);
+    }
+    if (threadIdx.x == 0) write_entry(e, slot, PKV_FACTOR, rk, rv);
+}
+
+hipError_t launch_import(const LaunchCtx &L, const CopyItems &items, const void *src) {
+    LayerPtrs p = layer_ptrs(L);
+    dim3 grid(items.n);
+    const bool db = L.geo.dense_dtype == PKV_BF16, fb = L.geo.factor_dtype == PKV_BF16;
+    if (db && fb)
+        hipLaunchKernelGGL((k_import<uint16_t, uint16_t>), grid, dim3(256), 0, L.stream, L.geo, p.table,
+                           p.dense, p.factor, (const char *)src, items);
+    else if (db)
+        hipLaunchKernelGGL((k_import<uint16_t, float>), grid, dim3(256), 0, L.stream, L.geo, p.table,
+                           p.dense, p.factor, (const char *)src, items);
+    else if (fb)
+        hipLaunchKernelGGL((k_import<float, uint16_t>), grid, dim3(256), 0, L.stream, L.geo, p.table,
+                           p.dense, p.factor, (const char *)src, items);
+    else
+        hipLaunchKernelGGL((k_import<float, float>), grid, dim3(256), 0, L.stream, L.geo, p.table, p.dense,
+                           p.factor, (const char *)src, items);
+    return hipGetLastError();
+}
+
+// ---- export (slots -> logical fp32 blocks) ----------------------------------
+
+template <typename TD, typename TF>
+__global__ __launch_bounds__(256) void k_export(Geo g, const pkv_page *table, const char *dense,
+                                                const char *factor, float *dst, CopyItems items,
+                                                int64_t block) {
+    const CopyItem it = items.it[blockIdx.x];
+    const int64_t head = g.head_index(it.b, it.h);
+    const pkv_page e = table[head * g.max_pages + it.j];
+    float *o = dst + it.src_off;
+    const int P = g.P, d = g.d, R = g.max_rank;
+    if (e.kind == PKV_DENSE) {
+        const TD *K = (const TD *)(dense + e.slot * g.dense_slot_bytes);
+        const TD *Vt = K + (int64_t)P * d;
+        for (int i = threadIdx.x; i < P * d; i += blockDim.x) {
+            int t = i / d, k = i % d;
+            o[i] = ld(K, i);
+            o[P * d + i] = ld(Vt, (int64_t)k * P + t);
+        }
+        for (int i = 2 * P * d + threadIdx.x; i < block; i += blockDim.x) o[i] = 0.f;
+        return;
+    }
+    if (e.kind != PKV_FACTOR) {
+        for (int i = threadIdx.x; i < block; i += blockDim.x) o[i] = 0.f;
+        return;
+    }
+    const int rk = e.rank_k, rv = e.rank_v, rk4 = r4(rk), rv4 = r4(rv);
+    const TF *Ak = (const TF *)(factor + e.slot * g.factor_slot_bytes);
+    const TF *Bk = Ak + (int64_t)P * rk4;
+    const TF *Avt = Bk + (int64_t)rk * d;
+    const TF *Bvt = Avt + (int64_t)rv * P;
+    float *Lk = o, *Rk = Lk + P * R, *Lv = Rk + R * d, *Rv = Lv + P * R;
+    for (int i = threadIdx.x; i < P * R; i += blockDim.x) {
+        int t = i / R, a = i % R;
+        Lk[i] = a < rk ? ld(Ak, t * rk4 + a) : 0.f;
+        Lv[i] = a < rv ? ld(Avt, (int64_t)a * P + t) : 0.f;
+    }
+    for (int i = threadIdx.x; i < R * d; i += blockDim.x) {
+        int a = i / d, k = i % d;
+        Rk[i] = a < rk ? ld(Bk, i) : 0.f;
+        Rv[i] = a < rv ? ld(Bvt, (int64_t)k * rv4 + a) : 0.f;
+    }
+    for (int i = 2 * (P + d) * R + threadIdx.x; i < block; i += blockDim.x) o[i] = 0.f;
+}
+
+hipError_t launch_export(const LaunchCtx &L, const CopyItems &items, float *dst, int64_t block) {
+    LayerPtrs p = layer_ptrs(L);
+    dim3 grid(items.n);
+    const bool db = L.geo.dense_dtype == PKV_BF16, fb = L.geo.factor_dtype == PKV_BF16;
+    if (db && fb)
+        hipLaunchKernelGGL((k_export<uint16_t, uint16_t>), grid, dim3(256), 0, L.stream, L.geo, p.table,
+                           p.dense, p.factor, dst, items, block);
+    else if (db)
+        hipLaunchKernelGGL((k_export<uint16_t, float>), grid, dim3(256), 0, L.stream, L.geo, p.table,
+                           p.dense, p.factor, dst, items, block);
+    else if (fb)
+        hipLaunchKernelGGL((k_export<float, uint16_t>), grid, dim3(256), 0, L.stream, L.geo, p.table,
+                           p.dense, p.factor, dst, items, block);
+    else
+        hipLaunchKernelGGL((k_export<float, float>), grid, dim3(256), 0, L.stream, L.geo, p.table, p.dense,
+                           p.factor, dst, items, block);
+    return hipGetLastError();
+}
+
+}  // namespace pkv

@@ -1,0 +1,277 @@
+// Batched per-page truncated decomposition (Section 3.3: the Gram matrix
+// G = X X^T of a P x d page, its top-r eigenvectors L, and R = L^T X, which
+// equal the rank-r truncated-SVD factors of Eq. (2) because P < d).
+//
+// One wavefront handles 64 / P decompositions; inside a group of P lanes,
+// lane c owns column c of G and column c of the accumulated rotation J, both
+// in registers. The eigenvectors come from one-sided Jacobi on G: pairs of
+// columns are rotated until they are orthogonal, using the xor ordering
+// (step m pairs column c with column c ^ m, m = 1 .. P-1), so the partner is
+// always one lane-xor away and every pair meets once per sweep. At
+// convergence G J = J diag(lambda) and lambda_c = j_c . (G j_c).
+// Included by pkv_kernels.hip.
+
+namespace pkv {
+
+constexpr int kMaxSweeps = 32;
+
+enum { SRC_CACHE = 0, SRC_PREFILL = 1 };
+
+struct CompressSrc {
+    int mode;
+    const void *k, *v;        // prefill source [B][Hkv][src_tokens][d]
+    int64_t src_tokens;
+    SeqArgs off;              // prefill: item offset of sequence b (off.len[B] = total)
+    const uint8_t *rank_k, *rank_v;
+    int def_rk, def_rv;
+};
+
+__device__ inline float wave_shfl_xor(float v, int m) { return __shfl_xor(v, m, 64); }
+
+template <typename TX, typename TF, int P>
+__global__ __launch_bounds__(64) void k_compress(Geo g, pkv_page *table, const char *dense, char *factor,
+                                                 CompressItems items, CompressSrc src, int64_t n_decomp) {
+    constexpr int D = 64 / P;                           // decompositions per wave
+    constexpr int PAD = sizeof(TX) == 2 ? 2 : 1;        // one dword of row padding
+    extern __shared__ unsigned char smem_raw[];
+    const int d = g.d, ld_x = d + PAD;
+    TX *sX_all = (TX *)smem_raw;
+
+    const int lane = threadIdx.x;
+    const int grp = lane / P, c = lane % P;
+    const int64_t q = (int64_t)blockIdx.x * D + grp;    // decomposition index
+    TX *sX = sX_all + (int64_t)grp * P * ld_x;
+
+    // ---- which page, which half (K or V), ranks, source --------------------
+    bool active = q < n_decomp;
+    int b = 0, h = 0, j = 0, rk = 1, rv = 1;
+    const int which = (int)(q & 1);
+    const TX *X = nullptr;
+    bool transposed = false;
+    if (active) {
+        const int64_t item = q >> 1;
+        if (src.mode == SRC_CACHE) {
+            const CompressItem it = items.it[item];
+            b = it.b; h = it.h; j = it.j; rk = it.rk; rv = it.rv;
+            const pkv_page e = table[g.head_index(b, h) * g.max_pages + j];
+            if (e.kind != PKV_DENSE) {
+                if (c == 0) raise_status(PKV_DEV_NOT_DENSE);
+                active = false;
+            } else {
+                const TX *slot = (const TX *)(dense + e.slot * g.dense_slot_bytes);
+                X = which == 0 ? slot : slot + (int64_t)g.P * d;
+                transposed = which == 1;
+            }
+        } else {
+            int bb = 0;
+            while (bb + 1 < src.off.n - 1 && src.off.len[bb + 1] <= item) ++bb;
+            const int64_t local = item - src.off.len[bb];
+            const int64_t nf = (src.off.len[bb + 1] - src.off.len[bb]) / g.Hkv;
+            b = bb;
+            h = (int)(local / nf);
+            j = g.sink_pages + (int)(local % nf);
+            const int64_t head = g.head_index(b, h);
+            if (src.rank_k) {
+                const int rmax = min(g.max_rank, min(g.P, g.d));
+                rk = max(1, min((int)src.rank_k[head * g.max_pages + j], rmax));
+                rv = max(1, min((int)src.rank_v[head * g.max_pages + j], rmax));
+            } else {
+                rk = src.def_rk;
+                rv = src.def_rv;
+            }
+            const TX *base = (const TX *)(which == 0 ? src.k : src.v);
+            X = base + (head * src.src_tokens + (int64_t)j * P) * d;
+        }
+    }
+
+    // ---- stage X (P x d) in LDS -------------------------------------------
+    if (active) {
+        if (!transposed) {
+            for (int i = c; i < P * d; i += P) sX[(i / d) * ld_x + (i % d)] = X[i];
+        } else {
+            for (int i = c; i < P * d; i += P) {      // X[t][k] = Vt[k][t]
+                const int k = i / P, t = i % P;
+                sX[t * ld_x + k] = X[i];
+            }
+        }
+    }
+    __syncthreads();
+
+    // ---- Gram column c: G[k][c] = x_k . x_c ---------------------------------
+    float gcol[P], jcol[P];
+#pragma unroll
+    for (int k = 0; k < P; ++k) { gcol[k] = 0.f; jcol[k] = (k == c) ? 1.f : 0.f; }
+    if (active) {
+        for (int kk = 0; kk < d; ++kk) {
+            const float xc = to_f32(sX[c * ld_x + kk]);
+#pragma unroll
+            for (int k = 0; k < P; ++k) gcol[k] = fmaf(to_f32(sX[k * ld_x + kk]), xc, gcol[k]);
+        }
+    }
+
+    // ---- one-sided Jacobi on G ---------------------------------------------
+    float nrm2 = 0.f;
+#pragma unroll
+    for (int k = 0; k < P; ++k) nrm2 = fmaf(gcol[k], gcol[k], nrm2);
+    float fro2 = nrm2;
+    for (int m = 1; m < P; m <<= 1) fro2 += wave_shfl_xor(fro2, m);
+    const float tol = (float)P * 1.1920929e-7f;        // P * 2^-23
+    const float tiny2 = tol * tol * fro2;
+
+    int sweeps = 0;
+    bool more = true;
+    while (more && sweeps < kMaxSweeps) {
+        ++sweeps;
+        int rotated = 0;
+        for (int m = 1; m < P; ++m) {
+            float pg[P];
+            float alpha = 0.f, gamma = 0.f;
+#pragma unroll
+            for (int k = 0; k < P; ++k) {
+                pg[k] = wave_shfl_xor(gcol[k], m);
+                alpha = fmaf(gcol[k], gcol[k], alpha);
+                gamma = fmaf(gcol[k], pg[k], gamma);
+            }
+            const float beta = wave_shfl_xor(alpha, m);
+            const bool lo = c < (c ^ m);
+            const float a_lo = lo ? alpha : beta, a_hi = lo ? beta : alpha;
+            float cs = 1.f, sn = 0.f;
+            if (a_lo > tiny2 && a_hi > tiny2 && fabsf(gamma) > tol * sqrtf(a_lo * a_hi)) {
+                const float zeta = (a_hi - a_lo) / (2.f * gamma);
+                const float t = (zeta >= 0.f ? 1.f : -1.f) / (fabsf(zeta) + sqrtf(fmaf(zeta, zeta, 1.f)));
+                cs = 1.f / sqrtf(fmaf(t, t, 1.f));
+                sn = cs * t;
+                rotated = 1;
+            }
+            const float s_eff = lo ? -sn : sn;
+#pragma unroll
+            for (int k = 0; k < P; ++k) gcol[k] = fmaf(cs, gcol[k], s_eff * pg[k]);
+#pragma unroll
+            for (int k = 0; k < P; ++k) {
+                const float pj = wave_shfl_xor(jcol[k], m);
+                jcol[k] = fmaf(cs, jcol[k], s_eff * pj);
+            }
+        }
+        more = __any(rotated);
+    }
+    if (more && active && c == 0) raise_status(PKV_DEV_NO_CONVERGE);
+
+    // ---- eigenvalues, order (descending; ties keep the lower index) --------
+    // Rotations by tiny angles round cos to 1 and grow |j_c| slightly, so each
+    // eigenvector is renormalized; lambda_c is the Rayleigh quotient.
+    float jn2 = 0.f, lam = 0.f;
+#pragma unroll
+    for (int k = 0; k < P; ++k) {
+        jn2 = fmaf(jcol[k], jcol[k], jn2);
+        lam = fmaf(jcol[k], gcol[k], lam);
+    }
+    lam /= jn2;
+    const float jinv = 1.f / sqrtf(jn2);
+#pragma unroll
+    for (int k = 0; k < P; ++k) jcol[k] *= jinv;
+    int rho = 0;
+    const int base = grp * P;
+    for (int k = 0; k < P; ++k) {
+        const float lk = __shfl(lam, base + k, 64);
+        rho += (lk > lam) || (lk == lam && k < c);
+    }
+
+    if (!active) return;
+
+    // ---- outputs ------------------------------------------------------------
+    const int rk4 = r4(rk), rv4 = r4(rv);
+    TF *Ak = (TF *)(factor + (g.head_index(b, h) * g.max_pages + j) * g.factor_slot_bytes);
+    TF *Bk = Ak + (int64_t)P * rk4;
+    TF *Avt = Bk + (int64_t)rk * d;
+    TF *Bvt = Avt + (int64_t)rv * P;
+    const int r = which == 0 ? rk : rv;
+    const int rr4 = which == 0 ? rk4 : rv4;
+    if (which == 0) {
+        if (rho < rk4)
+            for (int t = 0; t < P; ++t) st(Ak, (int64_t)t * rk4 + rho, rho < rk ? jcol[t] : 0.f);
+    } else {
+        if (rho < rv)
+            for (int t = 0; t < P; ++t) st(Avt, (int64_t)rho * P + t, jcol[t]);
+    }
+    // R row rho = sum_t L[t][rho] X[t][:], in chunks of 16 columns
+    for (int k0 = 0; k0 < d; k0 += 16) {
+        float acc[16];
+#pragma unroll
+        for (int u = 0; u < 16; ++u) acc[u] = 0.f;
+        for (int t = 0; t < P; ++t) {
+            const float lt = jcol[t];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) acc[u] = fmaf(lt, to_f32(sX[t * ld_x + k0 + u]), acc[u]);
+        }
+        if (which == 0) {
+            if (rho < rk)
+#pragma unroll
+                for (int u = 0; u < 16; ++u) st(Bk, (int64_t)rho * d + k0 + u, acc[u]);
+        } else {
+            if (rho < rv4)
+#pragma unroll
+                for (int u = 0; u < 16; ++u) st(Bvt, (int64_t)(k0 + u) * rv4 + rho, rho < rv ? acc[u] : 0.f);
+        }
+    }
+    (void)r; (void)rr4;
+}
+
+template <typename TX, typename TF, int P>
+hipError_t launch_compress_t(const LaunchCtx &L, const CompressItems &items, const CompressSrc &src,
+                             int64_t n_decomp) {
+    constexpr int D = 64 / P;
+    const int pad = sizeof(TX) == 2 ? 2 : 1;
+    const size_t smem = (size_t)D * P * (L.geo.d + pad) * sizeof(TX);
+    const int64_t blocks = ceil_div(n_decomp, D);
+    LayerPtrs p = layer_ptrs(L);
+    hipLaunchKernelGGL((k_compress<TX, TF, P>), dim3((unsigned)blocks), dim3(64), smem, L.stream, L.geo,
+                       p.table, p.dense, p.factor, items, src, n_decomp);
+    return hipGetLastError();
+}
+
+template <typename TX, typename TF>
+hipError_t launch_compress_p(const LaunchCtx &L, const CompressItems &items, const CompressSrc &src,
+                             int64_t n_decomp) {
+    switch (L.geo.P) {
+    case 16: return launch_compress_t<TX, TF, 16>(L, items, src, n_decomp);
+    case 32: return launch_compress_t<TX, TF, 32>(L, items, src, n_decomp);
+    case 64: return launch_compress_t<TX, TF, 64>(L, items, src, n_decomp);
+    default: return hipErrorInvalidValue;
+    }
+}
+
+hipError_t launch_compress_any(const LaunchCtx &L, const CompressItems &items, const CompressSrc &src,
+                               int64_t n_decomp) {
+    if (n_decomp <= 0) return hipSuccess;
+    const bool db = L.geo.dense_dtype == PKV_BF16, fb = L.geo.factor_dtype == PKV_BF16;
+    if (db && fb) return launch_compress_p<uint16_t, uint16_t>(L, items, src, n_decomp);
+    if (db) return launch_compress_p<uint16_t, float>(L, items, src, n_decomp);
+    if (fb) return launch_compress_p<float, uint16_t>(L, items, src, n_decomp);
+    return launch_compress_p<float, float>(L, items, src, n_decomp);
+}
+
+hipError_t launch_compress(const LaunchCtx &L, const CompressItems &items) {
+    CompressSrc src{};
+    src.mode = SRC_CACHE;
+    return launch_compress_any(L, items, src, 2LL * items.n);
+}
+
+hipError_t launch_prefill_compress(const LaunchCtx &L, const void *k, const void *v, int64_t src_tokens,
+                                   const int32_t *item_offsets, int64_t n_items, const uint8_t *rank_k,
+                                   const uint8_t *rank_v, int def_rk, int def_rv) {
+    CompressItems items{};
+    CompressSrc src{};
+    src.mode = SRC_PREFILL;
+    src.k = k;
+    src.v = v;
+    src.src_tokens = src_tokens;
+    src.off.n = L.geo.B + 1;
+    for (int i = 0; i <= L.geo.B; ++i) src.off.len[i] = item_offsets[i];
+    src.rank_k = rank_k;
+    src.rank_v = rank_v;
+    src.def_rk = def_rk;
+    src.def_rv = def_rv;
+    return launch_compress_any(L, items, src, 2 * n_items);
+}
+
+}  // namespace pkv

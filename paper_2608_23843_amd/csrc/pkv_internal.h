@@ -1,0 +1,135 @@
+// Internal definitions shared by the host side and the kernels of the
+// PuzzleKV library (not part of the public ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "puzzlekv.h"
+
+namespace pkv {
+
+constexpr int kMaxBatchArgs = 256;   // sequences whose lengths travel in kernel arguments
+constexpr int kCompressItemsPerLaunch = 96;
+constexpr int kCopyItemsPerLaunch = 64;
+
+__host__ __device__ inline int r4(int r) { return (r + 3) & ~3; }
+__host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Elements of a packed factor page pair at ranks (rk, rv).
+__host__ __device__ inline int64_t factor_page_elems(int P, int d, int rk, int rv) {
+    return (int64_t)P * r4(rk) + (int64_t)rk * d + (int64_t)rv * P + (int64_t)d * r4(rv);
+}
+
+// Kind of logical page j of a sequence of T tokens (sink S, window W tokens).
+__host__ __device__ inline int plan_kind(int64_t T, int P, int S, int W, int64_t j) {
+    if (j < 0 || j * P >= T) return PKV_EMPTY;
+    const bool complete = (j + 1) * P <= T;
+    const bool in_sink = j < ceil_div(S, P);
+    const bool in_window = (j + 1) * P > T - W;
+    return (complete && !in_sink && !in_window) ? PKV_FACTOR : PKV_DENSE;
+}
+
+// Flattened geometry, passed to kernels by value.
+struct Geo {
+    int B, Hkv, Hq, g, d, P, max_pages, max_rank;
+    int S, W, sink_pages, ring_len, dslots;   // dslots = dense slots per head
+    int dense_es, factor_es;                  // element sizes in bytes
+    int dense_dtype, factor_dtype;
+    int64_t dense_slot_bytes, factor_slot_bytes;
+    // per-layer strides
+    int64_t layer_entries;       // page-table entries per layer
+    int64_t layer_dense_bytes;   // dense pool bytes per layer
+    int64_t layer_factor_bytes;  // factor pool bytes per layer
+
+    __host__ __device__ int dense_ring_slot(int j) const {
+        return j < sink_pages ? j : sink_pages + (j - sink_pages) % ring_len;
+    }
+    __host__ __device__ int64_t head_index(int b, int h) const { return (int64_t)b * Hkv + h; }
+};
+
+// bf16 <-> fp32 with round-to-nearest-even (NaN kept quiet).
+__host__ __device__ inline float bf16_to_f32(uint16_t v) {
+    union { uint32_t u; float f; } x;
+    x.u = (uint32_t)v << 16;
+    return x.f;
+}
+__host__ __device__ inline uint16_t f32_to_bf16(float f) {
+    union { uint32_t u; float f; } x;
+    x.f = f;
+    if ((x.u & 0x7f800000u) == 0x7f800000u && (x.u & 0x007fffffu)) return (uint16_t)((x.u >> 16) | 0x40);
+    uint32_t r = x.u + 0x7fffu + ((x.u >> 16) & 1u);
+    return (uint16_t)(r >> 16);
+}
+
+// Storage element access: float or bf16 (uint16_t).
+template <typename T> __device__ inline float ld(const T *p, int64_t i);
+template <> __device__ inline float ld<float>(const float *p, int64_t i) { return p[i]; }
+template <> __device__ inline float ld<uint16_t>(const uint16_t *p, int64_t i) { return bf16_to_f32(p[i]); }
+__device__ inline float to_f32(float x) { return x; }
+__device__ inline float to_f32(uint16_t x) { return bf16_to_f32(x); }
+template <typename T> __device__ inline void st(T *p, int64_t i, float v);
+template <> __device__ inline void st<float>(float *p, int64_t i, float v) { p[i] = v; }
+template <> __device__ inline void st<uint16_t>(uint16_t *p, int64_t i, float v) { p[i] = f32_to_bf16(v); }
+
+// Reads and clears the sticky device status word of the current device.
+hipError_t status_read_clear(unsigned int *bits);
+
+// ---- launchers (defined in the .hip files) --------------------------------
+
+struct LaunchCtx {
+    const pkv_cache *c;
+    Geo geo;
+    int layer;
+    hipStream_t stream;
+};
+
+// Compress work item (one logical page: K and V decompositions).
+struct CompressItem {
+    int32_t b, h, j;
+    uint8_t rk, rv, pad0, pad1;
+};
+struct CompressItems {
+    int32_t n;
+    CompressItem it[kCompressItemsPerLaunch];
+};
+
+struct CopyItem {
+    int32_t b, h, j;
+    uint8_t kind, rk, rv, pad;
+    int64_t src_off;
+};
+struct CopyItems {
+    int32_t n;
+    CopyItem it[kCopyItemsPerLaunch];
+};
+
+struct SeqArgs {
+    int32_t n;  // batch
+    int32_t len[kMaxBatchArgs];
+};
+
+hipError_t launch_reset(const LaunchCtx &L, int64_t first_entry, int64_t n_entries);
+hipError_t launch_prefill_pages(const LaunchCtx &L, const void *k, const void *v, int64_t src_tokens,
+                                const SeqArgs &seq, const uint8_t *rank_k, const uint8_t *rank_v,
+                                int def_rk, int def_rv, int max_pages_in_batch);
+hipError_t launch_prefill_compress(const LaunchCtx &L, const void *k, const void *v,
+                                   int64_t src_tokens, const int32_t *item_offsets, int64_t n_items,
+                                   const uint8_t *rank_k, const uint8_t *rank_v, int def_rk, int def_rv);
+hipError_t launch_append(const LaunchCtx &L, const void *k_new, const void *v_new, const SeqArgs &pos);
+hipError_t launch_compress(const LaunchCtx &L, const CompressItems &items);
+hipError_t launch_compress_commit(const LaunchCtx &L, const CompressItems &items);
+hipError_t launch_import(const LaunchCtx &L, const CopyItems &items, const void *src);
+hipError_t launch_export(const LaunchCtx &L, const CopyItems &items, float *dst, int64_t block);
+
+struct AttnPlan {
+    int pages_per_chunk;
+    int n_chunks;
+    int use_mfma;
+};
+AttnPlan attention_plan(const Geo &g, int64_t max_T);
+int64_t attention_workspace_bytes(const Geo &g, int64_t max_T);
+hipError_t launch_attention(const LaunchCtx &L, const AttnPlan &plan, const void *q, const SeqArgs &seq,
+                            float *out, float *lse, void *ws);
+
+}  // namespace pkv

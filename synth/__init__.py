@@ -21,7 +21,9 @@ SeedSequence([seed, workload_id, tag, ...])):
 """
 from __future__ import annotations
 
+import concurrent.futures
 import dataclasses
+import functools
 
 import numpy as np
 
@@ -106,23 +108,35 @@ def round_storage(x: np.ndarray, dtype: str) -> np.ndarray:
 # --------------------------------------------------------------------------
 # Keys, values, queries, ranks
 # --------------------------------------------------------------------------
-def _rope(x: np.ndarray, positions: np.ndarray, base: float) -> np.ndarray:
-    """Rotate-half RoPE of rows of x (n x d) at the given absolute positions."""
-    d = x.shape[-1]
+@functools.lru_cache(maxsize=8)
+def _rope_table(n: int, d: int, base: float):
+    """cos and sin (n x d/2, float32) of the rotate-half RoPE angles t * base^(-2i/d)."""
     half = d // 2
     inv = base ** (-np.arange(half, dtype=np.float64) * 2.0 / d)
-    ang = positions.astype(np.float64)[:, None] * inv[None, :]
-    c, s = np.cos(ang), np.sin(ang)
-    a = x[:, :half].astype(np.float64)
-    b = x[:, half:].astype(np.float64)
-    return np.concatenate([a * c - b * s, b * c + a * s], axis=1).astype(np.float32)
+    ang = np.arange(n, dtype=np.float64)[:, None] * inv[None, :]
+    return np.cos(ang).astype(np.float32), np.sin(ang).astype(np.float32)
+
+
+def _rope(x: np.ndarray, base: float) -> np.ndarray:
+    """Rotate-half RoPE of the rows of x (n x d) at positions 0 .. n-1."""
+    n, d = x.shape
+    half = d // 2
+    c, s = _rope_table(n, d, base)
+    a = x[:, :half]
+    b = x[:, half:]
+    out = np.empty_like(x)
+    out[:, :half] = a * c - b * s
+    out[:, half:] = b * c + a * s
+    return out
 
 
 def _low_rank_pages(g: np.random.Generator, n_pages: int, P: int, d: int, r0: int):
     G = g.standard_normal((n_pages, P, r0), dtype=np.float32)
     W = g.standard_normal((n_pages, r0, d), dtype=np.float32)
     N = g.standard_normal((n_pages, P, d), dtype=np.float32)
-    return (np.matmul(G, W) + np.float32(0.05) * N).reshape(n_pages * P, d)
+    N *= np.float32(0.05)
+    N += np.matmul(G, W)
+    return N.reshape(n_pages * P, d)
 
 
 def outlier_channels(wl: Workload, seed: int, layer: int, h: int) -> np.ndarray:
@@ -143,18 +157,29 @@ def kv_head(wl: Workload, seed: int, layer: int, b: int, h: int, tokens: int | N
     if ch.size:
         K[:, ch] *= np.float32(10.0)
     if wl.rope_base is not None:
-        K = _rope(K, np.arange(n_pages * P), wl.rope_base)
+        K = _rope(K, wl.rope_base)
     return round_storage(K[:T], wl.dtype), round_storage(V[:T], wl.dtype)
 
 
-def kv_layer(wl: Workload, seed: int, layer: int, tokens: int | None = None):
-    """K, V of a whole layer: (batch, kv_heads, tokens, d) float32."""
+def kv_layer(wl: Workload, seed: int, layer: int, tokens: int | None = None, workers: int = 0):
+    """K, V of a whole layer: (batch, kv_heads, tokens, d) float32. Heads are
+    independent streams, drawn in parallel threads when workers > 1 (the
+    result does not depend on the thread count)."""
     T = wl.tokens + wl.decode_steps if tokens is None else int(tokens)
     K = np.empty((wl.batch, wl.kv_heads, T, wl.head_dim), dtype=np.float32)
     V = np.empty_like(K)
-    for b in range(wl.batch):
-        for h in range(wl.kv_heads):
-            K[b, h], V[b, h] = kv_head(wl, seed, layer, b, h, T)
+
+    def one(bh):
+        b, h = bh
+        K[b, h], V[b, h] = kv_head(wl, seed, layer, b, h, T)
+
+    heads = [(b, h) for b in range(wl.batch) for h in range(wl.kv_heads)]
+    if workers and workers > 1:
+        with concurrent.futures.ThreadPoolExecutor(workers) as ex:
+            list(ex.map(one, heads))
+    else:
+        for bh in heads:
+            one(bh)
     return K, V
 
 
@@ -195,3 +220,29 @@ def factor_page(wl: Workload, seed: int, layer: int, b: int, h: int, j: int, r_k
         R = g.standard_normal((r, d)) * np.sqrt(wl.r0 * P / r)
         out += [round_storage(L, wl.dtype), round_storage(R, wl.dtype)]
     return tuple(out)
+
+
+def decode_kv(wl: Workload, seed: int, layer: int, pos: int):
+    """K and V rows (batch, kv_heads, d) for the token at position pos, drawn
+    from the same page model as the prefill pages but from their own stream
+    (one stream per decode position), with the key outliers and RoPE at pos."""
+    P, d = wl.page, wl.head_dim
+    K = np.empty((wl.batch, wl.kv_heads, d), dtype=np.float32)
+    V = np.empty_like(K)
+    for b in range(wl.batch):
+        g = rng(seed, wl.wid, TAG_TOKEN, layer, pos, b)
+        for h in range(wl.kv_heads):
+            for X in (K, V):
+                x = g.standard_normal(wl.r0) @ g.standard_normal((wl.r0, d)) + 0.05 * g.standard_normal(d)
+                X[b, h] = x
+            ch = outlier_channels(wl, seed, layer, h)
+            if ch.size:
+                K[b, h, ch] *= 10.0
+    if wl.rope_base is not None:
+        half = d // 2
+        inv = wl.rope_base ** (-np.arange(half, dtype=np.float64) * 2.0 / d)
+        c, s = np.cos(pos * inv), np.sin(pos * inv)
+        a, bb = K[..., :half].copy(), K[..., half:].copy()
+        K[..., :half] = a * c - bb * s
+        K[..., half:] = bb * c + a * s
+    return round_storage(K, wl.dtype), round_storage(V, wl.dtype)

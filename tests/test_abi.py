@@ -1,0 +1,137 @@
+"""CPU checks of the C ABI: the library loads without a GPU, exports every
+symbol include/puzzlekv.h declares, its integer page planner matches the
+oracle bit for bit, its sizing follows the documented layout, and argument
+errors are reported before anything is enqueued (no device work here)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import accounting
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def pk():
+    import paper_2608_23843_amd as pk
+    pk.load_library()
+    return pk
+
+
+def _header_functions():
+    src = open(os.path.join(ROOT, "include", "puzzlekv.h")).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(pkv_[a-z_]+)\s*\(", src)))
+
+
+def test_exports_every_declared_symbol(pk):
+    from paper_2608_23843_amd import _lib
+    declared = _header_functions()
+    assert declared == sorted(_lib.EXPORTS)
+    lib = pk.load_library()
+    for name in declared:
+        assert hasattr(lib, name), name
+    assert b"gfx950" in lib.pkv_version()
+
+
+@pytest.mark.parametrize("P,S,W", [(16, 16, 32), (16, 0, 0), (32, 32, 32), (64, 64, 256), (64, 64, 512),
+                                   (16, 40, 20)])
+def test_planner_bit_exact_vs_oracle(pk, P, S, W):
+    for T in list(range(0, 6 * P + 3)) + [32768, 131072, 131073]:
+        n = -(-T // P) + 2
+        assert np.array_equal(pk.plan_pages(T, P, S, W, n), oracle.plan_pages(T, P, S, W, n)), T
+    for T in range(1, 12 * P):
+        assert np.array_equal(pk.eligible_pages(T - 1, T, P, S, W), oracle.eligible_pages(T - 1, T, P, S, W))
+    assert np.array_equal(pk.eligible_pages(100, 5000, P, S, W), oracle.eligible_pages(100, 5000, P, S, W))
+
+
+def test_workload_page_counts(pk):
+    # Qwen3-32B shape at 128K: pages 1..2039 factorized, 0 and 2040..2047 dense
+    kind = pk.plan_pages(131072, 64, 64, 512)
+    assert int((kind == 2).sum()) == 2039 and list(np.nonzero(kind == 1)[0]) == [0] + list(range(2040, 2048))
+    # Llama-3-8B shape at 32K with a 256-token window: 507 factor pages
+    assert int((pk.plan_pages(32768, 64, 64, 256) == 2).sum()) == 507
+
+
+def _cache(pk, **kw):
+    from paper_2608_23843_amd import _lib
+    c = _lib.PkvCache()
+    geo = dict(n_layers=2, batch=2, n_kv_heads=2, n_q_heads=8, head_dim=128, page_size=64, max_pages=8,
+               max_rank=32, sink_tokens=64, window_tokens=256, dense_dtype=1, factor_dtype=1)
+    geo.update(kw)
+    for k, v in geo.items():
+        setattr(c, k, v)
+    return c
+
+
+def test_sizing_follows_layout(pk):
+    lib = pk.load_library()
+    c = _cache(pk)
+    P, d = 64, 128
+    for rk, rv in [(16, 16), (24, 24), (32, 32), (14, 16), (1, 3)]:
+        r4 = lambda r: (r + 3) // 4 * 4
+        assert lib.pkv_factor_page_bytes(c, rk, rv) == 2 * (P * r4(rk) + rk * d + rv * P + d * r4(rv))
+    # rank multiple of 4: exactly the Eq. (3) storage of the factor pair
+    for r in (16, 24, 32):
+        ratio = lib.pkv_factor_page_bytes(c, r, r) / (2 * P * d * 2)
+        assert abs(ratio - accounting.page_storage_ratio(P, r, r, d)) < 1e-12
+    assert lib.pkv_dense_slot_bytes(c) == 2 * P * d * 2
+    assert lib.pkv_dense_slots_per_head(c) == 1 + 256 // 64 + 2
+    assert lib.pkv_factor_slot_bytes(c) % 256 == 0
+    assert lib.pkv_factor_slot_bytes(c) >= lib.pkv_factor_page_bytes(c, 32, 32)
+    assert lib.pkv_page_table_bytes(c) == 2 * 2 * 2 * 8 * 8
+    assert lib.pkv_dense_pool_bytes(c) == 2 * 2 * 2 * 7 * 2 * P * d * 2
+    assert lib.pkv_export_block_elems(c) == max(2 * P * d, 2 * (P + d) * 32)
+    assert lib.pkv_workspace_bytes(c, 0, 8 * 64) > 0
+
+
+@pytest.mark.parametrize("kw,code", [(dict(page_size=48), 2), (dict(head_dim=100), 2), (dict(max_rank=0), 3),
+                                     (dict(max_rank=65), 3), (dict(n_q_heads=7), 2), (dict(dense_dtype=5), 6),
+                                     (dict(batch=0), 2), (dict(sink_tokens=-1), 2)])
+def test_geometry_errors(pk, kw, code):
+    lib = pk.load_library()
+    c = _cache(pk, **kw)
+    c.dense_pool = c.factor_pool = c.page_table = 0x1000
+    assert lib.pkv_cache_check(c) == code
+    assert lib.pkv_last_error()
+
+
+def test_call_errors_before_any_launch(pk):
+    """Every call below fails host-side validation, so no kernel is launched on
+    the fake (never dereferenced) pool pointers."""
+    lib = pk.load_library()
+    c = _cache(pk)
+    c.dense_pool = c.factor_pool = c.page_table = 0x1000
+    vp = ctypes.c_void_p
+    i32 = lambda *v: np.array(v, dtype=np.int32)
+    u8 = lambda *v: np.array(v, dtype=np.uint8)
+    P = lambda a: a.ctypes.data_as(vp)
+    seq = i32(128, 128)
+    # attention: no workspace / too small / length beyond the table / bad layer
+    assert lib.pkv_mixed_decode_attention(c, 0, vp(0x2000), P(seq), vp(0x3000), None, None, 0, None) == 5
+    assert lib.pkv_mixed_decode_attention(c, 0, vp(0x2000), P(seq), vp(0x3000), None, vp(0x4000), 1, None) == 5
+    assert lib.pkv_mixed_decode_attention(c, 0, vp(0x2000), P(i32(8 * 64 + 1, 1)), vp(0x3000), None,
+                                          vp(0x4000), 1 << 30, None) == 2
+    assert lib.pkv_mixed_decode_attention(c, 2, vp(0x2000), P(seq), vp(0x3000), None, vp(0x4000), 1 << 30,
+                                          None) == 1
+    # compress: rank 0, rank above max, duplicate page, page out of range
+    b, h, j = i32(0, 1), i32(0, 1), i32(2, 3)
+    assert lib.pkv_compress_pages(c, 0, 2, P(b), P(h), P(j), P(u8(0, 4)), P(u8(4, 4)), None, 0, None) == 3
+    assert lib.pkv_compress_pages(c, 0, 2, P(b), P(h), P(j), P(u8(33, 4)), P(u8(4, 4)), None, 0, None) == 3
+    assert lib.pkv_compress_pages(c, 0, 2, P(i32(0, 0)), P(i32(1, 1)), P(i32(3, 3)), P(u8(4, 4)),
+                                  P(u8(4, 4)), None, 0, None) == 1
+    assert lib.pkv_compress_pages(c, 0, 2, P(b), P(h), P(i32(2, 8)), P(u8(4, 4)), P(u8(4, 4)), None, 0,
+                                  None) == 1
+    # append beyond the table; prefill with a length beyond the source
+    assert lib.pkv_append_kv(c, 0, vp(0x2000), vp(0x2000), P(i32(8 * 64, 0)), None) == 2
+    assert lib.pkv_prefill(c, 0, vp(0x2000), vp(0x2000), 100, P(i32(101, 5)), None, None, 4, 4, None, 0,
+                           None) == 2
+    assert lib.pkv_prefill(c, 0, vp(0x2000), vp(0x2000), 100, P(i32(50, 5)), None, None, 0, 4, None, 0,
+                           None) == 3
+    # import: bad kind
+    assert lib.pkv_import_pages(c, 0, 1, P(i32(0)), P(i32(0)), P(i32(0)), P(u8(7)), P(u8(0)), P(u8(0)),
+                                vp(0x2000), P(np.zeros(1, dtype=np.int64)), None, 0, None) == 1

@@ -1,0 +1,222 @@
+"""GPU parity of the page decomposition (pkv_prefill / pkv_compress_pages)
+against the oracle's one-sided Jacobi SVD, through the C ABI.
+
+The truncated SVD is unique only up to signs, rotations inside repeated
+singular values and ties at the cut, so the comparison uses sign-invariant
+quantities on the exported factors: the singular values sigma_i = |R_i|
+(Gram identity: R = L^T X has row norms sigma_i), the rank-r product L R
+against the oracle's X_r where the spectrum has a gap at r, orthonormality of
+L, and the Eckart-Young truncation error. Page-table entries are integers
+and must match the plan bit for bit."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from helpers import storage_round
+
+pytestmark = pytest.mark.gpu
+
+
+def _prefill_case(B, Hkv, d, P, T, S, W, rank, dense_dtype, factor_dtype, r0, seed=0, rope=None,
+                  outliers=0, rank_table=None):
+    import torch
+    import paper_2608_23843_amd as pk
+    max_pages = -(-T // P)
+    wl = synth.Workload("c", 91, B, Hkv, Hkv, d, P, T, S, W, r0, (rank,), dense_dtype, rope, outliers)
+    K, V = synth.kv_layer(wl, seed, 0, T)
+    max_rank = rank if rank_table is None else int(rank_table.max())
+    cache = pk.PuzzleKVCache(1, B, Hkv, Hkv, d, P, max_pages, max_rank, S, W, dense_dtype, factor_dtype)
+    kt = torch.from_numpy(K).to(device="cuda", dtype=cache.qdtype).contiguous()
+    vt = torch.from_numpy(V).to(device="cuda", dtype=cache.qdtype).contiguous()
+    if rank_table is None:
+        cache.prefill(0, kt, vt, [T] * B, default_rank=(rank, rank))
+    else:
+        rt = torch.from_numpy(rank_table.astype(np.uint8)).cuda().contiguous()
+        cache.prefill(0, kt, vt, [T] * B, rank_k=rt, rank_v=rt)
+    torch.cuda.synchronize()
+    return cache, K, V, max_pages
+
+
+def _export(cache, refs):
+    b, h, j = zip(*refs)
+    return cache.export_pages(0, list(b), list(h), list(j)).cpu().numpy().astype(np.float64)
+
+
+def _unpack_factor(blk, P, d, R):
+    Lk = blk[:P * R].reshape(P, R)
+    Rk = blk[P * R:P * R + R * d].reshape(R, d)
+    Lv = blk[P * R + R * d:2 * P * R + R * d].reshape(P, R)
+    Rv = blk[2 * P * R + R * d:2 * P * R + 2 * R * d].reshape(R, d)
+    return Lk, Rk, Lv, Rv
+
+
+def _check_factor(L, R, X, r, gap_tol, orth_tol, sig_tol):
+    """L (P x r), R (r x d) from the GPU, X the stored page (fp64).
+
+    sig_tol is the relative storage rounding of a factor entry: a row norm of
+    R moves by at most that fraction when R is stored (2^-8 for bf16, whose
+    unit roundoff is 2^-8; ~0 for fp32). On top of it the fp32 Gram gives
+    eigenvalues to about 1e-5 |G| = 1e-5 s_1^2."""
+    _, s, _, _ = oracle.svd_rows(X)
+    sig_gpu = np.linalg.norm(R, axis=1)
+    bound = sig_tol * s[:r] + 1e-5 * s[0] ** 2 / np.maximum(s[:r], 1e-30) + 1e-6 * s[0]
+    assert np.all(np.abs(sig_gpu - s[:r]) <= bound), (sig_gpu[:4], s[:4])
+    assert np.abs(L.T @ L - np.eye(r)).max() <= orth_tol
+    tail = np.sqrt(np.sum(s[r:] ** 2))
+    err = np.linalg.norm(X - L @ R)
+    assert err <= (1 + 1e-3) * tail + gap_tol * np.linalg.norm(X), (err, tail)
+    if r < len(s) and s[r] < 0.5 * s[r - 1]:
+        Lo, Ro, _, _ = oracle.truncated_factors(X, r)
+        Xr = Lo @ Ro
+        assert np.linalg.norm(L @ R - Xr) <= gap_tol * np.linalg.norm(Xr) + 1e-3 * tail
+
+
+@pytest.mark.parametrize("factor_dtype,gap_tol,orth_tol,sig_tol",
+                         [("f32", 1e-4, 1e-4, 1e-5), ("bf16", 6e-3, 1e-2, 4e-3)])
+def test_prefill_llama_pages(factor_dtype, gap_tol, orth_tol, sig_tol):
+    """Llama-3-8B page geometry (P=64, d=128, r=24 on rank-24 + noise pages)."""
+    B, Hkv, d, P, S, W, r = 1, 2, 128, 64, 64, 256, 24
+    T = 64 * 12 + 20
+    cache, K, V, npg = _prefill_case(B, Hkv, d, P, T, S, W, r, "bf16", factor_dtype, 24, rope=5e5,
+                                     outliers=4)
+    assert cache.device_status() == 0
+    kind = oracle.plan_pages(T, P, S, W, npg)
+    refs = [(0, h, j) for h in range(Hkv) for j in range(npg) if kind[j] == oracle.FACTOR]
+    blocks = _export(cache, refs)
+    R = cache.c.max_rank
+    for (b, h, j), blk in zip(refs, blocks):
+        Lk, Rk, Lv, Rv = _unpack_factor(blk, P, d, R)
+        for L, Rm, X in ((Lk, Rk, K[b, h, j * P:(j + 1) * P]), (Lv, Rv, V[b, h, j * P:(j + 1) * P])):
+            _check_factor(L[:, :r], Rm[:r], X.astype(np.float64), r, gap_tol, orth_tol, sig_tol)
+            assert np.all(L[:, r:] == 0) and np.all(Rm[r:] == 0)
+
+
+def test_prefill_page_table_and_dense_pages_bit_exact():
+    B, Hkv, d, P, S, W, r = 2, 2, 64, 16, 16, 48, 4
+    T = 16 * 10 + 7
+    cache, K, V, npg = _prefill_case(B, Hkv, d, P, T, S, W, r, "bf16", "bf16", 4)
+    slot, kind, rk, rv = cache.page_table_host(0)
+    plan = oracle.plan_pages(T, P, S, W, npg)
+    sink_pages = -(-S // P)
+    ring = -(-W // P) + 2
+    dslots = sink_pages + ring
+    for b in range(B):
+        for h in range(Hkv):
+            assert np.array_equal(kind[b, h], plan)
+            for j in range(npg):
+                head = b * Hkv + h
+                if plan[j] == oracle.FACTOR:
+                    assert (slot[b, h, j], rk[b, h, j], rv[b, h, j]) == (head * npg + j, r, r)
+                else:
+                    ring_pos = j if j < sink_pages else sink_pages + (j - sink_pages) % ring
+                    assert (slot[b, h, j], rk[b, h, j], rv[b, h, j]) == (head * dslots + ring_pos, 0, 0)
+    refs = [(b, h, j) for b in range(B) for h in range(Hkv) for j in range(npg) if plan[j] == oracle.DENSE]
+    blocks = _export(cache, refs)
+    for (b, h, j), blk in zip(refs, blocks):
+        rows = min(P, T - j * P)
+        Kp = blk[:P * d].reshape(P, d)
+        Vp = blk[P * d:2 * P * d].reshape(P, d)
+        assert np.array_equal(Kp[:rows], K[b, h, j * P:j * P + rows])
+        assert np.array_equal(Vp[:rows], V[b, h, j * P:j * P + rows])
+        assert np.all(Kp[rows:] == 0) and np.all(Vp[rows:] == 0)
+
+
+@pytest.mark.parametrize("P", [16, 32])
+def test_prefill_small_pages_variable_ranks_fp32(P):
+    """Several decompositions per wavefront (P < 64), fp32 pages and factors,
+    per-page ranks including rank 1 and full rank P."""
+    B, Hkv, d, S, W = 1, 2, 64, P, P
+    T = P * 9
+    npg = 9
+    rng = np.random.default_rng(5)
+    table = rng.choice([1, 3, P // 2, P], size=(B, Hkv, npg))
+    cache, K, V, npg = _prefill_case(B, Hkv, d, P, T, S, W, 0, "f32", "f32", P // 2, rank_table=table)
+    assert cache.device_status() == 0
+    kind = oracle.plan_pages(T, P, S, W, npg)
+    refs = [(0, h, j) for h in range(Hkv) for j in range(npg) if kind[j] == oracle.FACTOR]
+    blocks = _export(cache, refs)
+    R = cache.c.max_rank
+    for (b, h, j), blk in zip(refs, blocks):
+        r = int(table[b, h, j])
+        Lk, Rk, Lv, Rv = _unpack_factor(blk, P, d, R)
+        for L, Rm, X in ((Lk, Rk, K[b, h, j * P:(j + 1) * P]), (Lv, Rv, V[b, h, j * P:(j + 1) * P])):
+            _check_factor(L[:, :r], Rm[:r], X.astype(np.float64), r, 1e-4, 1e-4, 1e-5)
+            if r == P:
+                assert np.abs(L[:, :r] @ Rm[:r] - X).max() <= 1e-5 * np.abs(X).max()
+
+
+def test_incremental_compress_and_state_errors():
+    """Append tokens one by one until a page leaves the window, compress it with
+    pkv_compress_pages, and compare with the oracle; compressing it again
+    raises the not-dense device bit and leaves the entry unchanged."""
+    import torch
+    import paper_2608_23843_amd as pk
+    B, Hkv, d, P, S, W, r = 2, 2, 128, 64, 64, 128, 24
+    T0, steps = 64 * 4 + 60, 40
+    wl = synth.Workload("c", 92, B, Hkv, Hkv, d, P, T0, S, W, 24, (r,), "bf16", 5e5, 4,
+                        decode_steps=steps)
+    K, V = synth.kv_layer(wl, 0, 0)
+    max_pages = -(-(T0 + steps) // P)
+    cache = pk.PuzzleKVCache(1, B, Hkv, Hkv, d, P, max_pages, 32, S, W, "bf16", "bf16")
+    kt = torch.from_numpy(K[:, :, :T0]).to("cuda", torch.bfloat16).contiguous()
+    vt = torch.from_numpy(V[:, :, :T0]).to("cuda", torch.bfloat16).contiguous()
+    cache.prefill(0, kt, vt, [T0] * B, default_rank=(r, r))
+    converted = []
+    for t in range(T0, T0 + steps):
+        kn = torch.from_numpy(K[:, :, t]).to("cuda", torch.bfloat16).contiguous()
+        vn = torch.from_numpy(V[:, :, t]).to("cuda", torch.bfloat16).contiguous()
+        cache.append(0, kn, vn, [t] * B)
+        new = oracle.eligible_pages(t, t + 1, P, S, W)
+        for j in new:
+            refs = [(b, h, int(j)) for b in range(B) for h in range(Hkv)]
+            bb, hh, jj = zip(*refs)
+            cache.compress_pages(0, bb, hh, jj, [r] * len(refs), [16] * len(refs))
+            converted += refs
+        slot, kind, rk, rv = cache.page_table_host(0)
+        plan = oracle.plan_pages(t + 1, P, S, W, max_pages)
+        assert np.array_equal(kind, np.broadcast_to(plan, kind.shape)), t
+    assert cache.device_status() == 0
+    assert converted, "the run must cross a window boundary"
+    blocks = _export(cache, converted)
+    R = cache.c.max_rank
+    for (b, h, j), blk in zip(converted, blocks):
+        Lk, Rk, Lv, Rv = _unpack_factor(blk, P, d, R)
+        Xk = K[b, h, j * P:(j + 1) * P].astype(np.float64)
+        Xv = V[b, h, j * P:(j + 1) * P].astype(np.float64)
+        _check_factor(Lk[:, :r], Rk[:r], Xk, r, 6e-3, 1e-2, 4e-3)
+        _check_factor(Lv[:, :16], Rv[:16], Xv, 16, 6e-3, 1e-2, 4e-3)
+    # compressing a page that is already factorized: device bit, entry unchanged
+    before = cache.page_table(0).clone()
+    b, h, j = converted[0]
+    cache.compress_pages(0, [b], [h], [j], [r], [r])
+    assert cache.device_status() & pk._lib.PKV_DEV_NOT_DENSE
+    assert torch.equal(before, cache.page_table(0))
+    with pytest.raises(pk.PuzzleKVError, match="PKV_E_ARG"):
+        cache.compress_pages(0, [0, 0], [0, 0], [5, 5], [r, r], [r, r])
+
+
+def test_ring_overrun_is_reported():
+    """Appending past the window without compressing the page that left it would
+    overwrite a dense page: the append is refused with a device bit."""
+    import torch
+    import paper_2608_23843_amd as pk
+    B, Hkv, d, P, S, W = 1, 1, 64, 16, 16, 16
+    cache = pk.PuzzleKVCache(1, B, Hkv, Hkv, d, P, 16, 4, S, W, "f32", "f32")
+    row = torch.ones((1, 1, d), device="cuda")
+    for t in range(16 * 5):
+        cache.append(0, row, row, [t])
+    assert cache.device_status() & pk._lib.PKV_DEV_RING_OVERRUN
+
+
+def test_zero_page():
+    import torch
+    import paper_2608_23843_amd as pk
+    P, d = 16, 64
+    cache = pk.PuzzleKVCache(1, 1, 1, 1, d, P, 4, 4, 0, 0, "f32", "f32")
+    z = torch.zeros((1, 1, 4 * P, d), device="cuda")
+    cache.prefill(0, z, z, [4 * P], default_rank=(4, 4))
+    blk = _export(cache, [(0, 0, 1)])[0]
+    Lk, Rk, Lv, Rv = _unpack_factor(blk, P, d, 4)
+    assert np.all(Rk == 0) and np.all(Rv == 0)
+    assert np.abs(Lk.T @ Lk - np.eye(4)).max() < 1e-6
