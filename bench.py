@@ -77,6 +77,7 @@ def parse():
     ap.add_argument("--workload", default="qwen32b_128k")
     ap.add_argument("--layers", type=int, default=0, help="layers per step (default: the workload's)")
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--tokens", type=int, default=0, help="override the cached length T")
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="CPU-baseline budget for the oracle (0 disables)")
     ap.add_argument("--workers", type=int, default=16, help="host threads for input generation")
@@ -171,6 +172,9 @@ def main():
         sys.exit(1)
     torch.cuda.set_device(0)
     wl = synth.WORKLOADS[args.workload]
+    if args.tokens:
+        import dataclasses
+        wl = dataclasses.replace(wl, tokens=args.tokens, name=wl.name + "_T%d" % args.tokens)
     layers = args.layers or wl.layers
     B, Hkv, Hq, d, P, T = wl.batch, wl.kv_heads, wl.q_heads, wl.head_dim, wl.page, wl.tokens
     S, W = wl.sink, wl.window

@@ -3,8 +3,8 @@
 //
 // Work is split flash-decoding style: each workgroup owns one (sequence, KV
 // head) and a contiguous chunk of pages, keeps the running (m, l, O) state
-// of the g query heads of that KV head, and writes it as a partial; the
-// combine kernel merges the partials of a head with the Eq. (5) rescaling.
+// of the g query heads of that KV head, and writes it as a partial; the last
+// workgroup of a head merges its partials with the Eq. (5) rescaling.
 // Scores are kept in the base-2 domain (s * log2(e) / sqrt(d)) so every
 // exponential is one exp2.
 // Included by pkv_kernels.hip.
@@ -14,75 +14,161 @@ namespace pkv {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
-// Partials: [B*Hkv][n_chunks][g][d + 2] floats, slot layout {m2, l, O[0..d)}.
-__host__ __device__ inline int64_t partial_index(int64_t head, int chunk, int n_chunks, int qi, int g,
-                                                 int d) {
-    return ((head * n_chunks + chunk) * g + qi) * (int64_t)(d + 2);
+// Partial states of one call, for each (sequence, KV head) `head`, query qi
+// of the group and chunk c: O[head][qi][k][c] with the chunk index fastest
+// (padded to nc4, a multiple of 4, so a merge reads one output's chunks with
+// vector loads), and the max M[head][qi][c] (log2 units) and normalizer
+// L[head][qi][c]; then one merge counter per head.
+struct Partials {
+    float *o, *m, *l;
+    unsigned int *counters;
+    int nc, nc4, g, d;
+    __host__ __device__ int64_t oi(int64_t head, int qi, int k, int c) const {
+        return ((head * g + qi) * d + k) * nc4 + c;
+    }
+    __host__ __device__ int64_t mi(int64_t head, int qi, int c) const { return (head * g + qi) * nc4 + c; }
+};
+
+__host__ __device__ inline int64_t round256(int64_t b) { return (b + 255) / 256 * 256; }
+
+__host__ __device__ inline int64_t partials_bytes(int64_t heads, int n_chunks, int g, int d) {
+    const int64_t nc4 = (n_chunks + 3) / 4 * 4;
+    return round256(heads * g * d * nc4 * 4) + 2 * round256(heads * g * nc4 * 4) + round256(heads * 4);
+}
+
+__host__ __device__ inline Partials make_partials(void *ws, int64_t heads, int n_chunks, int g, int d) {
+    Partials p;
+    p.nc = n_chunks;
+    p.nc4 = (n_chunks + 3) / 4 * 4;
+    p.g = g;
+    p.d = d;
+    char *c = (char *)ws;
+    p.o = (float *)c;
+    c += round256(heads * g * d * p.nc4 * 4);
+    p.m = (float *)c;
+    c += round256(heads * g * p.nc4 * 4);
+    p.l = (float *)c;
+    c += round256(heads * g * p.nc4 * 4);
+    p.counters = (unsigned int *)c;
+    return p;
 }
 
 // ---- combine: Eq. (5) across the chunks of one head, then normalize -----------
 //
 // Fused into the split kernels: every workgroup publishes its partial, then
 // bumps the head's counter; the workgroup that brings it to n_chunks merges
-// the head (one wavefront) and resets the counter to zero for the next call.
-// No workgroup ever waits on another, so the pattern cannot stall.
+// the head and resets the counter to zero for the next call. No workgroup
+// ever waits on another, so the pattern cannot stall.
 
-// Workspace: partials, then one uint32 counter per (sequence, KV head).
-__host__ __device__ inline int64_t counters_offset(int64_t heads, int n_chunks, int g, int d) {
-    const int64_t bytes = heads * n_chunks * g * (int64_t)(d + 2) * (int64_t)sizeof(float);
-    return (bytes + 255) / 256 * 256;
-}
+// Called by every thread of a 256-thread workgroup after its partial stores.
+// The workgroup that completes the head merges all of its chunks (Eq. (5)):
+// the per-chunk maxima and normalizers go through LDS, then each thread owns
+// a few (query, dim) outputs and reads their chunk values with vector loads,
+// all issued before they are used.
+constexpr int kMergeThreads = 256;
+constexpr int kMergeMaxChunks = 64;   // chunk states staged in LDS per round
 
-__device__ inline float wave_max(float v) {
-    for (int m = 32; m >= 1; m >>= 1) v = fmaxf(v, __shfl_xor(v, m, 64));
-    return v;
-}
-__device__ inline float wave_sum(float v) {
-    for (int m = 32; m >= 1; m >>= 1) v += __shfl_xor(v, m, 64);
-    return v;
-}
-
-// Called by all lanes of one wavefront of every workgroup after its partial
-// stores. Returns after the merge (last workgroup) or immediately.
-__device__ void publish_and_merge(const Geo &g, int64_t head, int n_chunks, float *part,
-                                  unsigned int *counters, float *out, float *lse, int64_t T, int lane) {
-    __threadfence();  // partial stores visible device-wide before the count
-    unsigned int prev = 0;
-    if (lane == 0) prev = atomicAdd(&counters[head], 1u);
-    prev = __shfl(prev, 0, 64);
-    if (prev != (unsigned int)(n_chunks - 1)) return;
+__device__ void publish_and_merge(const Geo &g, int64_t head, const Partials &pp, float *out, float *lse,
+                                  int64_t T) {
+    __shared__ unsigned int s_prev;
+    __shared__ float sM[16], sL[16];
+    __shared__ float sW[16][kMergeMaxChunks];
+    const int tid = threadIdx.x;
+    const int nc = pp.nc;
+    __syncthreads();
+    __threadfence();  // this workgroup's partial visible device-wide before the count
+    if (tid == 0) s_prev = atomicAdd(&pp.counters[head], 1u);
+    __syncthreads();
+    if (s_prev != (unsigned int)(nc - 1)) return;
     __threadfence();  // see every other workgroup's partial
 
     const int G = g.g, d = g.d;
     const int b = (int)(head / g.Hkv), h = (int)(head % g.Hkv);
-    for (int qi = 0; qi < G; ++qi) {
-        float M = -INFINITY;
-        for (int c = lane; c < n_chunks; c += 64) M = fmaxf(M, part[partial_index(head, c, n_chunks, qi, G, d)]);
-        M = wave_max(M);
-        float l = 0.f;
-        for (int c = lane; c < n_chunks; c += 64) {
-            const int64_t p = partial_index(head, c, n_chunks, qi, G, d);
-            const float m = part[p];
-            if (m != -INFINITY) l += exp2f(m - M) * part[p + 1];
-        }
-        l = wave_sum(l);
-        const bool empty = T <= 0 || M == -INFINITY || !(l > 0.f);
-        const float inv = empty ? 0.f : 1.f / l;
-        const int qh = h * G + qi;
-        float *o = out + ((int64_t)b * g.Hq + qh) * d;
-        for (int k = lane; k < d; k += 64) {
-            float acc = 0.f;
-            if (!empty)
-                for (int c = 0; c < n_chunks; ++c) {
-                    const int64_t p = partial_index(head, c, n_chunks, qi, G, d);
-                    const float m = part[p];
-                    if (m != -INFINITY) acc = fmaf(exp2f(m - M), part[p + 2 + k], acc);
-                }
-            o[k] = acc * inv;
-        }
-        if (lse && lane == 0) lse[(int64_t)b * g.Hq + qh] = empty ? -INFINITY : (M + log2f(l)) * kLn2;
+    // global max and normalizer per query: chunk states staged in LDS (all
+    // loads issued at once), reduced by one thread per query
+    if (tid < G) {
+        sM[tid] = -INFINITY;
+        sL[tid] = 0.f;
     }
-    if (lane == 0) atomicExch(&counters[head], 0u);
+    for (int pass = 0; pass < 2; ++pass) {
+        for (int c0 = 0; c0 < nc; c0 += kMergeMaxChunks) {
+            const int ncr = min(kMergeMaxChunks, nc - c0);
+            __syncthreads();
+            for (int e = tid; e < G * kMergeMaxChunks; e += kMergeThreads) {
+                const int qi = e / kMergeMaxChunks, c = e % kMergeMaxChunks;
+                sW[qi][c] = c < ncr ? (pass == 0 ? pp.m[pp.mi(head, qi, c0 + c)] : pp.l[pp.mi(head, qi, c0 + c)])
+                                    : -INFINITY;
+                if (pass == 1 && c < ncr) {
+                    const float m = pp.m[pp.mi(head, qi, c0 + c)];
+                    sW[qi][c] = m == -INFINITY ? 0.f : exp2f(m - sM[qi]) * sW[qi][c];
+                }
+            }
+            __syncthreads();
+            if (tid < G) {
+                if (pass == 0) {
+                    float M = sM[tid];
+                    for (int c = 0; c < ncr; ++c) M = fmaxf(M, sW[tid][c]);
+                    sM[tid] = M;
+                } else {
+                    float l = sL[tid];
+                    for (int c = 0; c < ncr; ++c) l += sW[tid][c] == -INFINITY ? 0.f : sW[tid][c];
+                    sL[tid] = l;
+                }
+            }
+        }
+    }
+    __syncthreads();
+    constexpr int kOut = 16;  // g * d <= 16 * 256 outputs
+    float acc[kOut];
+#pragma unroll
+    for (int i = 0; i < kOut; ++i) acc[i] = 0.f;
+    for (int c0 = 0; c0 < nc; c0 += kMergeMaxChunks) {
+        const int ncr = min(kMergeMaxChunks, nc - c0);
+        for (int e = tid; e < G * kMergeMaxChunks; e += kMergeThreads) {
+            const int qi = e / kMergeMaxChunks, c = e % kMergeMaxChunks;
+            float wgt = 0.f;
+            if (c < ncr) {
+                const float m = pp.m[pp.mi(head, qi, c0 + c)];
+                wgt = (m == -INFINITY || sM[qi] == -INFINITY) ? 0.f : exp2f(m - sM[qi]);
+            }
+            sW[qi][c] = wgt;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int i = 0; i < kOut; ++i) {
+            const int idx = tid + i * kMergeThreads;
+            if (idx < G * d) {
+                const int qi = idx / d, k = idx % d;
+                const float *src = pp.o + pp.oi(head, qi, k, c0);
+                float a = acc[i];
+                int c = 0;
+                for (; c + 4 <= ncr; c += 4) {
+                    const float4 v = *(const float4 *)(src + c);
+                    a = fmaf(sW[qi][c], v.x, a);
+                    a = fmaf(sW[qi][c + 1], v.y, a);
+                    a = fmaf(sW[qi][c + 2], v.z, a);
+                    a = fmaf(sW[qi][c + 3], v.w, a);
+                }
+                for (; c < ncr; ++c) a = fmaf(sW[qi][c], src[c], a);   // never the padding slots
+                acc[i] = a;
+            }
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int i = 0; i < kOut; ++i) {
+        const int idx = tid + i * kMergeThreads;
+        if (idx < G * d) {
+            const int qi = idx / d, k = idx % d;
+            const bool empty = T <= 0 || !(sL[qi] > 0.f);
+            out[((int64_t)b * g.Hq + h * G + qi) * d + k] = empty ? 0.f : acc[i] / sL[qi];
+        }
+    }
+    if (lse && tid < G) {
+        const bool empty = T <= 0 || !(sL[tid] > 0.f);
+        lse[(int64_t)b * g.Hq + h * G + tid] = empty ? -INFINITY : (sM[tid] + log2f(sL[tid])) * kLn2;
+    }
+    if (tid == 0) atomicExch(&pp.counters[head], 0u);
 }
 
 // ---- generic kernel: any supported geometry, fp32 or bf16 storage ----------
@@ -99,8 +185,7 @@ template <typename TD, typename TF>
 __global__ __launch_bounds__(kGenThreads) void k_attn_generic(Geo g, const pkv_page *table,
                                                               const char *dense, const char *factor,
                                                               const TD *q, SeqArgs seq, int ppc,
-                                                              int n_chunks, float *part,
-                                                              unsigned int *counters, float *out,
+                                                              int n_chunks, Partials pp, float *out,
                                                               float *lse) {
     __shared__ float sq[16 * 256];
     __shared__ float sZ[16 * 64];
@@ -237,15 +322,13 @@ __global__ __launch_bounds__(kGenThreads) void k_attn_generic(Geo g, const pkv_p
         const int idx = tid + i * kGenThreads;
         if (idx >= n_out) break;
         const int qi = idx / d, k = idx % d;
-        part[partial_index(head, chunk, n_chunks, qi, G, d) + 2 + k] = o[i];
+        pp.o[pp.oi(head, qi, k, chunk)] = o[i];
     }
     if (tid < G) {
-        const int64_t p = partial_index(head, chunk, n_chunks, tid, G, d);
-        part[p] = sM[tid];
-        part[p + 1] = sL[tid];
+        pp.m[pp.mi(head, tid, chunk)] = sM[tid];
+        pp.l[pp.mi(head, tid, chunk)] = sL[tid];
     }
-    __syncthreads();
-    if (wave == 0) publish_and_merge(g, head, n_chunks, part, counters, out, lse, T, lane);
+    publish_and_merge(g, head, pp, out, lse, T);
 }
 
 }  // namespace pkv

@@ -4,15 +4,16 @@
 namespace pkv {
 
 // The split kernel keeps one workgroup per (sequence, KV head, chunk of pages).
-// Chunks are sized so the grid holds about `target` workgroups: enough waves
-// to cover every CU of the chip several times while each wave still streams
-// many pages (the merge cost grows with the chunk count).
+// Chunks are sized so the grid holds about `target` workgroups: for the
+// matrix-core kernel 512 four-wave workgroups, two per CU over the 256 CUs
+// (its register budget allows two waves per SIMD), each wave streaming many
+// pages; fewer chunks also keep the final merge short.
 AttnPlan attention_plan(const Geo &g, int64_t max_T) {
     AttnPlan p{};
     const int64_t n_pages = std::max<int64_t>(1, ceil_div(max_T, g.P));
     const int64_t heads = (int64_t)g.B * g.Hkv;
     p.use_mfma = mfma_supported(g) ? 1 : 0;
-    const int64_t target = p.use_mfma ? 4096 : 2048;
+    const int64_t target = p.use_mfma ? 512 : 1024;
     p.pages_per_chunk = (int)std::max<int64_t>(1, ceil_div(n_pages * heads, target));
     p.n_chunks = (int)ceil_div(n_pages, p.pages_per_chunk);
     return p;
@@ -20,34 +21,29 @@ AttnPlan attention_plan(const Geo &g, int64_t max_T) {
 
 int64_t attention_workspace_bytes(const Geo &g, int64_t max_T) {
     const AttnPlan p = attention_plan(g, max_T);
-    const int64_t heads = (int64_t)g.B * g.Hkv;
-    return counters_offset(heads, p.n_chunks, g.g, g.d) + heads * (int64_t)sizeof(unsigned int);
+    return partials_bytes((int64_t)g.B * g.Hkv, p.n_chunks, g.g, g.d);
 }
 
 template <typename TD, typename TF>
 static void launch_generic(const LaunchCtx &L, const LayerPtrs &p, const AttnPlan &plan, const void *q,
-                           const SeqArgs &seq, float *part, unsigned int *counters, float *out, float *lse) {
+                           const SeqArgs &seq, const Partials &pp, float *out, float *lse) {
     const Geo &g = L.geo;
     dim3 grid(plan.n_chunks, g.B * g.Hkv);
     hipLaunchKernelGGL((k_attn_generic<TD, TF>), grid, dim3(kGenThreads), 0, L.stream, g, p.table, p.dense,
-                       p.factor, (const TD *)q, seq, plan.pages_per_chunk, plan.n_chunks, part, counters, out,
-                       lse);
+                       p.factor, (const TD *)q, seq, plan.pages_per_chunk, plan.n_chunks, pp, out, lse);
 }
 
 hipError_t launch_attention(const LaunchCtx &L, const AttnPlan &plan, const void *q, const SeqArgs &seq,
                             float *out, float *lse, void *ws) {
     LayerPtrs p = layer_ptrs(L);
     const Geo &g = L.geo;
-    float *part = (float *)ws;
-    unsigned int *counters =
-        (unsigned int *)((char *)ws + counters_offset((int64_t)g.B * g.Hkv, plan.n_chunks, g.g, g.d));
-    if (plan.use_mfma)
-        return launch_attn_mfma(L, plan, (const uint16_t *)q, seq, part, counters, out, lse);
+    const Partials pp = make_partials(ws, (int64_t)g.B * g.Hkv, plan.n_chunks, g.g, g.d);
+    if (plan.use_mfma) return launch_attn_mfma(L, plan, (const uint16_t *)q, seq, pp, out, lse);
     const bool db = g.dense_dtype == PKV_BF16, fb = g.factor_dtype == PKV_BF16;
-    if (db && fb) launch_generic<uint16_t, uint16_t>(L, p, plan, q, seq, part, counters, out, lse);
-    else if (db) launch_generic<uint16_t, float>(L, p, plan, q, seq, part, counters, out, lse);
-    else if (fb) launch_generic<float, uint16_t>(L, p, plan, q, seq, part, counters, out, lse);
-    else launch_generic<float, float>(L, p, plan, q, seq, part, counters, out, lse);
+    if (db && fb) launch_generic<uint16_t, uint16_t>(L, p, plan, q, seq, pp, out, lse);
+    else if (db) launch_generic<uint16_t, float>(L, p, plan, q, seq, pp, out, lse);
+    else if (fb) launch_generic<float, uint16_t>(L, p, plan, q, seq, pp, out, lse);
+    else launch_generic<float, float>(L, p, plan, q, seq, pp, out, lse);
     return hipGetLastError();
 }
 
