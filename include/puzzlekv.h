@@ -92,8 +92,8 @@ typedef struct {
  * stores, packed from its start:
  *   A_K  = L_K          P  x r4(rk) row-major (columns >= rk are zero)
  *   B_K  = R_K          rk x d      row-major
- *   A_Vt = L_V^T        rv x P      row-major
  *   B_Vt = R_V^T        d  x r4(rv) row-major (columns >= rv are zero)
+ *   A_Vt = L_V^T        rv x P      row-major
  * for e * (P r4(rk) + rk d + rv P + d r4(rv)) bytes (pkv_factor_page_bytes).
  * Every operand is stored with its contraction index contiguous, the order
  * the attention kernel streams it in.

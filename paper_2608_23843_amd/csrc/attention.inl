@@ -220,10 +220,9 @@ __global__ __launch_bounds__(kGenThreads) void k_attn_generic(Geo g, const pkv_p
         const int rows = (int)min<int64_t>(P, T - j * P);
         if (e.kind == PKV_FACTOR) {
             const int rk = e.rank_k, rv = e.rank_v, rk4 = r4(rk), rv4 = r4(rv);
+            const FactorLayout fl = factor_layout(P, d, rk, rv);
             const TF *Ak = (const TF *)(factor + e.slot * g.factor_slot_bytes);
-            const TF *Bk = Ak + (int64_t)P * rk4;
-            const TF *Avt = Bk + (int64_t)rk * d;
-            const TF *Bvt = Avt + (int64_t)rv * P;
+            const TF *Bk = Ak + fl.bk, *Bvt = Ak + fl.bvt, *Avt = Ak + fl.avt;
             for (int i = tid; i < G * rk; i += kGenThreads) {
                 const int qi = i / rk, a = i % rk;
                 float z = 0.f;

@@ -8,36 +8,43 @@
 //   S^T = L_K Z^T        (M = token, K = rank)    L_K   stored P x r4
 //   Y^T = L_V^T E^T      (M = rank,  K = token)   L_V^T stored r x P
 //   O^T += R_V^T Y^T     (M = dim,   K = rank)    R_V^T stored d x r4
-// Each stored operand has its contraction index contiguous, so every lane
-// loads its A-operand slice straight from HBM. The accumulator layout of one
-// product (lane l holds rows 4(l/16)..4(l/16)+3 of column l%16 of each 16-row
-// tile) is reused as the B operand of the next: two 16-row tiles give a lane
-// exactly the 8 K-entries {4(l/16)+e} and {16+4(l/16)+e}, so the A operand is
-// read in that same permuted K order (two 8-byte loads) and no data moves
-// between lanes. fp32 intermediates (Z, exp weights, Y) enter the MFMA as a
-// bf16 hi/lo pair (two MFMAs), keeping about 16 mantissa bits; Q and the
-// stored pages are exact in bf16. Dense pages use S^T = K Q^T and
-// O^T += V^T E^T with V stored transposed.
+// The accumulator of one product becomes the B operand of the next without
+// moving data between lanes: lane (n, q) = (lane % 16, lane / 16) holds rows
+// 4q..4q+3 of column n of each 16-row tile, and the M rows of the tiles are
+// assigned to ranks (tokens) so that two tiles give the lane exactly the K
+// entries 8q..8q+7 a B operand needs, in natural order:
+//   rank tile rt,  row m  ->  rank  8 (m / 4) + 4 rt + m % 4
+//   token tile tt, row m  ->  token 32 (tt / 2) + 8 (m / 4) + 4 (tt % 2) + m % 4   (P >= 32)
+// Every A operand is then one contiguous 16-byte slice of a stored row.
+// fp32 intermediates (Z, exp weights, Y) enter the MFMA as a bf16 hi/lo pair
+// (two MFMAs), keeping about 16 mantissa bits; Q and the stored pages are
+// exact in bf16. Dense pages use S^T = K Q^T and O^T += V^T E^T with V stored
+// transposed. The normalizer is a fifth product, ones x E^T, so it needs no
+// per-token additions.
 //
-// Latency hiding: factor pages are read with buffer loads through a per-page
-// resource whose size is the page's byte count; slices a lane does not need
-// (rank rows past r) use an out-of-range offset and return zero without a
-// memory access, so the loads carry no branches. Each wave keeps its loads
-// half a page ahead of its math (see k_attn_mfma), so every wave always has
-// part of a page in flight, with one operand set in registers.
+// Factor operands are read with buffer loads, one resource per section of the
+// slot sized to that section: rank rows past the page's rank fall outside it
+// and read as zero, which also zeroes the matching entries of Z and Y, so the
+// K columns a lane reads past a row's end (always finite data of the same
+// page) multiply zeros. A page that is not a factor page gets empty
+// resources. Each wave keeps its loads half a page ahead of its math (see
+// k_attn_mfma).
 // Included by pkv_kernels.hip.
 
 namespace pkv {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kMfmaWaves = 4;
-constexpr float kRescaleLog2 = 8.0f;      // keep the running max until a page exceeds it by 2^8
-constexpr uint32_t kOutOfRange = 0x80000000u;
+// The running max (log2 units) is raised only when a score exceeds it by more
+// than this; below that the exp weights stay under 2^32 and the fp32 sums
+// cannot overflow, so most pages skip the cross-lane max and the rescale.
+constexpr float kLazyLog2 = 32.0f;
 constexpr int kBufferDword3 = 0x00020000; // raw buffer, 32-bit data format
 
 __device__ inline f32x4 mfma_bf16(const bf16x8 &a, const bf16x8 &b, const f32x4 &c) {
@@ -53,11 +60,18 @@ __device__ inline bf16x4 zero4() { return bf16x4{0, 0, 0, 0}; }
 __device__ inline bf16x8 zero8() { return bf16x8{0, 0, 0, 0, 0, 0, 0, 0}; }
 __device__ inline f32x4 zero_f4() { return f32x4{0.f, 0.f, 0.f, 0.f}; }
 
-__device__ inline __amdgpu_buffer_rsrc_t page_rsrc(const void *base, uint32_t bytes) {
-    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), (short)0, (int)bytes, kBufferDword3);
+// Row maps of the 16-row tiles (see the header comment).
+__device__ inline int rank_row(int rt, int m) { return 8 * (m >> 2) + 4 * rt + (m & 3); }
+template <int P>
+__device__ inline int token_row(int tt, int m) {
+    return P >= 32 ? 32 * (tt >> 1) + 8 * (m >> 2) + 4 * (tt & 1) + (m & 3) : m;
 }
-// Buffer loads: per-lane byte offset `voff` (an out-of-range value returns
-// zero), wave-uniform byte offset `soff` (scalar operand).
+
+__device__ inline __amdgpu_buffer_rsrc_t section_rsrc(const char *base, uint32_t bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(base), (short)0, (int)bytes, kBufferDword3);
+}
+// Buffer loads: per-lane byte offset `voff` (range checked), wave-uniform
+// byte offset `soff`.
 __device__ inline bf16x8 bld8(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff) {
     return __builtin_bit_cast(bf16x8, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
@@ -65,191 +79,190 @@ __device__ inline bf16x4 bld4(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t 
     return __builtin_bit_cast(bf16x4, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
 }
 
-// 8 fp32 values (two accumulator tiles) -> bf16 hi + lo operands.
-__device__ inline void split_hi_lo(const f32x4 &x0, const f32x4 &x1, bf16x8 &hi, bf16x8 &lo) {
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        const __bf16 h0 = (__bf16)x0[e];
-        const __bf16 h1 = (__bf16)x1[e];
-        hi[e] = h0;
-        hi[4 + e] = h1;
-        lo[e] = (__bf16)(x0[e] - (float)h0);
-        lo[4 + e] = (__bf16)(x1[e] - (float)h1);
-    }
+// Two fp32 values -> bf16 hi pair (round to nearest) and bf16 lo pair of the
+// remainders, as packed dwords.
+__device__ inline void split2(float a, float b, uint32_t &hi, uint32_t &lo) {
+    const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a, b}, bf16x2));
+    const float ha = __builtin_bit_cast(float, h << 16), hb = __builtin_bit_cast(float, h & 0xffff0000u);
+    hi = h;
+    lo = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2{a - ha, b - hb}, bf16x2));
+}
+// Two accumulator tiles -> hi and lo B operands (K entries 8q..8q+7).
+__device__ inline void split_tiles(const f32x4 &x0, const f32x4 &x1, bf16x8 &hi, bf16x8 &lo) {
+    uint32_t h0, h1, h2, h3, l0, l1, l2, l3;
+    split2(x0[0], x0[1], h0, l0);
+    split2(x0[2], x0[3], h1, l1);
+    split2(x1[0], x1[1], h2, l2);
+    split2(x1[2], x1[3], h3, l3);
+    hi = __builtin_bit_cast(bf16x8, u32x4{h0, h1, h2, h3});
+    lo = __builtin_bit_cast(bf16x8, u32x4{l0, l1, l2, l3});
+}
+// One tile (the other half of K zero).
+__device__ inline void split_tile(const f32x4 &x0, bf16x8 &hi, bf16x8 &lo) {
+    uint32_t h0, h1, l0, l1;
+    split2(x0[0], x0[1], h0, l0);
+    split2(x0[2], x0[3], h1, l1);
+    hi = __builtin_bit_cast(bf16x8, u32x4{h0, h1, 0u, 0u});
+    lo = __builtin_bit_cast(bf16x8, u32x4{l0, l1, 0u, 0u});
 }
 
 // Operand slices of one factor page held by one lane, in two halves: the key
 // factors feed phase 1 (scores and softmax), the value factors phase 2.
 template <int D, int P>
 struct KeyOps {
-    bf16x8 bk[2][D / 32];  // R_K rows 16*rt + n, d-chunk s
-    bf16x8 ak[P / 16];     // L_K row 16*tt + n, ranks {4 j4 .. +3} and {16 + 4 j4 .. +3}
+    bf16x8 bk[2][D / 32];  // R_K row rank_row(rt, n), d-chunk s
+    bf16x8 ak[P / 16];     // L_K row token_row(tt, n), ranks 8q..8q+7
 };
 template <int D, int P>
 struct ValueOps {
-    bf16x8 av[2][(P + 31) / 32];  // L_V^T row 16*rt + n, tokens of K-step ks in accumulator order
-    bf16x8 bv[D / 16];            // R_V^T row 16*dt + n, ranks as for ak
+    bf16x8 av[2][(P + 31) / 32];  // L_V^T row rank_row(rt, n), tokens of K-step ks
+    bf16x8 bv[D / 16];            // R_V^T row 16 dt + n, ranks 8q..8q+7
 };
 
-// Per page: the buffer resource and section offsets (scalars) and the lane's
-// byte offsets into each section (one value per operand half; out of range
-// where the lane's slice lies past the page's rank). A page that is not a
-// factor page gets a zero-size resource, so all its loads return zero.
+// Per page: one buffer resource per section and the page-dependent parts of
+// the lane offsets. Lane-constant offsets live in LaneOffs.
 struct PageRes {
-    __amdgpu_buffer_rsrc_t rs;
-    uint32_t oBk, oAvt, oBvt;     // section starts (bytes)
+    __amdgpu_buffer_rsrc_t ak, bk, bvt, avt;
     int rk, rv, rk4, rv4;
-    uint32_t v_bk[2], v_av[2];    // R_K / L_V^T rows of rank tile rt
-    uint32_t v_ak_lo, v_ak_hi;    // L_K ranks {4 j4..} / {16 + 4 j4..} (before the tile offset)
-    uint32_t v_bv_lo, v_bv_hi;    // R_V^T likewise
+};
+struct LaneOffs {
+    uint32_t bk[2], av[2];   // R_K / L_V^T row rank_row(rt, n), chunk q
+    uint32_t tok0;           // token_row(0, n)
 };
 
 template <int D, int P>
-__device__ inline PageRes page_res(const char *factor, int64_t slot_bytes, const pkv_page &e, int n, int j4) {
+__device__ inline PageRes page_res(const char *factor, int64_t slot_bytes, const pkv_page &e) {
     PageRes r;
     const bool is_f = e.kind == PKV_FACTOR;
     r.rk = is_f ? e.rank_k : 0;
     r.rv = is_f ? e.rank_v : 0;
     r.rk4 = r4(r.rk);
     r.rv4 = r4(r.rv);
-    const uint32_t bytes = (uint32_t)(2 * (P * r.rk4 + r.rk * D + r.rv * P + D * r.rv4));
-    r.rs = page_rsrc(factor + (is_f ? e.slot : 0) * slot_bytes, bytes);
-    r.oBk = 2u * P * r.rk4;
-    r.oAvt = r.oBk + 2u * r.rk * D;
-    r.oBvt = r.oAvt + 2u * r.rv * P;
-    const uint32_t lb_bk = 2u * (n * D + 8 * j4), lb_av = 2u * (n * P + 4 * j4);
-#pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
-        r.v_bk[rt] = 16 * rt + n < r.rk ? lb_bk : kOutOfRange;
-        r.v_av[rt] = 16 * rt + n < r.rv ? lb_av : kOutOfRange;
-    }
-    const uint32_t lb_ak = 2u * n * r.rk4 + 8u * j4, lb_bv = 2u * n * r.rv4 + 8u * j4;
-    r.v_ak_lo = 4 * j4 < r.rk4 ? lb_ak : kOutOfRange;
-    r.v_ak_hi = 16 + 4 * j4 < r.rk4 ? lb_ak + 32u : kOutOfRange;
-    r.v_bv_lo = 4 * j4 < r.rv4 ? lb_bv : kOutOfRange;
-    r.v_bv_hi = 16 + 4 * j4 < r.rv4 ? lb_bv + 32u : kOutOfRange;
+    const FactorLayout fl = factor_layout(P, D, r.rk, r.rv);
+    const char *base = factor + (is_f ? e.slot : 0) * slot_bytes;
+    r.ak = section_rsrc(base, (uint32_t)(2 * fl.bk));
+    r.bk = section_rsrc(base + 2 * fl.bk, (uint32_t)(2 * (fl.bvt - fl.bk)));
+    r.bvt = section_rsrc(base + 2 * fl.bvt, (uint32_t)(2 * (fl.avt - fl.bvt)));
+    r.avt = section_rsrc(base + 2 * fl.avt, (uint32_t)(2 * (fl.end - fl.avt)));
     return r;
 }
 
 template <int D, int P>
-__device__ inline void issue_key_loads(KeyOps<D, P> &f, const PageRes &r) {
+__device__ inline void issue_key_loads(KeyOps<D, P> &f, const PageRes &r, const LaneOffs &lo, int n, int q) {
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-        for (int s = 0; s < D / 32; ++s) f.bk[rt][s] = bld8(r.rs, r.v_bk[rt] + 64u * s, r.oBk + 32u * rt * D);
+        for (int s = 0; s < D / 32; ++s) f.bk[rt][s] = bld8(r.bk, lo.bk[rt] + 64u * s, 0u);
+    const uint32_t v_ak = 2u * (lo.tok0 * r.rk4 + 8 * q);
 #pragma unroll
     for (int tt = 0; tt < P / 16; ++tt) {
-        const uint32_t so = 32u * tt * r.rk4;
-        f.ak[tt] = cat4(bld4(r.rs, r.v_ak_lo, so), bld4(r.rs, r.v_ak_hi, so));
+        const uint32_t toff = P >= 32 ? 32u * (tt >> 1) + 4u * (tt & 1) : 0u;
+        f.ak[tt] = bld8(r.ak, v_ak, 2u * toff * r.rk4);
     }
 }
 
 template <int D, int P>
-__device__ inline void issue_value_loads(ValueOps<D, P> &f, const PageRes &r) {
+__device__ inline void issue_value_loads(ValueOps<D, P> &f, const PageRes &r, const LaneOffs &lo, int n, int q) {
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt)
 #pragma unroll
-        for (int ks = 0; ks < (P + 31) / 32; ++ks) {
-            const uint32_t so = r.oAvt + 32u * rt * P;
-            f.av[rt][ks] = cat4(bld4(r.rs, r.v_av[rt] + 64u * ks, so),
-                                32 * ks + 16 < P ? bld4(r.rs, r.v_av[rt] + 64u * ks + 32u, so) : zero4());
-        }
+        for (int ks = 0; ks < (P + 31) / 32; ++ks)
+            f.av[rt][ks] = P >= 32 ? bld8(r.avt, lo.av[rt] + 64u * ks, 0u) : cat4(bld4(r.avt, lo.av[rt], 0u), zero4());
+    const uint32_t v_bv = 2u * (n * r.rv4 + 8 * q);
 #pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) {
-        const uint32_t so = r.oBvt + 32u * dt * r.rv4;
-        f.bv[dt] = cat4(bld4(r.rs, r.v_bv_lo, so), bld4(r.rs, r.v_bv_hi, so));
-    }
+    for (int dt = 0; dt < D / 16; ++dt) f.bv[dt] = bld8(r.bvt, v_bv, 32u * dt * r.rv4);
 }
 
-// Running softmax state of one wave: O^T tiles, max (log2 units) and the
-// lane's share of the normalizer.
+// Running softmax state of one wave: O^T tiles, the normalizer (every row of
+// `l` holds its column's value) and the running max (log2 units).
 template <int D>
 struct WaveState {
     f32x4 o[D / 16];
-    float m_run, l_part;
+    f32x4 l;
+    float m_run;
 };
 
-// Online softmax over one page's scores st (raw, unscaled on entry); leaves
-// the exp weights as hi/lo B operands of the token contraction. Rows at or
-// past `rows` are masked (dense pages only; factor pages are complete).
+// Online softmax over one page's raw scores st (Eq. (5) state update);
+// leaves the exp weights as hi/lo B operands of the token contraction and
+// adds them to the normalizer. Rows at or past `rows` are masked (dense pages
+// only; factor pages are complete).
 template <int D, int P, bool MASK>
 __device__ inline void page_softmax(WaveState<D> &w, f32x4 (&st)[P / 16], bf16x8 (&eh)[(P + 31) / 32],
-                                    bf16x8 (&el)[(P + 31) / 32], int rows, int j4, float c2) {
+                                    bf16x8 (&el)[(P + 31) / 32], int rows, int q, float c2) {
     constexpr int TT = P / 16, KS = (P + 31) / 32, DT = D / 16;
     float pm = -INFINITY;
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt)
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-            float s = st[tt][v] * c2;
-            if (MASK && 16 * tt + 4 * j4 + v >= rows) s = -INFINITY;
-            st[tt][v] = s;
-            pm = fmaxf(pm, s);
+            if (MASK && token_row<P>(tt, 4 * q + v) >= rows) st[tt][v] = -INFINITY;
+            pm = fmaxf(pm, st[tt][v]);
         }
-    pm = fmaxf(pm, __shfl_xor(pm, 16, 64));
-    pm = fmaxf(pm, __shfl_xor(pm, 32, 64));
-    if (pm > w.m_run + kRescaleLog2 || w.m_run == -INFINITY) {
-        const float alpha = w.m_run == -INFINITY ? 0.f : exp2f(w.m_run - pm);
+    if (__builtin_amdgcn_ballot_w64(pm * c2 > w.m_run + kLazyLog2) != 0) {
+        pm = fmaxf(pm, __shfl_xor(pm, 16, 64));
+        pm = fmaxf(pm, __shfl_xor(pm, 32, 64));
+        const float m_new = fmaxf(w.m_run, pm * c2);
+        const float alpha = w.m_run == -INFINITY ? 0.f : exp2f(w.m_run - m_new);
 #pragma unroll
         for (int t = 0; t < DT; ++t) w.o[t] *= alpha;
-        w.l_part *= alpha;
-        w.m_run = pm;
+        w.l *= alpha;
+        w.m_run = m_new;
     }
+    const float nm = -w.m_run;
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const float ex = exp2f(st[tt][v] - w.m_run);
-            st[tt][v] = ex;
-            w.l_part += ex;
-        }
+        for (int v = 0; v < 4; ++v) st[tt][v] = __builtin_amdgcn_exp2f(fmaf(st[tt][v], c2, nm));
+    const bf16x8 ones = bf16x8{1, 1, 1, 1, 1, 1, 1, 1};
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks)
-        split_hi_lo(st[2 * ks], 2 * ks + 1 < TT ? st[2 * ks + 1] : zero_f4(), eh[ks], el[ks]);
+    for (int ks = 0; ks < KS; ++ks) {
+        if (2 * ks + 1 < TT) split_tiles(st[2 * ks], st[2 * ks + 1], eh[ks], el[ks]);
+        else split_tile(st[2 * ks], eh[ks], el[ks]);
+        w.l = mfma_bf16(ones, eh[ks], w.l);
+        w.l = mfma_bf16(ones, el[ks], w.l);
+    }
 }
 
 // Phase 1 of a factor page: Z^T = R_K Q^T, S^T = L_K Z^T, softmax.
 template <int D, int P>
-__device__ inline void factor_phase1(WaveState<D> &w, const KeyOps<D, P> &f, const bf16x8 (&qb)[D / 32], int rk,
-                                     bf16x8 (&eh)[(P + 31) / 32], bf16x8 (&el)[(P + 31) / 32], int j4, float c2) {
+__device__ inline void factor_phase1(WaveState<D> &w, const KeyOps<D, P> &f, const bf16x8 (&qb)[D / 32],
+                                     bf16x8 (&eh)[(P + 31) / 32], bf16x8 (&el)[(P + 31) / 32], int q, float c2) {
+    // both rank tiles hold ranks below 16 (rank_row), so neither is skipped
+    // for small ranks; rows past the rank read as zero
     f32x4 z[2];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
         z[rt] = zero_f4();
-        if (rk > 16 * rt)
 #pragma unroll
-            for (int s = 0; s < D / 32; ++s) z[rt] = mfma_bf16(f.bk[rt][s], qb[s], z[rt]);
+        for (int s = 0; s < D / 32; ++s) z[rt] = mfma_bf16(f.bk[rt][s], qb[s], z[rt]);
     }
     bf16x8 zh, zl;
-    z[0] *= c2;  // scores come out in log2 units
-    z[1] *= c2;
-    split_hi_lo(z[0], z[1], zh, zl);
+    split_tiles(z[0], z[1], zh, zl);
     f32x4 st[P / 16];
 #pragma unroll
     for (int tt = 0; tt < P / 16; ++tt) {
         st[tt] = mfma_bf16(f.ak[tt], zh, zero_f4());
         st[tt] = mfma_bf16(f.ak[tt], zl, st[tt]);
     }
-    page_softmax<D, P, false>(w, st, eh, el, P, j4, 1.0f);
+    page_softmax<D, P, false>(w, st, eh, el, P, q, c2);
 }
 
 // Phase 2 of a factor page: Y^T = L_V^T E^T, O^T += R_V^T Y^T.
 template <int D, int P>
-__device__ inline void factor_phase2(WaveState<D> &w, const ValueOps<D, P> &f, int rv,
+__device__ inline void factor_phase2(WaveState<D> &w, const ValueOps<D, P> &f,
                                      const bf16x8 (&eh)[(P + 31) / 32], const bf16x8 (&el)[(P + 31) / 32]) {
     f32x4 y[2];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
         y[rt] = zero_f4();
-        if (rv > 16 * rt)
 #pragma unroll
-            for (int ks = 0; ks < (P + 31) / 32; ++ks) {
-                y[rt] = mfma_bf16(f.av[rt][ks], eh[ks], y[rt]);
-                y[rt] = mfma_bf16(f.av[rt][ks], el[ks], y[rt]);
-            }
+        for (int ks = 0; ks < (P + 31) / 32; ++ks) {
+            y[rt] = mfma_bf16(f.av[rt][ks], eh[ks], y[rt]);
+            y[rt] = mfma_bf16(f.av[rt][ks], el[ks], y[rt]);
+        }
     }
     bf16x8 yh, yl;
-    split_hi_lo(y[0], y[1], yh, yl);
+    split_tiles(y[0], y[1], yh, yl);
 #pragma unroll
     for (int dt = 0; dt < D / 16; ++dt) {
         w.o[dt] = mfma_bf16(f.bv[dt], yh, w.o[dt]);
@@ -260,7 +273,7 @@ __device__ inline void factor_phase2(WaveState<D> &w, const ValueOps<D, P> &f, i
 // Dense page (sink, window, partial last page): loads and computes in place.
 template <int D, int P>
 __device__ inline void dense_page(WaveState<D> &w, const bf16x8 (&qb)[D / 32], const char *dense,
-                                  int64_t slot_bytes, int slot, int rows, int n, int j4, float c2) {
+                                  int64_t slot_bytes, int slot, int rows, int n, int q, float c2) {
     constexpr int KD = D / 32, DT = D / 16, TT = P / 16, KS = (P + 31) / 32;
     const uint16_t *K = (const uint16_t *)(dense + slot * slot_bytes);
     const uint16_t *Vt = K + (int64_t)P * D;
@@ -268,26 +281,23 @@ __device__ inline void dense_page(WaveState<D> &w, const bf16x8 (&qb)[D / 32], c
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt) {
         st[tt] = zero_f4();
+        const uint16_t *kp = K + (int64_t)token_row<P>(tt, n) * D + 8 * q;
 #pragma unroll
-        for (int s = 0; s < KD; ++s)
-            st[tt] = mfma_bf16(ld_b8(K + (int64_t)(16 * tt + n) * D + 32 * s + 8 * j4), qb[s], st[tt]);
+        for (int s = 0; s < KD; ++s) st[tt] = mfma_bf16(ld_b8(kp + 32 * s), qb[s], st[tt]);
     }
     bf16x8 eh[KS], el[KS];
-    page_softmax<D, P, true>(w, st, eh, el, rows, j4, c2);
+    page_softmax<D, P, true>(w, st, eh, el, rows, q, c2);
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
         const uint16_t *vp = Vt + (int64_t)(16 * dt + n) * P;
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-            const int t0 = 32 * ks + 4 * j4, t1 = 32 * ks + 16 + 4 * j4;
-            bf16x4 lo = ld_b4(vp + t0);
-            bf16x4 hi = 32 * ks + 16 < P ? ld_b4(vp + t1) : zero4();
+            // K entries 8q..8q+7 are tokens 32 ks + 8q + u (P >= 32) or 4q + u (P = 16)
+            const int t0 = P >= 32 ? 32 * ks + 8 * q : 4 * q;
+            bf16x8 vv = P >= 32 ? ld_b8(vp + t0) : cat4(ld_b4(vp + t0), zero4());
 #pragma unroll
-            for (int u = 0; u < 4; ++u) {   // rows past the sequence may hold anything
-                if (t0 + u >= rows) lo[u] = (__bf16)0.f;
-                if (t1 + u >= rows) hi[u] = (__bf16)0.f;
-            }
-            const bf16x8 vv = cat4(lo, hi);
+            for (int u = 0; u < (P >= 32 ? 8 : 4); ++u)   // rows past the sequence may hold anything
+                if (t0 + u >= rows) vv[u] = (__bf16)0.f;
             w.o[dt] = mfma_bf16(vv, eh[ks], w.o[dt]);
             w.o[dt] = mfma_bf16(vv, el[ks], w.o[dt]);
         }
@@ -328,7 +338,7 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 2) void k_attn_mfma(Geo g, const p
     // page resources) stays wave-uniform
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
     const int lane = threadIdx.x % 64;
-    const int n = lane & 15, j4 = lane >> 4;
+    const int n = lane & 15, q4 = lane >> 4;
     const int64_t T = seq.len[b];
     const int64_t n_pages = ceil_div(T, P);
     const int64_t j0 = (int64_t)chunk * ppc;
@@ -338,16 +348,19 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 2) void k_attn_mfma(Geo g, const p
     // query group as the B operand (K = d, N = query head)
     bf16x8 qb[KD];
     {
-        const uint16_t *qp = q + ((int64_t)b * g.Hq + (int64_t)h * G + n) * D + 8 * j4;
+        const uint16_t *qp = q + ((int64_t)b * g.Hq + (int64_t)h * G + n) * D + 8 * q4;
 #pragma unroll
         for (int s = 0; s < KD; ++s) qb[s] = n < G ? ld_b8(qp + 32 * s) : zero8();
+        // complete before the page loop: a load still pending on entry would
+        // make the first wait inside the loop body a full drain on every page
+        __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0)
     }
 
     WaveState<D> w;
 #pragma unroll
     for (int t = 0; t < DT; ++t) w.o[t] = zero_f4();
     w.m_run = -INFINITY;
-    w.l_part = 0.f;
+    w.l = zero_f4();
 
     // This wave's pages: j = first + kMfmaWaves * i, i < n_mine. Their
     // page-table entries come 64 at a time, one per lane, broadcast per page.
@@ -359,28 +372,39 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 2) void k_attn_mfma(Geo g, const p
         if ((i & 63) == 0) {
             const int64_t jl = first + (int64_t)kMfmaWaves * (i + lane);
             batch = (i + lane < n_mine) ? tab[jl] : make_uint2(0u, 0u);
+            // wait here, on the rare refill, so the per-page reads of `batch`
+            // below carry no wait on the (otherwise younger) operand loads
+            __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0)
         }
         return unpack_entry(batch, i & 63);
     };
 
+    LaneOffs lo;
+#pragma unroll
+    for (int rt = 0; rt < 2; ++rt) {
+        lo.bk[rt] = 2u * (rank_row(rt, n) * D + 8 * q4);
+        lo.av[rt] = 2u * (rank_row(rt, n) * P + (P >= 32 ? 8 : 4) * q4);
+    }
+    lo.tok0 = token_row<P>(0, n);
+    // The loop starts one step early with an empty page, so the loads of
+    // page 0 are issued by the loop body itself, in the order every later
+    // page's are: the waits the compiler places at the top of the body then
+    // count only the loads that page really needs.
     KeyOps<D, P> ko;
     ValueOps<D, P> vo;
     pkv_page cur;
     cur.kind = PKV_EMPTY;
-    if (n_mine > 0) cur = entry_of(0);
-    PageRes res = page_res<D, P>(factor, g.factor_slot_bytes, cur, n, j4);
-    issue_key_loads<D, P>(ko, res);
-    issue_value_loads<D, P>(vo, res);
-    for (int i = 0; i < n_mine; ++i) {
+    PageRes res = page_res<D, P>(factor, g.factor_slot_bytes, cur);
+    for (int i = -1; i < n_mine; ++i) {
         pkv_page nxt;
         nxt.kind = PKV_EMPTY;
         if (i + 1 < n_mine) nxt = entry_of(i + 1);
-        const PageRes nres = page_res<D, P>(factor, g.factor_slot_bytes, nxt, n, j4);
+        const PageRes nres = page_res<D, P>(factor, g.factor_slot_bytes, nxt);
         bf16x8 eh[KS], el[KS];
-        if (cur.kind == PKV_FACTOR) factor_phase1<D, P>(w, ko, qb, res.rk, eh, el, j4, c2);
-        issue_key_loads<D, P>(ko, nres);
-        if (cur.kind == PKV_FACTOR) factor_phase2<D, P>(w, vo, res.rv, eh, el);
-        issue_value_loads<D, P>(vo, nres);
+        if (cur.kind == PKV_FACTOR) factor_phase1<D, P>(w, ko, qb, eh, el, q4, c2);
+        issue_key_loads<D, P>(ko, nres, lo, n, q4);
+        if (cur.kind == PKV_FACTOR) factor_phase2<D, P>(w, vo, eh, el);
+        issue_value_loads<D, P>(vo, nres, lo, n, q4);
         cur = nxt;
         res = nres;
     }
@@ -390,7 +414,7 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 2) void k_attn_mfma(Geo g, const p
         const pkv_page e = entry_of(i);
         if (e.kind == PKV_DENSE) {
             const int64_t j = first + (int64_t)kMfmaWaves * i;
-            dense_page<D, P>(w, qb, dense, g.dense_slot_bytes, e.slot, (int)min<int64_t>(P, T - j * P), n, j4, c2);
+            dense_page<D, P>(w, qb, dense, g.dense_slot_bytes, e.slot, (int)min<int64_t>(P, T - j * P), n, q4, c2);
         } else if (e.kind != PKV_FACTOR && lane == 0) {
             raise_status(PKV_DEV_BAD_PAGE);
         }
@@ -399,17 +423,14 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 2) void k_attn_mfma(Geo g, const p
     // ---- merge the wave states (Eq. (5)) into the chunk's partial ---------
     __shared__ float s_m[kMfmaWaves][16], s_l[kMfmaWaves][16];
     __shared__ float s_o[kMfmaWaves][16][D];
-    float l_part = w.l_part;
-    l_part += __shfl_xor(l_part, 16, 64);
-    l_part += __shfl_xor(l_part, 32, 64);
-    if (j4 == 0) {
+    if (q4 == 0) {
         s_m[wave][n] = w.m_run;
-        s_l[wave][n] = l_part;
+        s_l[wave][n] = w.l[0];
     }
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) s_o[wave][n][16 * dt + 4 * j4 + v] = w.o[dt][v];
+        for (int v = 0; v < 4; ++v) s_o[wave][n][16 * dt + 4 * q4 + v] = w.o[dt][v];
     __syncthreads();
     for (int idx = threadIdx.x; idx < G * D; idx += 64 * kMfmaWaves) {
         const int qi = idx / D, k = idx % D;

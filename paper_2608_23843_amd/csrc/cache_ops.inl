@@ -223,10 +223,9 @@ __global__ __launch_bounds__(256) void k_import(Geo g, pkv_page *table, char *de
     const TF *Lv = Rk + (int64_t)rk * d;
     const TF *Rv = Lv + (int64_t)P * rv;
     const int slot = (int)(head * g.max_pages + it.j);
+    const FactorLayout fl = factor_layout(P, d, rk, rv);
     TF *Ak = (TF *)(factor + slot * g.factor_slot_bytes);
-    TF *Bk = Ak + (int64_t)P * rk4;
-    TF *Avt = Bk + (int64_t)rk * d;
-    TF *Bvt = Avt + (int64_t)rv * P;
+    TF *Bk = Ak + fl.bk, *Bvt = Ak + fl.bvt, *Avt = Ak + fl.avt;
     for (int i = threadIdx.x; i < P * rk4; i += blockDim.x) {
         int t = i / rk4, a = i % rk4;
         Ak[i] = a < rk ? Lk[t * rk + a] : TF(0);
@@ -289,10 +288,9 @@ __global__ __launch_bounds__(256) void k_export(Geo g, const pkv_page *table, co
         return;
     }
     const int rk = e.rank_k, rv = e.rank_v, rk4 = r4(rk), rv4 = r4(rv);
+    const FactorLayout fl = factor_layout(P, d, rk, rv);
     const TF *Ak = (const TF *)(factor + e.slot * g.factor_slot_bytes);
-    const TF *Bk = Ak + (int64_t)P * rk4;
-    const TF *Avt = Bk + (int64_t)rk * d;
-    const TF *Bvt = Avt + (int64_t)rv * P;
+    const TF *Bk = Ak + fl.bk, *Bvt = Ak + fl.bvt, *Avt = Ak + fl.avt;
     float *Lk = o, *Rk = Lk + P * R, *Lv = Rk + R * d, *Rv = Lv + P * R;
     for (int i = threadIdx.x; i < P * R; i += blockDim.x) {
         int t = i / R, a = i % R;

@@ -180,10 +180,9 @@ __global__ __launch_bounds__(64) void k_compress(Geo g, pkv_page *table, const c
 
     // ---- outputs ------------------------------------------------------------
     const int rk4 = r4(rk), rv4 = r4(rv);
+    const FactorLayout fl = factor_layout(P, d, rk, rv);
     TF *Ak = (TF *)(factor + (g.head_index(b, h) * g.max_pages + j) * g.factor_slot_bytes);
-    TF *Bk = Ak + (int64_t)P * rk4;
-    TF *Avt = Bk + (int64_t)rk * d;
-    TF *Bvt = Avt + (int64_t)rv * P;
+    TF *Bk = Ak + fl.bk, *Bvt = Ak + fl.bvt, *Avt = Ak + fl.avt;
     const int r = which == 0 ? rk : rv;
     const int rr4 = which == 0 ? rk4 : rv4;
     if (which == 0) {

@@ -21,6 +21,23 @@ __host__ __device__ inline int64_t factor_page_elems(int P, int d, int rk, int r
     return (int64_t)P * r4(rk) + (int64_t)rk * d + (int64_t)rv * P + (int64_t)d * r4(rv);
 }
 
+// Section starts (in elements) of a factor slot holding ranks (rk, rv):
+// A_K = L_K (P x r4(rk)), B_K = R_K (rk x d), B_Vt = R_V^T (d x r4(rv)),
+// A_Vt = L_V^T (rv x P), packed in that order. A_Vt comes last because its
+// reads past rank rv are the ones that must stop at the page's end.
+struct FactorLayout {
+    int64_t ak, bk, bvt, avt, end;
+};
+__host__ __device__ inline FactorLayout factor_layout(int P, int d, int rk, int rv) {
+    FactorLayout f;
+    f.ak = 0;
+    f.bk = (int64_t)P * r4(rk);
+    f.bvt = f.bk + (int64_t)rk * d;
+    f.avt = f.bvt + (int64_t)d * r4(rv);
+    f.end = f.avt + (int64_t)rv * P;
+    return f;
+}
+
 // Kind of logical page j of a sequence of T tokens (sink S, window W tokens).
 __host__ __device__ inline int plan_kind(int64_t T, int P, int S, int W, int64_t j) {
     if (j < 0 || j * P >= T) return PKV_EMPTY;
