@@ -201,10 +201,12 @@ pkv_status pkv_compress_pages(const pkv_cache *c, int32_t layer, int32_t n, cons
  * lse: device fp32 [batch][n_q_heads] log-sum-exp of the scaled scores, or NULL.
  * Softmax scale 1/sqrt(d); query head i uses KV head i / (n_q_heads / n_kv_heads).
  * Workspace: pkv_workspace_bytes(PKV_OP_ATTENTION, max seq_len) bytes holding
- * per-chunk partial states and one counter per (sequence, KV head); it must be
- * zero-filled before its first use, and every call leaves it ready for the
+ * per-chunk partial states and two counters per (sequence, KV head); it must
+ * be zero-filled before its first use, and every call leaves it ready for the
  * next (the counters return to zero). Calls that share a workspace must not
- * overlap. One kernel launch per call. */
+ * overlap. One kernel launch per call. With bf16 storage the pages of a head
+ * are handed to the GPU's waves dynamically, so the order of the fp32 sums,
+ * and with it the last bits of out and lse, can differ from call to call. */
 pkv_status pkv_mixed_decode_attention(const pkv_cache *c, int32_t layer, const void *q,
                                       const int32_t *seq_len, float *out, float *lse, void *ws,
                                       size_t ws_bytes, pkv_stream s);

@@ -16,12 +16,14 @@ constexpr float kLn2 = 0.6931471805599453f;
 
 // Partial states of one call, for each (sequence, KV head) `head`, query qi
 // of the group and chunk c: O[head][qi][k][c] with the chunk index fastest
-// (padded to nc4, a multiple of 4, so a merge reads one output's chunks with
-// vector loads), and the max M[head][qi][c] (log2 units) and normalizer
-// L[head][qi][c]; then one merge counter per head.
+// (padded to nc4, a multiple of 4, so one output's chunks share cache lines),
+// and the max M[head][qi][c] (log2 units) and normalizer L[head][qi][c]; then
+// one merge counter per head.
 struct Partials {
     float *o, *m, *l;
-    unsigned int *counters;
+    unsigned int *counters;  // chunks published, per head
+    unsigned int *claims;    // pages handed out, per head (streaming kernel), one per 256 bytes
+    __host__ __device__ unsigned int *claim(int64_t head) const { return claims + head * 64; }
     int nc, nc4, g, d;
     __host__ __device__ int64_t oi(int64_t head, int qi, int k, int c) const {
         return ((head * g + qi) * d + k) * nc4 + c;
@@ -33,7 +35,7 @@ __host__ __device__ inline int64_t round256(int64_t b) { return (b + 255) / 256 
 
 __host__ __device__ inline int64_t partials_bytes(int64_t heads, int n_chunks, int g, int d) {
     const int64_t nc4 = (n_chunks + 3) / 4 * 4;
-    return round256(heads * g * d * nc4 * 4) + 2 * round256(heads * g * nc4 * 4) + round256(heads * 4);
+    return round256(heads * g * d * nc4 * 4) + 2 * round256(heads * g * nc4 * 4) + round256(heads * 4) + heads * 256;
 }
 
 __host__ __device__ inline Partials make_partials(void *ws, int64_t heads, int n_chunks, int g, int d) {
@@ -50,6 +52,8 @@ __host__ __device__ inline Partials make_partials(void *ws, int64_t heads, int n
     p.l = (float *)c;
     c += round256(heads * g * p.nc4 * 4);
     p.counters = (unsigned int *)c;
+    c += round256(heads * 4);
+    p.claims = (unsigned int *)c;
     return p;
 }
 
@@ -59,116 +63,74 @@ __host__ __device__ inline Partials make_partials(void *ws, int64_t heads, int n
 // bumps the head's counter; the workgroup that brings it to n_chunks merges
 // the head and resets the counter to zero for the next call. No workgroup
 // ever waits on another, so the pattern cannot stall.
+//
+// Partials and counters are written and read with device-scope atomic
+// accesses (relaxed), which the caches keep coherent across the chip's
+// L2 slices one access at a time. A device-scope fence would instead write
+// back and invalidate a whole L2 per workgroup, stalling every other
+// workgroup's stream on that slice. Order comes from waiting for the
+// workgroup's own stores to complete before the counter is bumped.
+__device__ inline void st_dev(float *p, float v) { __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); }
+__device__ inline float ld_dev(const float *p) {
+    return __hip_atomic_load(const_cast<float *>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
 
-// Called by every thread of a 256-thread workgroup after its partial stores.
+// Called by every thread of an NT-thread workgroup after its partial stores.
 // The workgroup that completes the head merges all of its chunks (Eq. (5)):
-// the per-chunk maxima and normalizers go through LDS, then each thread owns
-// a few (query, dim) outputs and reads their chunk values with vector loads,
-// all issued before they are used.
-constexpr int kMergeThreads = 256;
-constexpr int kMergeMaxChunks = 64;   // chunk states staged in LDS per round
-
+// each thread owns a few (query, dim) outputs and folds the chunks in
+// groups of eight, issuing a group's loads (max, normalizer, output) at once
+// and rescaling its running state once per group.
+template <int NT>
 __device__ void publish_and_merge(const Geo &g, int64_t head, const Partials &pp, float *out, float *lse,
                                   int64_t T) {
     __shared__ unsigned int s_prev;
-    __shared__ float sM[16], sL[16];
-    __shared__ float sW[16][kMergeMaxChunks];
     const int tid = threadIdx.x;
     const int nc = pp.nc;
+    __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0): this thread's partial stores have completed
     __syncthreads();
-    __threadfence();  // this workgroup's partial visible device-wide before the count
-    if (tid == 0) s_prev = atomicAdd(&pp.counters[head], 1u);
+    if (tid == 0) s_prev = __hip_atomic_fetch_add(&pp.counters[head], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
     if (s_prev != (unsigned int)(nc - 1)) return;
-    __threadfence();  // see every other workgroup's partial
 
     const int G = g.g, d = g.d;
     const int b = (int)(head / g.Hkv), h = (int)(head % g.Hkv);
-    // global max and normalizer per query: chunk states staged in LDS (all
-    // loads issued at once), reduced by one thread per query
-    if (tid < G) {
-        sM[tid] = -INFINITY;
-        sL[tid] = 0.f;
-    }
-    for (int pass = 0; pass < 2; ++pass) {
-        for (int c0 = 0; c0 < nc; c0 += kMergeMaxChunks) {
-            const int ncr = min(kMergeMaxChunks, nc - c0);
-            __syncthreads();
-            for (int e = tid; e < G * kMergeMaxChunks; e += kMergeThreads) {
-                const int qi = e / kMergeMaxChunks, c = e % kMergeMaxChunks;
-                sW[qi][c] = c < ncr ? (pass == 0 ? pp.m[pp.mi(head, qi, c0 + c)] : pp.l[pp.mi(head, qi, c0 + c)])
-                                    : -INFINITY;
-                if (pass == 1 && c < ncr) {
-                    const float m = pp.m[pp.mi(head, qi, c0 + c)];
-                    sW[qi][c] = m == -INFINITY ? 0.f : exp2f(m - sM[qi]) * sW[qi][c];
-                }
-            }
-            __syncthreads();
-            if (tid < G) {
-                if (pass == 0) {
-                    float M = sM[tid];
-                    for (int c = 0; c < ncr; ++c) M = fmaxf(M, sW[tid][c]);
-                    sM[tid] = M;
-                } else {
-                    float l = sL[tid];
-                    for (int c = 0; c < ncr; ++c) l += sW[tid][c] == -INFINITY ? 0.f : sW[tid][c];
-                    sL[tid] = l;
-                }
-            }
-        }
-    }
-    __syncthreads();
-    constexpr int kOut = 16;  // g * d <= 16 * 256 outputs
-    float acc[kOut];
+    for (int idx = tid; idx < G * d; idx += NT) {
+        const int qi = idx / d, k = idx % d;
+        const float *mp = pp.m + pp.mi(head, qi, 0), *lp = pp.l + pp.mi(head, qi, 0);
+        const float *op = pp.o + pp.oi(head, qi, k, 0);
+        float M = -INFINITY, L = 0.f, A = 0.f;
+        for (int c0 = 0; c0 < nc; c0 += 8) {
+            float mv[8], lv[8], ov[8];
 #pragma unroll
-    for (int i = 0; i < kOut; ++i) acc[i] = 0.f;
-    for (int c0 = 0; c0 < nc; c0 += kMergeMaxChunks) {
-        const int ncr = min(kMergeMaxChunks, nc - c0);
-        for (int e = tid; e < G * kMergeMaxChunks; e += kMergeThreads) {
-            const int qi = e / kMergeMaxChunks, c = e % kMergeMaxChunks;
-            float wgt = 0.f;
-            if (c < ncr) {
-                const float m = pp.m[pp.mi(head, qi, c0 + c)];
-                wgt = (m == -INFINITY || sM[qi] == -INFINITY) ? 0.f : exp2f(m - sM[qi]);
+            for (int u = 0; u < 8; ++u) {
+                const bool ok = c0 + u < nc;
+                mv[u] = ok ? ld_dev(mp + c0 + u) : -INFINITY;
+                lv[u] = ok ? ld_dev(lp + c0 + u) : 0.f;
+                ov[u] = ok ? ld_dev(op + c0 + u) : 0.f;
             }
-            sW[qi][c] = wgt;
-        }
-        __syncthreads();
+            float Mg = M;
 #pragma unroll
-        for (int i = 0; i < kOut; ++i) {
-            const int idx = tid + i * kMergeThreads;
-            if (idx < G * d) {
-                const int qi = idx / d, k = idx % d;
-                const float *src = pp.o + pp.oi(head, qi, k, c0);
-                float a = acc[i];
-                int c = 0;
-                for (; c + 4 <= ncr; c += 4) {
-                    const float4 v = *(const float4 *)(src + c);
-                    a = fmaf(sW[qi][c], v.x, a);
-                    a = fmaf(sW[qi][c + 1], v.y, a);
-                    a = fmaf(sW[qi][c + 2], v.z, a);
-                    a = fmaf(sW[qi][c + 3], v.w, a);
-                }
-                for (; c < ncr; ++c) a = fmaf(sW[qi][c], src[c], a);   // never the padding slots
-                acc[i] = a;
+            for (int u = 0; u < 8; ++u) Mg = fmaxf(Mg, mv[u]);
+            if (Mg == -INFINITY) continue;   // no tokens in any chunk so far
+            const float sc = M == -INFINITY ? 0.f : exp2f(M - Mg);
+            L *= sc;
+            A *= sc;
+#pragma unroll
+            for (int u = 0; u < 8; ++u) {
+                const float wgt = mv[u] == -INFINITY ? 0.f : exp2f(mv[u] - Mg);
+                L = fmaf(wgt, lv[u], L);
+                A = fmaf(wgt, ov[u], A);
             }
+            M = Mg;
         }
-        __syncthreads();
+        const bool empty = T <= 0 || !(L > 0.f);
+        out[((int64_t)b * g.Hq + h * G + qi) * d + k] = empty ? 0.f : A / L;
+        if (lse && k == 0) lse[(int64_t)b * g.Hq + h * G + qi] = empty ? -INFINITY : (M + log2f(L)) * kLn2;
     }
-#pragma unroll
-    for (int i = 0; i < kOut; ++i) {
-        const int idx = tid + i * kMergeThreads;
-        if (idx < G * d) {
-            const int qi = idx / d, k = idx % d;
-            const bool empty = T <= 0 || !(sL[qi] > 0.f);
-            out[((int64_t)b * g.Hq + h * G + qi) * d + k] = empty ? 0.f : acc[i] / sL[qi];
-        }
+    if (tid == 0) {
+        __hip_atomic_store(&pp.counters[head], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(pp.claim(head), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    if (lse && tid < G) {
-        const bool empty = T <= 0 || !(sL[tid] > 0.f);
-        lse[(int64_t)b * g.Hq + h * G + tid] = empty ? -INFINITY : (sM[tid] + log2f(sL[tid])) * kLn2;
-    }
-    if (tid == 0) atomicExch(&pp.counters[head], 0u);
 }
 
 // ---- generic kernel: any supported geometry, fp32 or bf16 storage ----------
@@ -321,13 +283,13 @@ __global__ __launch_bounds__(kGenThreads) void k_attn_generic(Geo g, const pkv_p
         const int idx = tid + i * kGenThreads;
         if (idx >= n_out) break;
         const int qi = idx / d, k = idx % d;
-        pp.o[pp.oi(head, qi, k, chunk)] = o[i];
+        st_dev(&pp.o[pp.oi(head, qi, k, chunk)], o[i]);
     }
     if (tid < G) {
-        pp.m[pp.mi(head, tid, chunk)] = sM[tid];
-        pp.l[pp.mi(head, tid, chunk)] = sL[tid];
+        st_dev(&pp.m[pp.mi(head, tid, chunk)], sM[tid]);
+        st_dev(&pp.l[pp.mi(head, tid, chunk)], sL[tid]);
     }
-    publish_and_merge(g, head, pp, out, lse, T);
+    publish_and_merge<kGenThreads>(g, head, pp, out, lse, T);
 }
 
 }  // namespace pkv

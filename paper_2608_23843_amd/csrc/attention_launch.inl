@@ -5,15 +5,15 @@ namespace pkv {
 
 // The split kernel keeps one workgroup per (sequence, KV head, chunk of pages).
 // Chunks are sized so the grid holds about `target` workgroups: for the
-// matrix-core kernel 512 four-wave workgroups, two per CU over the 256 CUs
-// (its register budget allows two waves per SIMD), each wave streaming many
-// pages; fewer chunks also keep the final merge short.
+// matrix-core kernel 256 eight-wave workgroups, one per CU (its register
+// budget allows two waves per SIMD), each wave streaming many pages; fewer
+// chunks also keep the final merge short.
 AttnPlan attention_plan(const Geo &g, int64_t max_T) {
     AttnPlan p{};
     const int64_t n_pages = std::max<int64_t>(1, ceil_div(max_T, g.P));
     const int64_t heads = (int64_t)g.B * g.Hkv;
     p.use_mfma = mfma_supported(g) ? 1 : 0;
-    const int64_t target = p.use_mfma ? 512 : 1024;
+    const int64_t target = p.use_mfma ? 256 : 1024;
     p.pages_per_chunk = (int)std::max<int64_t>(1, ceil_div(n_pages * heads, target));
     p.n_chunks = (int)ceil_div(n_pages, p.pages_per_chunk);
     return p;

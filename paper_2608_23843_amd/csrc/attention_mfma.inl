@@ -40,7 +40,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kMfmaWaves = 4;
+constexpr int kMfmaWaves = 8;
 // The running max (log2 units) is raised only when a score exceeds it by more
 // than this; below that the exp weights stay under 2^32 and the fp32 sums
 // cannot overflow, so most pages skip the cross-lane max and the rescale.
@@ -130,16 +130,43 @@ struct LaneOffs {
     uint32_t tok0;           // token_row(0, n)
 };
 
+// One step of a wave's stream: a factor page, or a unit of min(P, 32)
+// tokens of a dense page (`half` = which unit), so that dense pages flow
+// through the same pipelined loop and operand registers as factor pages.
+struct Unit {
+    pkv_page e;   // e.kind == PKV_EMPTY: no unit
+    int64_t j;    // logical page
+    int half;     // dense pages: unit index within the page
+};
+template <int P>
+__device__ constexpr int dense_unit_tokens() { return P < 32 ? P : 32; }
+
 template <int D, int P>
-__device__ inline PageRes page_res(const char *factor, int64_t slot_bytes, const pkv_page &e) {
+__device__ inline PageRes unit_res(const char *factor, int64_t fslot_bytes, const char *dense, int64_t dslot_bytes,
+                                   const Unit &u) {
     PageRes r;
-    const bool is_f = e.kind == PKV_FACTOR;
-    r.rk = is_f ? e.rank_k : 0;
-    r.rv = is_f ? e.rank_v : 0;
+    if (u.e.kind == PKV_DENSE) {
+        // K rows of the unit feed the R_K registers (the same rank_row lane
+        // map serves as the token map of two 16-row tiles), V^T columns of
+        // the unit the R_V^T registers with row length P.
+        constexpr int UT = dense_unit_tokens<P>();
+        const char *base = dense + u.e.slot * dslot_bytes;
+        r.rk = r.rv = 0;
+        r.rk4 = 0;
+        r.rv4 = P;
+        r.ak = section_rsrc(base, 0u);
+        r.avt = section_rsrc(base, 0u);
+        r.bk = section_rsrc(base + 2 * UT * u.half * D, (uint32_t)(2 * UT * D));
+        r.bvt = section_rsrc(base + 2 * P * D + 2 * UT * u.half, (uint32_t)(2 * (D * P - UT * u.half)));
+        return r;
+    }
+    const bool is_f = u.e.kind == PKV_FACTOR;
+    r.rk = is_f ? u.e.rank_k : 0;
+    r.rv = is_f ? u.e.rank_v : 0;
     r.rk4 = r4(r.rk);
     r.rv4 = r4(r.rv);
     const FactorLayout fl = factor_layout(P, D, r.rk, r.rv);
-    const char *base = factor + (is_f ? e.slot : 0) * slot_bytes;
+    const char *base = factor + (is_f ? u.e.slot : 0) * fslot_bytes;
     r.ak = section_rsrc(base, (uint32_t)(2 * fl.bk));
     r.bk = section_rsrc(base + 2 * fl.bk, (uint32_t)(2 * (fl.bvt - fl.bk)));
     r.bvt = section_rsrc(base + 2 * fl.bvt, (uint32_t)(2 * (fl.avt - fl.bvt)));
@@ -223,10 +250,15 @@ __device__ inline void page_softmax(WaveState<D> &w, f32x4 (&st)[P / 16], bf16x8
     }
 }
 
-// Phase 1 of a factor page: Z^T = R_K Q^T, S^T = L_K Z^T, softmax.
+// Phase 1 of a unit. Factor page: Z^T = R_K Q^T, S^T = L_K Z^T, softmax.
+// Dense unit: the same first product with the unit's K rows in the R_K
+// registers is already S^T (two 16-token tiles); softmax with tokens at or
+// past `rows` masked. Either way the exp weights come out as hi/lo B operands
+// of the token contraction (a dense unit uses K-step 0 only).
 template <int D, int P>
-__device__ inline void factor_phase1(WaveState<D> &w, const KeyOps<D, P> &f, const bf16x8 (&qb)[D / 32],
-                                     bf16x8 (&eh)[(P + 31) / 32], bf16x8 (&el)[(P + 31) / 32], int q, float c2) {
+__device__ inline void unit_phase1(WaveState<D> &w, const KeyOps<D, P> &f, const bf16x8 (&qb)[D / 32], bool dense,
+                                   int rows, bf16x8 (&eh)[(P + 31) / 32], bf16x8 (&el)[(P + 31) / 32], int q,
+                                   float c2) {
     // both rank tiles hold ranks below 16 (rank_row), so neither is skipped
     // for small ranks; rows past the rank read as zero
     f32x4 z[2];
@@ -235,6 +267,13 @@ __device__ inline void factor_phase1(WaveState<D> &w, const KeyOps<D, P> &f, con
         z[rt] = zero_f4();
 #pragma unroll
         for (int s = 0; s < D / 32; ++s) z[rt] = mfma_bf16(f.bk[rt][s], qb[s], z[rt]);
+    }
+    if (dense) {
+        bf16x8 eh1[1], el1[1];
+        page_softmax<D, 32, true>(w, z, eh1, el1, rows, q, c2);
+        eh[0] = eh1[0];
+        el[0] = el1[0];
+        return;
     }
     bf16x8 zh, zl;
     split_tiles(z[0], z[1], zh, zl);
@@ -247,70 +286,49 @@ __device__ inline void factor_phase1(WaveState<D> &w, const KeyOps<D, P> &f, con
     page_softmax<D, P, false>(w, st, eh, el, P, q, c2);
 }
 
-// Phase 2 of a factor page: Y^T = L_V^T E^T, O^T += R_V^T Y^T.
+// Phase 2 of a unit. Factor page: Y^T = L_V^T E^T, O^T += R_V^T Y^T. Dense
+// unit: O^T += V^T E^T with the unit's V^T columns in the R_V^T registers;
+// columns at or past `rows` may hold anything, so they are zeroed.
 template <int D, int P>
-__device__ inline void factor_phase2(WaveState<D> &w, const ValueOps<D, P> &f,
-                                     const bf16x8 (&eh)[(P + 31) / 32], const bf16x8 (&el)[(P + 31) / 32]) {
-    f32x4 y[2];
+__device__ inline void unit_phase2(WaveState<D> &w, const ValueOps<D, P> &f, bool dense, int rows,
+                                   const bf16x8 (&eh)[(P + 31) / 32], const bf16x8 (&el)[(P + 31) / 32], int q) {
+    bf16x8 bh, bl;
+    if (dense) {
+        bh = eh[0];
+        bl = el[0];
+    } else {
+        f32x4 y[2];
 #pragma unroll
-    for (int rt = 0; rt < 2; ++rt) {
-        y[rt] = zero_f4();
+        for (int rt = 0; rt < 2; ++rt) {
+            y[rt] = zero_f4();
 #pragma unroll
-        for (int ks = 0; ks < (P + 31) / 32; ++ks) {
-            y[rt] = mfma_bf16(f.av[rt][ks], eh[ks], y[rt]);
-            y[rt] = mfma_bf16(f.av[rt][ks], el[ks], y[rt]);
+            for (int ks = 0; ks < (P + 31) / 32; ++ks) {
+                y[rt] = mfma_bf16(f.av[rt][ks], eh[ks], y[rt]);
+                y[rt] = mfma_bf16(f.av[rt][ks], el[ks], y[rt]);
+            }
         }
+        split_tiles(y[0], y[1], bh, bl);
     }
-    bf16x8 yh, yl;
-    split_tiles(y[0], y[1], yh, yl);
+    const bool mask = dense && rows < 32;
 #pragma unroll
     for (int dt = 0; dt < D / 16; ++dt) {
-        w.o[dt] = mfma_bf16(f.bv[dt], yh, w.o[dt]);
-        w.o[dt] = mfma_bf16(f.bv[dt], yl, w.o[dt]);
-    }
-}
-
-// Dense page (sink, window, partial last page): loads and computes in place.
-template <int D, int P>
-__device__ inline void dense_page(WaveState<D> &w, const bf16x8 (&qb)[D / 32], const char *dense,
-                                  int64_t slot_bytes, int slot, int rows, int n, int q, float c2) {
-    constexpr int KD = D / 32, DT = D / 16, TT = P / 16, KS = (P + 31) / 32;
-    const uint16_t *K = (const uint16_t *)(dense + slot * slot_bytes);
-    const uint16_t *Vt = K + (int64_t)P * D;
-    f32x4 st[TT];
+        bf16x8 vv = f.bv[dt];
+        if (mask) {
 #pragma unroll
-    for (int tt = 0; tt < TT; ++tt) {
-        st[tt] = zero_f4();
-        const uint16_t *kp = K + (int64_t)token_row<P>(tt, n) * D + 8 * q;
-#pragma unroll
-        for (int s = 0; s < KD; ++s) st[tt] = mfma_bf16(ld_b8(kp + 32 * s), qb[s], st[tt]);
-    }
-    bf16x8 eh[KS], el[KS];
-    page_softmax<D, P, true>(w, st, eh, el, rows, q, c2);
-#pragma unroll
-    for (int dt = 0; dt < DT; ++dt) {
-        const uint16_t *vp = Vt + (int64_t)(16 * dt + n) * P;
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-            // K entries 8q..8q+7 are tokens 32 ks + 8q + u (P >= 32) or 4q + u (P = 16)
-            const int t0 = P >= 32 ? 32 * ks + 8 * q : 4 * q;
-            bf16x8 vv = P >= 32 ? ld_b8(vp + t0) : cat4(ld_b4(vp + t0), zero4());
-#pragma unroll
-            for (int u = 0; u < (P >= 32 ? 8 : 4); ++u)   // rows past the sequence may hold anything
-                if (t0 + u >= rows) vv[u] = (__bf16)0.f;
-            w.o[dt] = mfma_bf16(vv, eh[ks], w.o[dt]);
-            w.o[dt] = mfma_bf16(vv, el[ks], w.o[dt]);
+            for (int u = 0; u < 8; ++u)
+                if (8 * q + u >= rows) vv[u] = (__bf16)0.f;
         }
+        w.o[dt] = mfma_bf16(vv, bh, w.o[dt]);
+        w.o[dt] = mfma_bf16(vv, bl, w.o[dt]);
     }
 }
 
-// Entry `sl` of the lane-distributed batch, read with readlane so the slot and
-// ranks are wave-uniform scalars (the page's buffer resource then lives in
-// scalar registers and its loads need no per-lane resource handling).
-__device__ inline pkv_page unpack_entry(uint2 ent, int sl) {
+// A page-table entry read at a wave-uniform address, as scalars: the page's
+// buffer resources then live in scalar registers.
+__device__ inline pkv_page unpack_entry(uint2 ent) {
     pkv_page e;
-    e.slot = (int32_t)__builtin_amdgcn_readlane((int)ent.x, sl);
-    const unsigned int meta = (unsigned int)__builtin_amdgcn_readlane((int)ent.y, sl);
+    e.slot = (int32_t)__builtin_amdgcn_readfirstlane((int)ent.x);
+    const unsigned int meta = (unsigned int)__builtin_amdgcn_readfirstlane((int)ent.y);
     e.kind = (uint8_t)(meta & 0xffu);
     e.rank_k = (uint8_t)((meta >> 8) & 0xffu);
     e.rank_v = (uint8_t)((meta >> 16) & 0xffu);
@@ -318,16 +336,19 @@ __device__ inline pkv_page unpack_entry(uint2 ent, int sl) {
     return e;
 }
 
-// Four wavefronts per workgroup take the chunk's pages round-robin, each with
-// its own running state; the states are merged in LDS at the end. Per wave
-// the loads run half a page ahead of the math: phase 1 of page i reads the
-// key operands, which are then refilled with page i+1's while phase 2 of
-// page i reads the value operands, refilled in turn with page i+1's. One
-// operand set per wave keeps the register budget at two waves per SIMD.
+// One workgroup of eight wavefronts per CU (two per SIMD) streams a chunk of
+// one head's pages; each wave keeps its own running state, and the states
+// are merged in LDS at the end. Per wave the loads run half a page ahead of
+// the math: phase 1 of page i reads the key operands, which are then refilled
+// with page i+1's while phase 2 of page i reads the value operands, refilled
+// in turn with page i+1's. One operand set per wave keeps the register budget
+// at two waves per SIMD.
 template <int D, int P>
-__global__ __launch_bounds__(64 * kMfmaWaves, 2) void k_attn_mfma(Geo g, const pkv_page *table, const char *dense,
-                                                                  const char *factor, const uint16_t *q, SeqArgs seq,
-                                                                  int ppc, int n_chunks, Partials pp, float *out,
+__global__ __launch_bounds__(64 * kMfmaWaves, 1) void k_attn_mfma(Geo g, const pkv_page *__restrict__ table,
+                                                                  const char *__restrict__ dense,
+                                                                  const char *__restrict__ factor,
+                                                                  const uint16_t *__restrict__ q, SeqArgs seq,
+                                                                  int /*ppc*/, int n_chunks, Partials pp, float *out,
                                                                   float *lse) {
     constexpr int KD = D / 32, DT = D / 16, KS = (P + 31) / 32;
     const int chunk = blockIdx.x;
@@ -341,8 +362,6 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 2) void k_attn_mfma(Geo g, const p
     const int n = lane & 15, q4 = lane >> 4;
     const int64_t T = seq.len[b];
     const int64_t n_pages = ceil_div(T, P);
-    const int64_t j0 = (int64_t)chunk * ppc;
-    const int64_t j1 = min<int64_t>(j0 + ppc, n_pages);
     const float c2 = kLog2e / sqrtf((float)D);
 
     // query group as the B operand (K = d, N = query head)
@@ -362,21 +381,64 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 2) void k_attn_mfma(Geo g, const p
     w.m_run = -INFINITY;
     w.l = zero_f4();
 
-    // This wave's pages: j = first + kMfmaWaves * i, i < n_mine. Their
-    // page-table entries come 64 at a time, one per lane, broadcast per page.
-    const int64_t first = j0 + wave;
-    const int n_mine = first < j1 ? (int)ceil_div(j1 - first, kMfmaWaves) : 0;
+    // Pages are handed out dynamically: every wave of every workgroup of a
+    // head takes the head's next page from one device-wide counter, so the
+    // waves and CUs that the memory system serves faster simply take more
+    // pages and all finish together. A dense page becomes P / 32 units of up
+    // to 32 tokens that flow through the same pipelined loop (and operand
+    // registers) as factor pages.
     const uint2 *tab = (const uint2 *)(table + head * g.max_pages);
-    uint2 batch = make_uint2(0u, 0u);
-    auto entry_of = [&](int i) -> pkv_page {
-        if ((i & 63) == 0) {
-            const int64_t jl = first + (int64_t)kMfmaWaves * (i + lane);
-            batch = (i + lane < n_mine) ? tab[jl] : make_uint2(0u, 0u);
-            // wait here, on the rare refill, so the per-page reads of `batch`
-            // below carry no wait on the (otherwise younger) operand loads
-            __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0)
+    constexpr int UT = dense_unit_tokens<P>();
+    // claim: take the head's next page index and start reading its entry
+    struct Claim {
+        int64_t j;
+        uint2 raw;
+    };
+    auto claim = [&]() -> Claim {
+        unsigned int k = 0u;
+        if (lane == 0) k = __hip_atomic_fetch_add(pp.claim(head), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        Claim c;
+        c.j = (int64_t)__builtin_amdgcn_readfirstlane(k);
+        c.raw = c.j < n_pages ? tab[c.j] : make_uint2(0u, 0u);
+        return c;
+    };
+    Claim ahead = claim();
+    Unit pending;                 // second and later units of a dense page
+    pending.e.kind = PKV_EMPTY;
+    pending.j = 0;
+    pending.half = 0;
+    auto next_unit = [&]() -> Unit {
+        if (pending.e.kind == PKV_DENSE) {
+            Unit u = pending;
+            const int next_half = u.half + 1;
+            if ((int64_t)next_half * UT >= min<int64_t>(P, T - u.j * P)) pending.e.kind = PKV_EMPTY;
+            else pending.half = next_half;
+            return u;
         }
-        return unpack_entry(batch, i & 63);
+        while (ahead.j < n_pages) {
+            Unit u;
+            u.e = unpack_entry(ahead.raw);
+            u.j = ahead.j;
+            u.half = 0;
+            ahead = claim();
+            if (u.e.kind == PKV_FACTOR) return u;
+            if (u.e.kind == PKV_DENSE) {
+                if (UT < min<int64_t>(P, T - u.j * P)) {
+                    pending = u;
+                    pending.half = 1;
+                }
+                return u;
+            }
+            if (lane == 0) raise_status(PKV_DEV_BAD_PAGE);
+        }
+        Unit none;
+        none.e.kind = PKV_EMPTY;
+        none.j = 0;
+        none.half = 0;
+        return none;
+    };
+    auto unit_rows = [&](const Unit &u) -> int {
+        return (int)min<int64_t>(UT, T - u.j * P - (int64_t)UT * u.half);
     };
 
     LaneOffs lo;
@@ -386,38 +448,29 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 2) void k_attn_mfma(Geo g, const p
         lo.av[rt] = 2u * (rank_row(rt, n) * P + (P >= 32 ? 8 : 4) * q4);
     }
     lo.tok0 = token_row<P>(0, n);
-    // The loop starts one step early with an empty page, so the loads of
-    // page 0 are issued by the loop body itself, in the order every later
-    // page's are: the waits the compiler places at the top of the body then
-    // count only the loads that page really needs.
+    // The loop starts one step early with an empty unit, so the loads of the
+    // first unit are issued by the loop body itself, in the order every later
+    // unit's are: the waits the compiler places at the top of the body then
+    // count only the loads that unit really needs. The page after the next
+    // is claimed one iteration ahead, hiding its table read.
     KeyOps<D, P> ko;
     ValueOps<D, P> vo;
-    pkv_page cur;
-    cur.kind = PKV_EMPTY;
-    PageRes res = page_res<D, P>(factor, g.factor_slot_bytes, cur);
-    for (int i = -1; i < n_mine; ++i) {
-        pkv_page nxt;
-        nxt.kind = PKV_EMPTY;
-        if (i + 1 < n_mine) nxt = entry_of(i + 1);
-        const PageRes nres = page_res<D, P>(factor, g.factor_slot_bytes, nxt);
+    Unit cur;
+    cur.e.kind = PKV_EMPTY;
+    cur.j = 0;
+    cur.half = 0;
+    Unit nxt = next_unit();
+    while (cur.e.kind != PKV_EMPTY || nxt.e.kind != PKV_EMPTY) {
+        const PageRes nres = unit_res<D, P>(factor, g.factor_slot_bytes, dense, g.dense_slot_bytes, nxt);
         bf16x8 eh[KS], el[KS];
-        if (cur.kind == PKV_FACTOR) factor_phase1<D, P>(w, ko, qb, eh, el, q4, c2);
+        const int rows = unit_rows(cur);
+        const bool live = cur.e.kind != PKV_EMPTY, dns = cur.e.kind == PKV_DENSE;
+        if (live) unit_phase1<D, P>(w, ko, qb, dns, rows, eh, el, q4, c2);
         issue_key_loads<D, P>(ko, nres, lo, n, q4);
-        if (cur.kind == PKV_FACTOR) factor_phase2<D, P>(w, vo, eh, el);
+        if (live) unit_phase2<D, P>(w, vo, dns, rows, eh, el, q4);
         issue_value_loads<D, P>(vo, nres, lo, n, q4);
         cur = nxt;
-        res = nres;
-    }
-    // Dense pages (a few per sequence: sink, window, last) after the stream,
-    // when the operand registers are free.
-    for (int i = 0; i < n_mine; ++i) {
-        const pkv_page e = entry_of(i);
-        if (e.kind == PKV_DENSE) {
-            const int64_t j = first + (int64_t)kMfmaWaves * i;
-            dense_page<D, P>(w, qb, dense, g.dense_slot_bytes, e.slot, (int)min<int64_t>(P, T - j * P), n, q4, c2);
-        } else if (e.kind != PKV_FACTOR && lane == 0) {
-            raise_status(PKV_DEV_BAD_PAGE);
-        }
+        nxt = next_unit();
     }
 
     // ---- merge the wave states (Eq. (5)) into the chunk's partial ---------
@@ -444,13 +497,13 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 2) void k_attn_mfma(Geo g, const p
             acc = fmaf(sc, s_o[ww][qi][k], acc);
             l = fmaf(sc, s_l[ww][qi], l);
         }
-        pp.o[pp.oi(head, qi, k, chunk)] = acc;
+        st_dev(&pp.o[pp.oi(head, qi, k, chunk)], acc);
         if (k == 0) {
-            pp.m[pp.mi(head, qi, chunk)] = M;
-            pp.l[pp.mi(head, qi, chunk)] = l;
+            st_dev(&pp.m[pp.mi(head, qi, chunk)], M);
+            st_dev(&pp.l[pp.mi(head, qi, chunk)], l);
         }
     }
-    publish_and_merge(g, head, pp, out, lse, T);
+    publish_and_merge<64 * kMfmaWaves>(g, head, pp, out, lse, T);
 }
 
 inline bool mfma_supported(const Geo &g) {

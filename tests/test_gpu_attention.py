@@ -144,9 +144,12 @@ def test_full_rank_factors_match_dense_fp32():
 
 
 def test_repeated_calls_share_workspace():
-    """The merge counters return to zero after every call: calls that reuse one
-    workspace give identical results, for both kernels (bf16 pages use the
-    matrix-core kernel, fp32 pages the generic one)."""
+    """The merge and page counters return to zero after every call, so calls
+    that reuse one workspace give the same results, for both kernels (bf16
+    pages use the matrix-core kernel, fp32 pages the generic one). The generic
+    kernel's chunks are fixed, so it repeats bit for bit; the matrix-core
+    kernel hands pages to waves dynamically, so its summation order (and the
+    last bits) may change between calls."""
     import torch
     import paper_2608_23843_amd as pk
     for dt, P in (("bf16", 64), ("f32", 16)):
@@ -164,5 +167,10 @@ def test_repeated_calls_share_workspace():
         first, lse0 = first.clone(), lse0.clone()
         for _ in range(3):
             out, lse = cache.attention(0, q, [P * 40, P * 33], workspace=ws)
-            assert torch.equal(out, first) and torch.equal(lse, lse0)
+            if dt == "f32":
+                assert torch.equal(out, first) and torch.equal(lse, lse0)
+            else:
+                scale = float(first.abs().max())
+                assert float((out - first).abs().max()) <= 1e-5 * scale
+                assert float((lse - lse0).abs().max()) <= 1e-5
         assert np.all(ws[-16:].cpu().numpy() == 0)
