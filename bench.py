@@ -242,6 +242,13 @@ def main():
     toks = [tuple(torch.from_numpy(x).to("cuda", bf).contiguous() for x in synth.decode_kv(wl, args.seed, 0, T + s))
             for s in range(n_steps)]
     stream = torch.cuda.current_stream()
+    # every event is created (and one pair exercised) before the timed region
+    pool = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in range(args.steps * layers)]
+    pool[0][0].record(stream)
+    pool[0][1].record(stream)
+    step_marks = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    torch.cuda.synchronize()
     call_events = []
     step_start = step_end = None
     compress_calls = 0
@@ -249,7 +256,7 @@ def main():
         timed = s >= args.warmup
         if s == args.warmup:
             torch.cuda.synchronize()
-            step_start = torch.cuda.Event(enable_timing=True)
+            step_start = step_marks[0]
             step_start.record(stream)
         pos = T + s
         new_pages = pk.eligible_pages(pos, pos + 1, P, S, W)
@@ -261,7 +268,7 @@ def main():
                 cache.compress_pages(layer, bb, hh, jj, rr, rr)
                 compress_calls += 1
             if timed:
-                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0, e1 = pool[len(call_events)]
                 e0.record(stream)
             cache.attention(layer, qs[s], [pos + 1] * B, out=out, lse=lse, workspace=ws)
             if timed:
@@ -270,7 +277,7 @@ def main():
         if s == 0:
             torch.cuda.synchronize()
             log("first step done")
-    step_end = torch.cuda.Event(enable_timing=True)
+    step_end = step_marks[1]
     step_end.record(stream)
     torch.cuda.synchronize()
     status |= cache.device_status()
@@ -278,8 +285,11 @@ def main():
     ms_per_step = ms_total / args.steps
     call_ms = np.array([a.elapsed_time(b) for a, b in call_events])
     attn_us = float(call_ms.mean() * 1e3)
-    log("decode: %.3f ms/step, attention %.1f us/layer (median %.1f), status %d"
-        % (ms_per_step, attn_us, float(np.median(call_ms) * 1e3), status))
+    pct = np.percentile(call_ms * 1e3, [10, 50, 90, 99])
+    log("decode: %.3f ms/step, attention %.1f us/layer (p10 %.1f, median %.1f, p90 %.1f, p99 %.1f, max %.1f), "
+        "status %d" % (ms_per_step, attn_us, pct[0], pct[1], pct[2], pct[3], float(call_ms.max() * 1e3), status))
+    per_step = call_ms.reshape(args.steps, layers).mean(axis=1) * 1e3
+    log("attention us/layer by timed step: " + " ".join("%.1f" % x for x in per_step))
     if not np.isfinite(out.float().cpu().numpy()).all():
         raise RuntimeError("non-finite attention output")
 
