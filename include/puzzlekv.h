@@ -47,7 +47,7 @@ typedef enum {
     PKV_E_HIP = 7          /* HIP runtime error; pkv_last_error() has its text */
 } pkv_status;
 
-/* Element types. PKV_INT4 is a factor storage type only (reserved). */
+/* Element types. PKV_INT4 is a factor storage type only (see below). */
 typedef enum { PKV_F32 = 0, PKV_BF16 = 1, PKV_INT4 = 2 } pkv_dtype;
 
 /* Kind of a logical page. */
@@ -97,6 +97,19 @@ typedef struct {
  * for e * (P r4(rk) + rk d + rv P + d r4(rv)) bytes (pkv_factor_page_bytes).
  * Every operand is stored with its contraction index contiguous, the order
  * the attention kernel streams it in.
+ *
+ * INT4 factors (factor_dtype PKV_INT4; Section 4.3 "Quantization
+ * Compatibility"): a factor page stores the balanced factors
+ * L~ = U Sigma^(1/2) and R~ = Sigma^(1/2) W^T of K and V, each quantized to
+ * symmetric 4-bit codes in [-7, 7] with one fp16 scale per run of up to 32
+ * consecutive elements along the paper's direction: column-wise for L~_K,
+ * R~_K and R~_V, row-wise for L~_V. Scale = fp16(max|x| / 7) rounded to
+ * nearest even; code = x / scale rounded half to even (exactly, as in fp64);
+ * a zero scale gives zero codes. Needs bf16 dense pages, P = 64,
+ * head_dim = 128 and max_rank <= 32; the slot layout is internal (codes
+ * packed eight to a 32-bit word in the order the attention kernel reads
+ * them), pkv_factor_page_bytes gives its size (5,344 bytes at ranks 24/24).
+ * Pages enter and leave in the canonical blob of pkv_int4_blob_bytes.
  */
 typedef struct {
     int32_t n_layers;
@@ -110,7 +123,7 @@ typedef struct {
     int32_t sink_tokens;   /* S >= 0 */
     int32_t window_tokens; /* W >= 0 */
     int32_t dense_dtype;   /* PKV_F32 or PKV_BF16 (also the query dtype) */
-    int32_t factor_dtype;  /* PKV_F32 or PKV_BF16 */
+    int32_t factor_dtype;  /* PKV_F32, PKV_BF16 or PKV_INT4 */
     void *dense_pool;      /* device */
     void *factor_pool;     /* device */
     pkv_page *page_table;  /* device */
@@ -218,8 +231,9 @@ pkv_status pkv_mixed_decode_attention(const pkv_cache *c, int32_t layer, const v
  * pkv_import_pages writes n pages of `layer`: b, kv_head, page, kind, rank_k,
  * rank_v, src_offset are host [n]; src is a device array in the destination
  * dtype (dense_dtype for dense pages, factor_dtype for factor pages) and page
- * i's block starts src_offset[i] elements into it. The page-table entry is set.
- * Workspace: pkv_workspace_bytes(PKV_OP_IMPORT, n). */
+ * i's block starts src_offset[i] elements into it (for INT4 factor pages the
+ * block is the canonical INT4 blob and src_offset[i] counts bytes). The
+ * page-table entry is set. Workspace: pkv_workspace_bytes(PKV_OP_IMPORT, n). */
 pkv_status pkv_import_pages(const pkv_cache *c, int32_t layer, int32_t n, const int32_t *b,
                             const int32_t *kv_head, const int32_t *page, const uint8_t *kind,
                             const uint8_t *rank_k, const uint8_t *rank_v, const void *src,
@@ -228,11 +242,26 @@ pkv_status pkv_import_pages(const pkv_cache *c, int32_t layer, int32_t n, const 
 /* pkv_export_pages reads n pages of `layer` as fp32 into dst (device), page i
  * at dst + i * pkv_export_block_elems(c): DENSE as K, V (P x d each); FACTOR as
  * L_K (P x max_rank), R_K (max_rank x d), L_V (P x max_rank), R_V (max_rank x d)
- * with entries past the page's ranks zero; EMPTY as zeros. */
+ * with entries past the page's ranks zero; EMPTY as zeros. INT4 factor pages
+ * come out dequantized (code x scale) as the balanced factors L~, R~. */
 int64_t pkv_export_block_elems(const pkv_cache *c);
 pkv_status pkv_export_pages(const pkv_cache *c, int32_t layer, int32_t n, const int32_t *b,
                             const int32_t *kv_head, const int32_t *page, float *dst, void *ws,
                             size_t ws_bytes, pkv_stream s);
+
+/* Canonical INT4 page blob (import and pkv_export_int4_pages): int8 codes
+ * L~_K [P][rk], R~_K [rk][d], L~_V [P][rv], R~_V [rv][d] (row-major), then
+ * fp16 scales L~_K [P/32][rk] (run u covers tokens 32u..32u+31 of column a),
+ * R~_K [d], L~_V [P], R~_V [d] (one run per line since ranks are <= 32).
+ * Returns its size in bytes, or -1 if the cache is not INT4 or the ranks are
+ * outside 1..max_rank. For INT4 factor pages pkv_import_pages reads this blob
+ * at src + src_offset[i] bytes (dense pages keep element offsets). */
+int64_t pkv_int4_blob_bytes(const pkv_cache *c, int32_t rank_k, int32_t rank_v);
+/* Writes the blobs of n INT4 factor pages to dst (device), page i at
+ * dst + i * pkv_int4_blob_bytes(c, max_rank, max_rank); a page that is not a
+ * factor page gives zeros. */
+pkv_status pkv_export_int4_pages(const pkv_cache *c, int32_t layer, int32_t n, const int32_t *b,
+                                 const int32_t *kv_head, const int32_t *page, void *dst, pkv_stream s);
 
 /* ---- diagnostics --------------------------------------------------------- */
 

@@ -13,13 +13,14 @@ import ctypes
 import numpy as np
 
 from . import _lib
-from ._lib import (PKV_BF16, PKV_DENSE, PKV_EMPTY, PKV_F32, PKV_FACTOR, PKV_OP_ATTENTION,
+from ._lib import (PKV_BF16, PKV_DENSE, PKV_EMPTY, PKV_F32, PKV_FACTOR, PKV_INT4, PKV_OP_ATTENTION,
                    PKV_OP_COMPRESS, PKV_OP_IMPORT, PKV_OP_PREFILL, PuzzleKVError, check)
 
 __all__ = ["PuzzleKVCache", "plan_pages", "eligible_pages", "load_library", "PuzzleKVError",
-           "PKV_EMPTY", "PKV_DENSE", "PKV_FACTOR", "PKV_F32", "PKV_BF16"]
+           "PKV_EMPTY", "PKV_DENSE", "PKV_FACTOR", "PKV_F32", "PKV_BF16", "PKV_INT4"]
 
-_DTYPES = {"f32": PKV_F32, "fp32": PKV_F32, "float32": PKV_F32, "bf16": PKV_BF16, "bfloat16": PKV_BF16}
+_DTYPES = {"f32": PKV_F32, "fp32": PKV_F32, "float32": PKV_F32, "bf16": PKV_BF16, "bfloat16": PKV_BF16,
+           "int4": PKV_INT4}
 
 
 def load_library():
@@ -97,7 +98,7 @@ class PuzzleKVCache:
         c.page_table = self.table.data_ptr()
         check(lib.pkv_cache_check(ctypes.byref(c)), "PuzzleKVCache")
         self.qdtype = torch.bfloat16 if c.dense_dtype == PKV_BF16 else torch.float32
-        self.fdtype = torch.bfloat16 if c.factor_dtype == PKV_BF16 else torch.float32
+        self.fdtype = {PKV_BF16: torch.bfloat16, PKV_F32: torch.float32, PKV_INT4: torch.uint8}[c.factor_dtype]
         self.reset()
 
     # ---- geometry ----------------------------------------------------------
@@ -201,6 +202,22 @@ class PuzzleKVCache:
                                         _np_ptr(page), _np_ptr(kind), _np_ptr(rk), _np_ptr(rv),
                                         src.data_ptr(), _np_ptr(off), None, 0,
                                         _stream_handle(self.torch, stream)), "pkv_import_pages")
+
+    def int4_blob_bytes(self, rank_k: int, rank_v: int) -> int:
+        """Size of the canonical INT4 page blob (pkv_int4_blob_bytes)."""
+        return int(self.lib.pkv_int4_blob_bytes(ctypes.byref(self.c), rank_k, rank_v))
+
+    def export_int4_pages(self, layer, b, h, page, stream=None):
+        """Returns a device uint8 tensor (n, blob bytes at max_rank) of canonical INT4 blobs."""
+        torch = self.torch
+        b, h, page = _i32(b), _i32(h), _i32(page)
+        n = b.size
+        blk = self.int4_blob_bytes(self.c.max_rank, self.c.max_rank)
+        dst = torch.zeros((max(n, 1), blk), dtype=torch.uint8, device=self.device)
+        check(self.lib.pkv_export_int4_pages(ctypes.byref(self.c), layer, n, _np_ptr(b), _np_ptr(h),
+                                             _np_ptr(page), dst.data_ptr(), _stream_handle(torch, stream)),
+              "pkv_export_int4_pages")
+        return dst[:n]
 
     def export_block_elems(self) -> int:
         return int(self.lib.pkv_export_block_elems(ctypes.byref(self.c)))

@@ -13,7 +13,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libpuzzlekv.so")
 
 SOURCES = ["pkv_kernels.hip", "pkv_host.cpp"]
-DEPS = ["pkv_internal.h", "cache_ops.inl", "compress.inl", "attention.inl", "attention_mfma.inl",
+DEPS = ["pkv_internal.h", "cache_ops.inl", "int4.inl", "compress.inl", "attention.inl", "attention_mfma.inl", "attention_q4.inl",
         "attention_launch.inl"]
 
 

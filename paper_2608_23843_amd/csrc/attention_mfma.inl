@@ -41,6 +41,7 @@ typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kMfmaWaves = 8;
+constexpr int kQ4DenseStage = 256;   // dense pages of one head a workgroup can queue (INT4 kernel)
 // The running max (log2 units) is raised only when a score exceeds it by more
 // than this; below that the exp weights stay under 2^32 and the fp32 sums
 // cannot overflow, so most pages skip the cross-lane max and the rescale.
@@ -209,14 +210,13 @@ struct WaveState {
     float m_run;
 };
 
-// Online softmax over one page's raw scores st (Eq. (5) state update);
-// leaves the exp weights as hi/lo B operands of the token contraction and
-// adds them to the normalizer. Rows at or past `rows` are masked (dense pages
-// only; factor pages are complete).
+// Online softmax over one page's raw scores st (Eq. (5) state update): the
+// running max is raised (and the state rescaled) only when needed, then st
+// holds the exp weights. Rows at or past `rows` are masked (dense pages only;
+// factor pages are complete).
 template <int D, int P, bool MASK>
-__device__ inline void page_softmax(WaveState<D> &w, f32x4 (&st)[P / 16], bf16x8 (&eh)[(P + 31) / 32],
-                                    bf16x8 (&el)[(P + 31) / 32], int rows, int q, float c2) {
-    constexpr int TT = P / 16, KS = (P + 31) / 32, DT = D / 16;
+__device__ inline void page_exp(WaveState<D> &w, f32x4 (&st)[P / 16], int rows, int q, float c2) {
+    constexpr int TT = P / 16, DT = D / 16;
     float pm = -INFINITY;
 #pragma unroll
     for (int tt = 0; tt < TT; ++tt)
@@ -240,6 +240,15 @@ __device__ inline void page_softmax(WaveState<D> &w, f32x4 (&st)[P / 16], bf16x8
     for (int tt = 0; tt < TT; ++tt)
 #pragma unroll
         for (int v = 0; v < 4; ++v) st[tt][v] = __builtin_amdgcn_exp2f(fmaf(st[tt][v], c2, nm));
+}
+
+// bf16 pages: the exp weights become hi/lo B operands of the token
+// contraction, and the normalizer (every row of w.l) is a ones x E^T product.
+template <int D, int P, bool MASK>
+__device__ inline void page_softmax(WaveState<D> &w, f32x4 (&st)[P / 16], bf16x8 (&eh)[(P + 31) / 32],
+                                    bf16x8 (&el)[(P + 31) / 32], int rows, int q, float c2) {
+    constexpr int TT = P / 16, KS = (P + 31) / 32;
+    page_exp<D, P, MASK>(w, st, rows, q, c2);
     const bf16x8 ones = bf16x8{1, 1, 1, 1, 1, 1, 1, 1};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
@@ -248,6 +257,17 @@ __device__ inline void page_softmax(WaveState<D> &w, f32x4 (&st)[P / 16], bf16x8
         w.l = mfma_bf16(ones, eh[ks], w.l);
         w.l = mfma_bf16(ones, el[ks], w.l);
     }
+}
+
+// INT4 pages: the exp weights stay fp32 (phase 2 scales them); w.l[0] keeps
+// this lane's share of the normalizer.
+template <int D, int P, bool MASK>
+__device__ inline void page_softmax_exp(WaveState<D> &w, f32x4 (&st)[P / 16], int rows, int q, float c2) {
+    page_exp<D, P, MASK>(w, st, rows, q, c2);
+    float s = 0.f;
+#pragma unroll
+    for (int tt = 0; tt < P / 16; ++tt) s += (st[tt][0] + st[tt][1]) + (st[tt][2] + st[tt][3]);
+    w.l[0] += s;
 }
 
 // Phase 1 of a unit. Factor page: Z^T = R_K Q^T, S^T = L_K Z^T, softmax.
@@ -323,6 +343,12 @@ __device__ inline void unit_phase2(WaveState<D> &w, const ValueOps<D, P> &f, boo
     }
 }
 
+}  // namespace pkv
+
+#include "attention_q4.inl"
+
+namespace pkv {
+
 // A page-table entry read at a wave-uniform address, as scalars: the page's
 // buffer resources then live in scalar registers.
 __device__ inline pkv_page unpack_entry(uint2 ent) {
@@ -343,7 +369,7 @@ __device__ inline pkv_page unpack_entry(uint2 ent) {
 // with page i+1's while phase 2 of page i reads the value operands, refilled
 // in turn with page i+1's. One operand set per wave keeps the register budget
 // at two waves per SIMD.
-template <int D, int P>
+template <int D, int P, bool Q4>
 __global__ __launch_bounds__(64 * kMfmaWaves, 1) void k_attn_mfma(Geo g, const pkv_page *__restrict__ table,
                                                                   const char *__restrict__ dense,
                                                                   const char *__restrict__ factor,
@@ -402,6 +428,63 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 1) void k_attn_mfma(Geo g, const p
         c.raw = c.j < n_pages ? tab[c.j] : make_uint2(0u, 0u);
         return c;
     };
+    if constexpr (Q4) {
+        // INT4 factor pages stream through the pipelined loop; dense pages met
+        // on the way are queued (a head has at most as many dense pages as
+        // dense slots, which the host keeps within the queue) and done after.
+        __shared__ int s_dense[kQ4DenseStage];
+        __shared__ unsigned int s_nd;
+        if (threadIdx.x == 0) s_nd = 0u;
+        __syncthreads();
+        f16x8 qh[4];
+#pragma unroll
+        for (int s = 0; s < 4; ++s)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) qh[s][e] = (_Float16)(float)qb[s][e];
+        Claim ahead = claim();
+        auto next_factor = [&]() -> pkv_page {
+            while (ahead.j < n_pages) {
+                const pkv_page e = unpack_entry(ahead.raw);
+                const int64_t j = ahead.j;
+                ahead = claim();
+                if (e.kind == PKV_FACTOR) return e;
+                if (lane == 0) {
+                    if (e.kind == PKV_DENSE) {
+                        const unsigned int di = atomicAdd(&s_nd, 1u);
+                        if (di < (unsigned int)kQ4DenseStage) s_dense[di] = (int)j;
+                    } else {
+                        raise_status(PKV_DEV_BAD_PAGE);
+                    }
+                }
+            }
+            pkv_page none;
+            none.kind = PKV_EMPTY;
+            return none;
+        };
+        Q4Key ko;
+        Q4Val vo;
+        pkv_page cur;
+        cur.kind = PKV_EMPTY;
+        pkv_page nxt = next_factor();
+        while (cur.kind == PKV_FACTOR || nxt.kind == PKV_FACTOR) {
+            const Q4Res nres = q4_res(factor, g.factor_slot_bytes, nxt);
+            f32x4 st[4];
+            const bool live = cur.kind == PKV_FACTOR;
+            if (live) q4_phase1<D>(w, ko, qh, st, q4, c2);
+            q4_issue_key_loads(ko, nres, n, q4);
+            if (live) q4_phase2<D>(w, vo, st);
+            q4_issue_value_loads(vo, nres, n, q4);
+            cur = nxt;
+            nxt = next_factor();
+        }
+        __syncthreads();
+        const int nd = (int)min(s_nd, (unsigned int)kQ4DenseStage);
+        for (int i = wave; i < nd; i += kMfmaWaves) {
+            const int64_t j = s_dense[i];
+            const pkv_page e = unpack_entry(tab[j]);
+            q4_dense_page<D>(w, qb, dense, g.dense_slot_bytes, e.slot, (int)min<int64_t>(P, T - j * P), n, q4, c2);
+        }
+    } else {
     Claim ahead = claim();
     Unit pending;                 // second and later units of a dense page
     pending.e.kind = PKV_EMPTY;
@@ -472,13 +555,19 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 1) void k_attn_mfma(Geo g, const p
         cur = nxt;
         nxt = next_unit();
     }
+    }
 
     // ---- merge the wave states (Eq. (5)) into the chunk's partial ---------
     __shared__ float s_m[kMfmaWaves][16], s_l[kMfmaWaves][16];
     __shared__ float s_o[kMfmaWaves][16][D];
+    float l_col = w.l[0];
+    if constexpr (Q4) {   // lane shares of the normalizer
+        l_col += __shfl_xor(l_col, 16, 64);
+        l_col += __shfl_xor(l_col, 32, 64);
+    }
     if (q4 == 0) {
         s_m[wave][n] = w.m_run;
-        s_l[wave][n] = w.l[0];
+        s_l[wave][n] = l_col;
     }
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt)
@@ -507,6 +596,7 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 1) void k_attn_mfma(Geo g, const p
 }
 
 inline bool mfma_supported(const Geo &g) {
+    if (g.factor_dtype == PKV_INT4) return true;   // validated on the host (bf16 dense, P = 64, d = 128)
     return g.dense_dtype == PKV_BF16 && g.factor_dtype == PKV_BF16 && (g.d == 64 || g.d == 128) &&
            (g.P == 16 || g.P == 32 || g.P == 64) && g.max_rank <= 32 && g.g <= 16;
 }
@@ -517,9 +607,12 @@ hipError_t launch_attn_mfma(const LaunchCtx &L, const AttnPlan &plan, const uint
     const Geo &g = L.geo;
     dim3 grid(plan.n_chunks, g.B * g.Hkv);
 #define PKV_LAUNCH_MFMA(DD, PP)                                                                         \
-    hipLaunchKernelGGL((k_attn_mfma<DD, PP>), grid, dim3(64 * kMfmaWaves), 0, L.stream, g, p.table, p.dense, \
-                       p.factor, q, seq, plan.pages_per_chunk, plan.n_chunks, pp, out, lse)
-    if (g.d == 128) {
+    hipLaunchKernelGGL((k_attn_mfma<DD, PP, false>), grid, dim3(64 * kMfmaWaves), 0, L.stream, g, p.table,   \
+                       p.dense, p.factor, q, seq, plan.pages_per_chunk, plan.n_chunks, pp, out, lse)
+    if (g.factor_dtype == PKV_INT4) {
+        hipLaunchKernelGGL((k_attn_mfma<128, 64, true>), grid, dim3(64 * kMfmaWaves), 0, L.stream, g, p.table,
+                           p.dense, p.factor, q, seq, plan.pages_per_chunk, plan.n_chunks, pp, out, lse);
+    } else if (g.d == 128) {
         if (g.P == 64) PKV_LAUNCH_MFMA(128, 64);
         else if (g.P == 32) PKV_LAUNCH_MFMA(128, 32);
         else PKV_LAUNCH_MFMA(128, 16);

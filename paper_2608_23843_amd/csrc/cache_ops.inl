@@ -243,6 +243,7 @@ __global__ __launch_bounds__(256) void k_import(Geo g, pkv_page *table, char *de
 }
 
 hipError_t launch_import(const LaunchCtx &L, const CopyItems &items, const void *src) {
+    if (L.geo.factor_dtype == PKV_INT4) return launch_import_q4(L, items, src);
     LayerPtrs p = layer_ptrs(L);
     dim3 grid(items.n);
     const bool db = L.geo.dense_dtype == PKV_BF16, fb = L.geo.factor_dtype == PKV_BF16;
@@ -306,6 +307,7 @@ __global__ __launch_bounds__(256) void k_export(Geo g, const pkv_page *table, co
 }
 
 hipError_t launch_export(const LaunchCtx &L, const CopyItems &items, float *dst, int64_t block) {
+    if (L.geo.factor_dtype == PKV_INT4) return launch_export_dq4(L, items, dst, block);
     LayerPtrs p = layer_ptrs(L);
     dim3 grid(items.n);
     const bool db = L.geo.dense_dtype == PKV_BF16, fb = L.geo.factor_dtype == PKV_BF16;

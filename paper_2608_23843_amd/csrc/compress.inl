@@ -28,6 +28,11 @@ struct CompressSrc {
 
 __device__ inline float wave_shfl_xor(float v, int m) { return __shfl_xor(v, m, 64); }
 
+// Factor storage marker for INT4 pages (balanced, quantized factors).
+struct q4_t {};
+template <typename TF> struct is_q4 { static constexpr bool value = false; };
+template <> struct is_q4<q4_t> { static constexpr bool value = true; };
+
 template <typename TX, typename TF, int P>
 __global__ __launch_bounds__(64) void k_compress(Geo g, pkv_page *table, const char *dense, char *factor,
                                                  CompressItems items, CompressSrc src, int64_t n_decomp) {
@@ -178,6 +183,36 @@ __global__ __launch_bounds__(64) void k_compress(Geo g, pkv_page *table, const c
 
     if (!active) return;
 
+    if constexpr (is_q4<TF>::value) {
+        // ---- INT4 outputs (Section 4.3): balance by Sigma^(1/2), quantize --------
+        // sigma = sqrt(lambda); L~ column = L column * sigma^(1/2), R~ row =
+        // R row / sigma^(1/2) (zero where sigma is zero), staged in LDS after X.
+        float *sL = (float *)(sX_all + (int64_t)P * ld_x);   // P x 32
+        float *sR = sL + P * 32;                              // 32 x d
+        float *sScale = sR + 32 * d;                          // (P/32) r8 + d <= 64 + d
+        const int r = which == 0 ? rk : rv;
+        const float root = sqrtf(sqrtf(fmaxf(lam, 0.f)));
+        const float inv = root > 0.f ? 1.f / root : 0.f;
+        if (rho < r)
+            for (int t = 0; t < P; ++t) sL[t * 32 + rho] = jcol[t] * root;
+        for (int k0 = 0; k0 < d; k0 += 16) {
+            float acc[16];
+#pragma unroll
+            for (int u = 0; u < 16; ++u) acc[u] = 0.f;
+            for (int t = 0; t < P; ++t) {
+                const float lt = jcol[t];
+#pragma unroll
+                for (int u = 0; u < 16; ++u) acc[u] = fmaf(lt, to_f32(sX[t * ld_x + k0 + u]), acc[u]);
+            }
+            if (rho < r)
+#pragma unroll
+                for (int u = 0; u < 16; ++u) sR[rho * d + k0 + u] = acc[u] * inv;
+        }
+        __syncthreads();
+        const Int4Layout f4 = int4_layout(P, d, rk, rv);
+        char *slot4 = factor + (g.head_index(b, h) * g.max_pages + j) * g.factor_slot_bytes;
+        q4_quantize_store(slot4, f4, P, d, r, which, sL, sR, sScale, lane);
+    } else {
     // ---- outputs ------------------------------------------------------------
     const int rk4 = r4(rk), rv4 = r4(rv);
     const FactorLayout fl = factor_layout(P, d, rk, rv);
@@ -213,6 +248,7 @@ __global__ __launch_bounds__(64) void k_compress(Geo g, pkv_page *table, const c
         }
     }
     (void)r; (void)rr4;
+    }
 }
 
 template <typename TX, typename TF, int P>
@@ -220,7 +256,8 @@ hipError_t launch_compress_t(const LaunchCtx &L, const CompressItems &items, con
                              int64_t n_decomp) {
     constexpr int D = 64 / P;
     const int pad = sizeof(TX) == 2 ? 2 : 1;
-    const size_t smem = (size_t)D * P * (L.geo.d + pad) * sizeof(TX);
+    size_t smem = (size_t)D * P * (L.geo.d + pad) * sizeof(TX);
+    if (is_q4<TF>::value) smem += (size_t)(P * 32 + 32 * L.geo.d + 64 + L.geo.d) * sizeof(float);
     const int64_t blocks = ceil_div(n_decomp, D);
     LayerPtrs p = layer_ptrs(L);
     hipLaunchKernelGGL((k_compress<TX, TF, P>), dim3((unsigned)blocks), dim3(64), smem, L.stream, L.geo,
@@ -242,6 +279,10 @@ hipError_t launch_compress_p(const LaunchCtx &L, const CompressItems &items, con
 hipError_t launch_compress_any(const LaunchCtx &L, const CompressItems &items, const CompressSrc &src,
                                int64_t n_decomp) {
     if (n_decomp <= 0) return hipSuccess;
+    if (L.geo.factor_dtype == PKV_INT4) {   // validated: bf16 dense pages, P = 64
+        if (L.geo.P != 64 || L.geo.dense_dtype != PKV_BF16) return hipErrorInvalidValue;
+        return launch_compress_t<uint16_t, q4_t, 64>(L, items, src, n_decomp);
+    }
     const bool db = L.geo.dense_dtype == PKV_BF16, fb = L.geo.factor_dtype == PKV_BF16;
     if (db && fb) return launch_compress_p<uint16_t, uint16_t>(L, items, src, n_decomp);
     if (db) return launch_compress_p<uint16_t, float>(L, items, src, n_decomp);

@@ -54,9 +54,22 @@ pkv_status check_geometry(const pkv_cache *c) {
     if (c->sink_tokens < 0 || c->window_tokens < 0)
         return fail(PKV_E_SHAPE, "sink and window must be non-negative");
     if (elem_size(c->dense_dtype) == 0) return fail(PKV_E_UNSUPPORTED, "dense dtype %d", c->dense_dtype);
+    if (c->factor_dtype == PKV_INT4) {
+        if (c->dense_dtype != PKV_BF16 || c->page_size != 64 || c->head_dim != 128 || c->max_rank > 32)
+            return fail(PKV_E_UNSUPPORTED,
+                        "INT4 factors need bf16 dense pages, P = 64, head_dim = 128 and max_rank <= 32");
+        if (ceil_div(c->sink_tokens, c->page_size) + ceil_div(c->window_tokens, c->page_size) + 2 > 256)
+            return fail(PKV_E_UNSUPPORTED, "INT4 factors need at most 256 dense slots per head");
+        return PKV_OK;
+    }
     if (elem_size(c->factor_dtype) == 0)
         return fail(PKV_E_UNSUPPORTED, "factor dtype %d", c->factor_dtype);
     return PKV_OK;
+}
+
+int64_t factor_page_bytes_of(int dtype, int P, int d, int rk, int rv) {
+    if (dtype == PKV_INT4) return int4_layout(P, d, rk, rv).end;
+    return factor_page_elems(P, d, rk, rv) * elem_size(dtype);
 }
 
 Geo make_geo(const pkv_cache *c) {
@@ -79,7 +92,7 @@ Geo make_geo(const pkv_cache *c) {
     g.dense_dtype = c->dense_dtype;
     g.factor_dtype = c->factor_dtype;
     g.dense_slot_bytes = 2LL * g.P * g.d * g.dense_es;
-    int64_t fb = factor_page_elems(g.P, g.d, g.max_rank, g.max_rank) * g.factor_es;
+    int64_t fb = factor_page_bytes_of(c->factor_dtype, g.P, g.d, g.max_rank, g.max_rank);
     g.factor_slot_bytes = (fb + 255) / 256 * 256;
     g.layer_entries = (int64_t)g.B * g.Hkv * g.max_pages;
     g.layer_dense_bytes = (int64_t)g.B * g.Hkv * g.dslots * g.dense_slot_bytes;
@@ -161,8 +174,12 @@ size_t pkv_page_table_bytes(const pkv_cache *c) {
 size_t pkv_factor_page_bytes(const pkv_cache *c, int32_t rank_k, int32_t rank_v) {
     if (check_geometry(c) != PKV_OK) return 0;
     if (rank_k < 1 || rank_v < 1 || rank_k > c->max_rank || rank_v > c->max_rank) return 0;
-    return (size_t)(factor_page_elems(c->page_size, c->head_dim, rank_k, rank_v) *
-                    elem_size(c->factor_dtype));
+    return (size_t)factor_page_bytes_of(c->factor_dtype, c->page_size, c->head_dim, rank_k, rank_v);
+}
+int64_t pkv_int4_blob_bytes(const pkv_cache *c, int32_t rank_k, int32_t rank_v) {
+    if (check_geometry(c) != PKV_OK || c->factor_dtype != PKV_INT4) return -1;
+    if (rank_k < 1 || rank_v < 1 || rank_k > c->max_rank || rank_v > c->max_rank) return -1;
+    return int4_blob_bytes(c->page_size, c->head_dim, rank_k, rank_v);
 }
 int64_t pkv_export_block_elems(const pkv_cache *c) {
     if (check_geometry(c) != PKV_OK) return -1;
@@ -432,6 +449,38 @@ pkv_status pkv_export_pages(const pkv_cache *c, int32_t layer, int32_t n, const 
             it.src_off = (int64_t)x * block;
         }
         if ((st = check_launch(launch_export(L, items, dst, block), "pkv_export_pages")) != PKV_OK) return st;
+    }
+    return PKV_OK;
+}
+
+pkv_status pkv_export_int4_pages(const pkv_cache *c, int32_t layer, int32_t n, const int32_t *b,
+                                 const int32_t *kv_head, const int32_t *page, void *dst, pkv_stream s) {
+    pkv_status st = check_cache(c, true);
+    if (st != PKV_OK) return st;
+    if (c->factor_dtype != PKV_INT4) return fail(PKV_E_ARG, "the cache's factor dtype is not PKV_INT4");
+    if ((st = check_layer(c, layer)) != PKV_OK) return st;
+    if (n < 0) return fail(PKV_E_ARG, "n < 0");
+    if (n == 0) return PKV_OK;
+    if (!b || !kv_head || !page || !dst) return fail(PKV_E_ARG, "NULL argument");
+    LaunchCtx L = ctx(c, layer, s);
+    const int64_t block = int4_blob_bytes(c->page_size, c->head_dim, c->max_rank, c->max_rank);
+    for (int base = 0; base < n; base += kCopyItemsPerLaunch) {
+        CopyItems items{};
+        items.n = std::min(kCopyItemsPerLaunch, n - base);
+        for (int i = 0; i < items.n; ++i) {
+            int x = base + i;
+            if (b[x] < 0 || b[x] >= c->batch || kv_head[x] < 0 || kv_head[x] >= c->n_kv_heads ||
+                page[x] < 0 || page[x] >= c->max_pages)
+                return fail(PKV_E_ARG, "page ref %d out of range", x);
+            CopyItem &it = items.it[i];
+            it.b = b[x];
+            it.h = kv_head[x];
+            it.j = page[x];
+            it.src_off = (int64_t)x * block;
+        }
+        if ((st = check_launch(launch_export_int4(L, items, (char *)dst, block), "pkv_export_int4_pages")) !=
+            PKV_OK)
+            return st;
     }
     return PKV_OK;
 }

@@ -38,6 +38,48 @@ __host__ __device__ inline FactorLayout factor_layout(int P, int d, int rk, int 
     return f;
 }
 
+// INT4 factor slot (factor dtype PKV_INT4; P = 64, d = 128, ranks <= 32).
+// Codes are 4-bit two's complement, eight to a dword with element e at bit
+// int4_nib(e); scales are fp16. Byte offsets of the sections, in order:
+//   akc  A_K codes      [kq][i][tt] dwords: token row tau(tt, i), ranks 8kq + e
+//   aks  A_K scales     [kq][run][e]: column-wise runs of 32 tokens, rank 8kq + e
+//   bks  B_K scales     [kq][s][e]: dim 32s + 8kq + e (column-wise, one run)
+//   bkc  B_K codes      [a][kq][s] dwords: rank row a, dims 32s + 8kq + e
+//   bvc  B_V^T codes    [kq][i][dt] dwords: dim 16dt + i, ranks 8kq + e
+//   bvs  B_V scales     [q][dt][v]: dim 16dt + 4q + v (column-wise, one run)
+//   avs  A_V scales     [q][tt][v]: token tau(tt, 4q + v) (row-wise, one run)
+//   avc  A_V^T codes    [i][kq][rt][ks] dwords: rank row pi(rt, i), tokens 32ks + 8kq + e
+// where pi and tau are the attention kernel's tile row maps. Each section is
+// ordered so that one lane of that kernel reads its operand slice as one
+// 16-byte piece, and the sections whose rows can pass the page's rank (bkc,
+// avc) end the key and value halves, so those reads fall outside the page.
+__host__ __device__ inline int r8(int r) { return (r + 7) & ~7; }
+__host__ __device__ inline int int4_nib(int e) { return 4 * (e >> 1) + 16 * (e & 1); }
+struct Int4Layout {
+    int64_t akc, aks, bks, bkc, keys_end, bvc, bvs, avs, avc, end;
+};
+__host__ __device__ inline Int4Layout int4_layout(int P, int d, int rk, int rv) {
+    Int4Layout f;
+    f.akc = 0;
+    f.aks = f.akc + (int64_t)r8(rk) * P / 2;
+    f.bks = f.aks + (int64_t)r8(rk) * (P / 32) * 2;
+    f.bkc = f.bks + 2LL * d;
+    f.keys_end = f.bkc + (int64_t)rk * d / 2;
+    f.bvc = f.keys_end;
+    f.bvs = f.bvc + (int64_t)r8(rv) * d / 2;
+    f.avs = f.bvs + 2LL * d;
+    f.avc = f.avs + 2LL * P;
+    f.end = f.avc + (int64_t)r8(rv) * P / 2;
+    return f;
+}
+// Tile row maps shared by the INT4 layout and the attention kernel: rank tile
+// rt, row m -> rank 8(m/4) + 4rt + m%4; token tile tt, row m -> token
+// 32(tt/2) + 8(m/4) + 4(tt%2) + m%4 (P >= 32).
+__host__ __device__ inline int tile_rank_row(int rt, int m) { return 8 * (m >> 2) + 4 * rt + (m & 3); }
+__host__ __device__ inline int tile_token_row(int tt, int m) {
+    return 32 * (tt >> 1) + 8 * (m >> 2) + 4 * (tt & 1) + (m & 3);
+}
+
 // Kind of logical page j of a sequence of T tokens (sink S, window W tokens).
 __host__ __device__ inline int plan_kind(int64_t T, int P, int S, int W, int64_t j) {
     if (j < 0 || j * P >= T) return PKV_EMPTY;
@@ -138,6 +180,16 @@ hipError_t launch_compress(const LaunchCtx &L, const CompressItems &items);
 hipError_t launch_compress_commit(const LaunchCtx &L, const CompressItems &items);
 hipError_t launch_import(const LaunchCtx &L, const CopyItems &items, const void *src);
 hipError_t launch_export(const LaunchCtx &L, const CopyItems &items, float *dst, int64_t block);
+hipError_t launch_export_int4(const LaunchCtx &L, const CopyItems &items, char *dst, int64_t block_bytes);
+hipError_t launch_import_q4(const LaunchCtx &L, const CopyItems &items, const void *src);
+hipError_t launch_export_dq4(const LaunchCtx &L, const CopyItems &items, float *dst, int64_t block);
+// Canonical INT4 page blob (import and code export): int8 codes L_K [P][rk],
+// R_K [rk][d], L_V [P][rv], R_V [rv][d], then fp16 scales L_K [P/32][rk],
+// R_K [d], L_V [P], R_V [d].
+__host__ __device__ inline int64_t int4_blob_bytes(int P, int d, int rk, int rv) {
+    return (int64_t)P * rk + (int64_t)rk * d + (int64_t)P * rv + (int64_t)rv * d +
+           2LL * ((P / 32) * rk + d + P + d);
+}
 
 struct AttnPlan {
     int pages_per_chunk;

@@ -9,6 +9,7 @@
 #include "pkv_internal.h"
 
 #include "cache_ops.inl"
+#include "int4.inl"
 #include "compress.inl"
 #include "attention.inl"
 #include "attention_mfma.inl"

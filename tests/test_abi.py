@@ -25,7 +25,7 @@ def pk():
 def _header_functions():
     src = open(os.path.join(ROOT, "include", "puzzlekv.h")).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
-    return sorted(set(re.findall(r"\b(pkv_[a-z_]+)\s*\(", src)))
+    return sorted(set(re.findall(r"\b(pkv_[a-z0-9_]+)\s*\(", src)))
 
 
 def test_exports_every_declared_symbol(pk):
