@@ -9,6 +9,9 @@ bf16 factors with a per-page rank drawn from {16, 24, 32}. A decode step runs
 pages that leave the window (the host planner decides; none at this length
 inside a short run), and mixed-page decode attention.
 
+--workload qwen32b_int4: the same heads and length at batch 8 with factor
+pages stored as INT4 codes plus fp16 scales (Section 4.3), one layer per step.
+
 Setup (untimed): the seeded generator draws layer 0's prompt K/V, the GPU
 decomposition builds its hybrid cache (timed separately for pages/s), and the
 layer's buffers are copied into the 63 other layers. Inputs are resident in
@@ -30,9 +33,8 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBPS = 8000.0
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "attention_traffic.txt")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_23843_amd", "csrc", f)
-                  for f in ("attention.inl", "attention_mfma.inl", "attention_launch.inl")]
+                  for f in ("attention.inl", "attention_mfma.inl", "attention_q4.inl", "attention_launch.inl")]
 
 
 def log(msg: str) -> None:
@@ -50,13 +52,18 @@ def kernel_hash() -> str:
     return h.hexdigest()[:16]
 
 
+def traffic_file(workload: str) -> str:
+    return os.path.join(ROOT, "profiles", "attention_%s_traffic.txt" % workload)
+
+
 def measured_traffic(workload: str):
     """HBM bytes per attention launch from the committed rocprofv3 counter
     summary, if it was taken on the current kernel source; else None."""
-    if not os.path.exists(TRAFFIC_FILE):
+    path = traffic_file(workload)
+    if not os.path.exists(path):
         return None
     vals = {}
-    with open(TRAFFIC_FILE) as f:
+    with open(path) as f:
         for line in f:
             if "=" in line and not line.startswith("#"):
                 k, v = line.split("=", 1)
@@ -117,23 +124,35 @@ def cpu_baseline(wl, seed, seq_T, K_dense, V_dense, q, budget_s, layers):
     import numpy as np
     import oracle
     import synth
+    from oracle import int4 as q4
     P, d, g = wl.page, wl.head_dim, wl.group
+    int4 = wl.factors == "int4"
     kinds = oracle.plan_pages(seq_T, P, wl.sink, wl.window)
     ranks = synth.page_ranks(wl, seed, 0, len(kinds))
     times, heads = [], []
     for b in range(wl.batch):
         for h in range(wl.kv_heads):
             pages = []
+            encoded = {}
             for j, kd in enumerate(kinds):
                 if kd == oracle.FACTOR:
                     r = int(ranks[b, h, j])
                     Lk, Rk, Lv, Rv = synth.factor_page(wl, seed, 0, b, h, j, r, r)
-                    pages.append(("factor", Lk, Rk, Lv, Rv))
+                    if int4:
+                        encoded[j] = [q4.encode_page(w, L, R, np.linalg.norm(R, axis=1))
+                                      for w, L, R in (("K", Lk, Rk), ("V", Lv, Rv))]
+                        pages.append(None)
+                    else:
+                        pages.append(("factor", Lk, Rk, Lv, Rv))
                 else:
                     Kp, Vp = K_dense[(b, h, j)], V_dense[(b, h, j)]
                     pages.append(("dense", Kp, Vp))
-            head = oracle.HeadCache(seq_T, P, d, pages)
             t = time.time()
+            for j, (ek, ev) in encoded.items():   # INT4: dequantization is part of the timed work
+                pages[j] = ("factor",) + tuple(
+                    q4.dequantize_lines(e[c + "_codes"], e[c + "_scales"], q4.AXIS[c + "_" + w])
+                    for e, w in ((ek, "K"), (ev, "V")) for c in ("L", "R"))
+            head = oracle.HeadCache(seq_T, P, d, pages)
             oracle.attention(head, q[b, h * g:(h + 1) * g].astype(np.float64))
             times.append(time.time() - t)
             heads.append((b, h))
@@ -146,9 +165,10 @@ def cpu_baseline(wl, seed, seq_T, K_dense, V_dense, q, budget_s, layers):
     us_step = per_head * n_heads * layers * 1e6
     return {
         "value": us_step, "unit": "us/step", "cores": oracle.num_threads(), "kind": "oracle",
-        "sample": "%d of %d (sequence, KV head) heads of one layer at T=%d (fp64 rebuild + softmax), "
-                  "%.2f s per head, extrapolated x%d heads x%d layers" % (len(times), n_heads, seq_T,
-                                                                          per_head, n_heads, layers),
+        "sample": "%d of %d (sequence, KV head) heads of one layer at T=%d (fp64 %srebuild + softmax), "
+                  "%.2f s per head, extrapolated x%d heads x%d layers"
+                  % (len(times), n_heads, seq_T, "INT4 dequantization + " if int4 else "", per_head, n_heads,
+                     layers),
     }
 
 
@@ -200,7 +220,7 @@ def main():
     ranks_np = synth.page_ranks(wl, args.seed, 0, max_pages)
     ranks = torch.from_numpy(ranks_np).cuda().contiguous()
 
-    cache = pk.PuzzleKVCache(layers, B, Hkv, Hq, d, P, max_pages, max_rank, S, W, "bf16", "bf16")
+    cache = pk.PuzzleKVCache(layers, B, Hkv, Hq, d, P, max_pages, max_rank, S, W, wl.dtype, wl.factors)
     log("cache: factor pool %.1f GB, dense pool %.2f GB" % (cache.factor_pool.numel() / 1e9,
                                                             cache.dense_pool.numel() / 1e9))
 
@@ -301,9 +321,13 @@ def main():
                 "frac": round(achieved / HBM_PEAK_GBPS, 4),
                 "traffic": traffic}
 
+    metrics = {
+        "qwen32b_128k": "mixed-page decode attention time per decode step (64 layers, Qwen3-32B heads, 128K context)",
+        "qwen32b_int4": "mixed-page decode attention time per decode step (INT4 factor pages, Qwen3-32B heads, "
+                        "128K context, batch 8)",
+    }
     result = {
-        "metric": "mixed-page decode attention time per decode step (64 layers, Qwen3-32B heads, 128K context)"
-                  if wl.name == "qwen32b_128k" else "mixed-page decode attention time per decode step",
+        "metric": metrics.get(wl.name, "mixed-page decode attention time per decode step"),
         "value": round(ms_per_step * 1e3, 2),
         "unit": "us/step",
         "n_gpus": 1,
@@ -313,10 +337,11 @@ def main():
         "higher_is_better": False,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "bf16",
+        "dtype": "bf16" if wl.factors == "bf16" else "int4 factors, fp16/bf16 MFMA, fp32 accumulate",
         "data": "synthetic",
         "config": {"workload": wl.name, "batch": B, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d,
                    "page": P, "tokens": T, "sink": S, "window": W, "ranks": list(wl.ranks),
+                   "factor_storage": wl.factors,
                    "layers": layers, "step": "append + planner + compress-when-eligible + attention per layer"},
         "attention_us_per_layer": round(attn_us, 2),
         "attention_algorithmic_bytes": int(abytes),

@@ -49,6 +49,11 @@ class Workload:
     outliers: int
     layers: int = 1
     decode_steps: int = 0
+    factor_dtype: str = ""  # storage of factor pages when it differs from dtype ("int4")
+
+    @property
+    def factors(self) -> str:
+        return self.factor_dtype or self.dtype
 
     @property
     def group(self) -> int:
@@ -70,7 +75,7 @@ WORKLOADS = {
                                     256, 24, (24,), "bf16", 5.0e5, 4, decode_steps=512),
     # INT4 factors: Qwen3-32B heads, batch 8, T=128K.
     "qwen32b_int4": Workload("qwen32b_int4", 5, 8, 8, 64, 128, 64, 131072, 64, 512, 24,
-                             (16, 24, 32), "bf16", 1.0e6, 4),
+                             (16, 24, 32), "bf16", 1.0e6, 4, factor_dtype="int4"),
 }
 
 
