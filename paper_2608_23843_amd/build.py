@@ -29,6 +29,10 @@ def flags() -> list[str]:
         "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
         # packed fp32 instructions are left to nobody: the compiler may not form them
         "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+        # the page-claim atomics are issued by one lane whose result is read
+        # later; the wave-level atomic rewrite would read it at once, waiting
+        # for every load issued before it
+        "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
         "-Wno-unused-command-line-argument",
         "-I", INCLUDE, "-I", CSRC,
     ]

@@ -40,12 +40,16 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kMfmaWaves = 8;
+constexpr int kMfmaWaves = 8;     // wavefronts per workgroup, bf16 kernel (two per SIMD)
+constexpr int kMfmaWavesQ4 = 12;  // INT4 kernel: three per SIMD to cover its dependency stalls
+template <bool Q4>
+constexpr int attn_waves() { return Q4 ? kMfmaWavesQ4 : kMfmaWaves; }
 constexpr int kQ4DenseStage = 256;   // dense pages of one head a workgroup can queue (INT4 kernel)
 // The running max (log2 units) is raised only when a score exceeds it by more
 // than this; below that the exp weights stay under 2^32 and the fp32 sums
 // cannot overflow, so most pages skip the cross-lane max and the rescale.
 constexpr float kLazyLog2 = 32.0f;
+constexpr float kLazyLog2Q4 = 4.0f;   // INT4 kernel: weights stay at most 2^4 (fp16 operands)
 constexpr int kBufferDword3 = 0x00020000; // raw buffer, 32-bit data format
 
 __device__ inline f32x4 mfma_bf16(const bf16x8 &a, const bf16x8 &b, const f32x4 &c) {
@@ -214,7 +218,7 @@ struct WaveState {
 // running max is raised (and the state rescaled) only when needed, then st
 // holds the exp weights. Rows at or past `rows` are masked (dense pages only;
 // factor pages are complete).
-template <int D, int P, bool MASK>
+template <int D, int P, bool MASK, int LAZY = (int)kLazyLog2>
 __device__ inline void page_exp(WaveState<D> &w, f32x4 (&st)[P / 16], int rows, int q, float c2) {
     constexpr int TT = P / 16, DT = D / 16;
     float pm = -INFINITY;
@@ -225,7 +229,7 @@ __device__ inline void page_exp(WaveState<D> &w, f32x4 (&st)[P / 16], int rows, 
             if (MASK && token_row<P>(tt, 4 * q + v) >= rows) st[tt][v] = -INFINITY;
             pm = fmaxf(pm, st[tt][v]);
         }
-    if (__builtin_amdgcn_ballot_w64(pm * c2 > w.m_run + kLazyLog2) != 0) {
+    if (__builtin_amdgcn_ballot_w64(pm * c2 > w.m_run + (float)LAZY) != 0) {
         pm = fmaxf(pm, __shfl_xor(pm, 16, 64));
         pm = fmaxf(pm, __shfl_xor(pm, 32, 64));
         const float m_new = fmaxf(w.m_run, pm * c2);
@@ -257,17 +261,6 @@ __device__ inline void page_softmax(WaveState<D> &w, f32x4 (&st)[P / 16], bf16x8
         w.l = mfma_bf16(ones, eh[ks], w.l);
         w.l = mfma_bf16(ones, el[ks], w.l);
     }
-}
-
-// INT4 pages: the exp weights stay fp32 (phase 2 scales them); w.l[0] keeps
-// this lane's share of the normalizer.
-template <int D, int P, bool MASK>
-__device__ inline void page_softmax_exp(WaveState<D> &w, f32x4 (&st)[P / 16], int rows, int q, float c2) {
-    page_exp<D, P, MASK>(w, st, rows, q, c2);
-    float s = 0.f;
-#pragma unroll
-    for (int tt = 0; tt < P / 16; ++tt) s += (st[tt][0] + st[tt][1]) + (st[tt][2] + st[tt][3]);
-    w.l[0] += s;
 }
 
 // Phase 1 of a unit. Factor page: Z^T = R_K Q^T, S^T = L_K Z^T, softmax.
@@ -370,13 +363,14 @@ __device__ inline pkv_page unpack_entry(uint2 ent) {
 // in turn with page i+1's. One operand set per wave keeps the register budget
 // at two waves per SIMD.
 template <int D, int P, bool Q4>
-__global__ __launch_bounds__(64 * kMfmaWaves, 1) void k_attn_mfma(Geo g, const pkv_page *__restrict__ table,
+__global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, const pkv_page *__restrict__ table,
                                                                   const char *__restrict__ dense,
                                                                   const char *__restrict__ factor,
                                                                   const uint16_t *__restrict__ q, SeqArgs seq,
                                                                   int /*ppc*/, int n_chunks, Partials pp, float *out,
                                                                   float *lse) {
     constexpr int KD = D / 32, DT = D / 16, KS = (P + 31) / 32;
+    constexpr int NW = attn_waves<Q4>();
     const int chunk = blockIdx.x;
     const int64_t head = blockIdx.y;
     const int b = (int)(head / g.Hkv), h = (int)(head % g.Hkv);
@@ -401,6 +395,11 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 1) void k_attn_mfma(Geo g, const p
         __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0)
     }
 
+    // merge buffers; the INT4 kernel also keeps its O^T accumulators in s_o
+    // (rows padded to D + 4 floats against bank conflicts)
+    __shared__ float s_m[NW][16], s_l[NW][16];
+    __shared__ float s_o[NW][16][D + 4];
+
     WaveState<D> w;
 #pragma unroll
     for (int t = 0; t < DT; ++t) w.o[t] = zero_f4();
@@ -420,9 +419,19 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 1) void k_attn_mfma(Geo g, const p
         int64_t j;
         uint2 raw;
     };
-    auto claim = [&]() -> Claim {
+    // A claim is issued (the atomic) at the top of a loop iteration and taken
+    // (its result read) at the bottom: the vector memory counter is in
+    // order, so waiting for an atomic issued after the next page's loads
+    // would also wait for those loads and serialize every page.
+    auto issue_claim = [&]() -> unsigned int {
         unsigned int k = 0u;
         if (lane == 0) k = __hip_atomic_fetch_add(pp.claim(head), 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return k;
+    };
+    auto take_claim = [&](unsigned int k) -> Claim {
+        // pinned here: hoisted up to the atomic, the read of its result would
+        // wait for every load issued before it
+        asm volatile("" : "+v"(k));
         Claim c;
         c.j = (int64_t)__builtin_amdgcn_readfirstlane(k);
         c.raw = c.j < n_pages ? tab[c.j] : make_uint2(0u, 0u);
@@ -434,19 +443,38 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 1) void k_attn_mfma(Geo g, const p
         // dense slots, which the host keeps within the queue) and done after.
         __shared__ int s_dense[kQ4DenseStage];
         __shared__ unsigned int s_nd;
+        // the query group as fp16 B operands, elements of pairs 1 and 3
+        // (e = 2, 3, 6, 7) divided by 16 for the raw key words (exact unless
+        // subnormal); one copy per workgroup (every wave serves this head),
+        // read per page instead of held in registers
+        __shared__ f16x8 s_qh[4][64];
         if (threadIdx.x == 0) s_nd = 0u;
+        if (wave == 0) {
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                f16x8 h;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) h[e] = (_Float16)((float)qb[s][e] * ((e & 2) ? 0.0625f : 1.0f));
+                s_qh[s][lane] = h;
+            }
+        }
+        Q4State w4;
+        w4.ol = &s_o[wave][n][4 * q4];
+        w4.l = 0.f;
+        w4.m_run = -INFINITY;
+#pragma unroll
+        for (int dt = 0; dt < DT; ++dt) lds_st4(w4.ol + 16 * dt, zero_f4());
         __syncthreads();
-        f16x8 qh[4];
-#pragma unroll
-        for (int s = 0; s < 4; ++s)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) qh[s][e] = (_Float16)(float)qb[s][e];
-        Claim ahead = claim();
-        auto next_factor = [&]() -> pkv_page {
+        const Q4Consts kq4 = q4_consts(n);
+        Claim ahead = take_claim(issue_claim());
+        // pre: a claim issued while ahead.j < n_pages, taken by the first step
+        auto next_factor = [&](unsigned int pre) -> pkv_page {
+            bool have_pre = true;
             while (ahead.j < n_pages) {
                 const pkv_page e = unpack_entry(ahead.raw);
                 const int64_t j = ahead.j;
-                ahead = claim();
+                ahead = take_claim(have_pre ? pre : issue_claim());
+                have_pre = false;
                 if (e.kind == PKV_FACTOR) return e;
                 if (lane == 0) {
                     if (e.kind == PKV_DENSE) {
@@ -462,35 +490,57 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 1) void k_attn_mfma(Geo g, const p
             return none;
         };
         Q4Key ko;
-        Q4Val vo;
+        Q4ValY vy;
+        Q4ValO vo;
         pkv_page cur;
         cur.kind = PKV_EMPTY;
-        pkv_page nxt = next_factor();
+        pkv_page nxt = next_factor(ahead.j < n_pages ? issue_claim() : 0u);
         while (cur.kind == PKV_FACTOR || nxt.kind == PKV_FACTOR) {
+            const unsigned int pre = ahead.j < n_pages ? issue_claim() : 0u;
             const Q4Res nres = q4_res(factor, g.factor_slot_bytes, nxt);
-            f32x4 st[4];
             const bool live = cur.kind == PKV_FACTOR;
-            if (live) q4_phase1<D>(w, ko, qh, st, q4, c2);
-            q4_issue_key_loads(ko, nres, n, q4);
-            if (live) q4_phase2<D>(w, vo, st);
-            q4_issue_value_loads(vo, nres, n, q4);
+            if (live) {
+                f32x4 st[4];
+                q4_scores(ko, s_qh, lane, st, kq4);
+                q4_issue_key_loads(ko, nres, n, q4);
+                q4_exp<D, 64, false>(w4, st, 64, q4, c2);
+                f16x8 yh, yl;
+                q4_values_y(vy, st, yh, yl, kq4);
+                q4_issue_y_loads(vy, nres, n, q4);
+                q4_values_o<D>(w4, vo, yh, yl, kq4);
+                q4_issue_o_loads(vo, nres, n, q4);
+            } else {
+                q4_issue_key_loads(ko, nres, n, q4);
+                q4_issue_y_loads(vy, nres, n, q4);
+                q4_issue_o_loads(vo, nres, n, q4);
+            }
             cur = nxt;
-            nxt = next_factor();
+            nxt = next_factor(pre);
         }
         __syncthreads();
         const int nd = (int)min(s_nd, (unsigned int)kQ4DenseStage);
-        for (int i = wave; i < nd; i += kMfmaWaves) {
+        // the bf16 query group is read again here rather than kept in
+        // registers through the stream
+        const uint16_t *qp = q + ((int64_t)b * g.Hq + (int64_t)h * G + n) * D + 8 * q4;
+        for (int i = wave; i < nd; i += NW) {
             const int64_t j = s_dense[i];
             const pkv_page e = unpack_entry(tab[j]);
-            q4_dense_page<D>(w, qb, dense, g.dense_slot_bytes, e.slot, (int)min<int64_t>(P, T - j * P), n, q4, c2);
+            bf16x8 qd[KD];
+#pragma unroll
+            for (int s = 0; s < KD; ++s) qd[s] = n < G ? ld_b8(qp + 32 * s) : zero8();
+            q4_dense_page<D>(w4, qd, dense, g.dense_slot_bytes, e.slot, (int)min<int64_t>(P, T - j * P), n, q4, c2);
         }
+        w.m_run = w4.m_run;
+        w.l[0] = w4.l;
     } else {
-    Claim ahead = claim();
+    Claim ahead = take_claim(issue_claim());
     Unit pending;                 // second and later units of a dense page
     pending.e.kind = PKV_EMPTY;
     pending.j = 0;
     pending.half = 0;
-    auto next_unit = [&]() -> Unit {
+    // pre: a claim issued while needs_claim() held, taken by the first step
+    auto needs_claim = [&]() -> bool { return pending.e.kind != PKV_DENSE && ahead.j < n_pages; };
+    auto next_unit = [&](unsigned int pre) -> Unit {
         if (pending.e.kind == PKV_DENSE) {
             Unit u = pending;
             const int next_half = u.half + 1;
@@ -498,12 +548,14 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 1) void k_attn_mfma(Geo g, const p
             else pending.half = next_half;
             return u;
         }
+        bool have_pre = true;
         while (ahead.j < n_pages) {
             Unit u;
             u.e = unpack_entry(ahead.raw);
             u.j = ahead.j;
             u.half = 0;
-            ahead = claim();
+            ahead = take_claim(have_pre ? pre : issue_claim());
+            have_pre = false;
             if (u.e.kind == PKV_FACTOR) return u;
             if (u.e.kind == PKV_DENSE) {
                 if (UT < min<int64_t>(P, T - u.j * P)) {
@@ -542,8 +594,9 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 1) void k_attn_mfma(Geo g, const p
     cur.e.kind = PKV_EMPTY;
     cur.j = 0;
     cur.half = 0;
-    Unit nxt = next_unit();
+    Unit nxt = next_unit(needs_claim() ? issue_claim() : 0u);
     while (cur.e.kind != PKV_EMPTY || nxt.e.kind != PKV_EMPTY) {
+        const unsigned int pre = needs_claim() ? issue_claim() : 0u;
         const PageRes nres = unit_res<D, P>(factor, g.factor_slot_bytes, dense, g.dense_slot_bytes, nxt);
         bf16x8 eh[KS], el[KS];
         const int rows = unit_rows(cur);
@@ -553,13 +606,11 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 1) void k_attn_mfma(Geo g, const p
         if (live) unit_phase2<D, P>(w, vo, dns, rows, eh, el, q4);
         issue_value_loads<D, P>(vo, nres, lo, n, q4);
         cur = nxt;
-        nxt = next_unit();
+        nxt = next_unit(pre);
     }
     }
 
     // ---- merge the wave states (Eq. (5)) into the chunk's partial ---------
-    __shared__ float s_m[kMfmaWaves][16], s_l[kMfmaWaves][16];
-    __shared__ float s_o[kMfmaWaves][16][D];
     float l_col = w.l[0];
     if constexpr (Q4) {   // lane shares of the normalizer
         l_col += __shfl_xor(l_col, 16, 64);
@@ -569,22 +620,28 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 1) void k_attn_mfma(Geo g, const p
         s_m[wave][n] = w.m_run;
         s_l[wave][n] = l_col;
     }
+    if constexpr (!Q4) {   // the INT4 kernel accumulated in s_o already
 #pragma unroll
-    for (int dt = 0; dt < DT; ++dt)
+        for (int dt = 0; dt < DT; ++dt)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) s_o[wave][n][16 * dt + 4 * q4 + v] = w.o[dt][v];
+            for (int v = 0; v < 4; ++v) s_o[wave][n][16 * dt + 4 * q4 + v] = w.o[dt][v];
+    }
     __syncthreads();
-    for (int idx = threadIdx.x; idx < G * D; idx += 64 * kMfmaWaves) {
+    for (int idx = threadIdx.x; idx < G * D; idx += 64 * NW) {
         const int qi = idx / D, k = idx % D;
         float M = -INFINITY;
 #pragma unroll
-        for (int ww = 0; ww < kMfmaWaves; ++ww) M = fmaxf(M, s_m[ww][qi]);
+        for (int ww = 0; ww < NW; ++ww) M = fmaxf(M, s_m[ww][qi]);
         float acc = 0.f, l = 0.f;
 #pragma unroll
-        for (int ww = 0; ww < kMfmaWaves; ++ww) {
+        for (int ww = 0; ww < NW; ++ww) {
             const float sc = s_m[ww][qi] == -INFINITY ? 0.f : exp2f(s_m[ww][qi] - M);
             acc = fmaf(sc, s_o[ww][qi][k], acc);
             l = fmaf(sc, s_l[ww][qi], l);
+        }
+        if constexpr (Q4) {   // back from the INT4 kernel's units of 2^-4
+            acc *= kQ4Unit;
+            l *= kQ4Unit;
         }
         st_dev(&pp.o[pp.oi(head, qi, k, chunk)], acc);
         if (k == 0) {
@@ -592,7 +649,7 @@ __global__ __launch_bounds__(64 * kMfmaWaves, 1) void k_attn_mfma(Geo g, const p
             st_dev(&pp.l[pp.mi(head, qi, chunk)], l);
         }
     }
-    publish_and_merge<64 * kMfmaWaves>(g, head, pp, out, lse, T);
+    publish_and_merge<64 * NW>(g, head, pp, out, lse, T);
 }
 
 inline bool mfma_supported(const Geo &g) {
@@ -610,7 +667,7 @@ hipError_t launch_attn_mfma(const LaunchCtx &L, const AttnPlan &plan, const uint
     hipLaunchKernelGGL((k_attn_mfma<DD, PP, false>), grid, dim3(64 * kMfmaWaves), 0, L.stream, g, p.table,   \
                        p.dense, p.factor, q, seq, plan.pages_per_chunk, plan.n_chunks, pp, out, lse)
     if (g.factor_dtype == PKV_INT4) {
-        hipLaunchKernelGGL((k_attn_mfma<128, 64, true>), grid, dim3(64 * kMfmaWaves), 0, L.stream, g, p.table,
+        hipLaunchKernelGGL((k_attn_mfma<128, 64, true>), grid, dim3(64 * kMfmaWavesQ4), 0, L.stream, g, p.table,
                            p.dense, p.factor, q, seq, plan.pages_per_chunk, plan.n_chunks, pp, out, lse);
     } else if (g.d == 128) {
         if (g.P == 64) PKV_LAUNCH_MFMA(128, 64);

@@ -1,23 +1,28 @@
 // Mixed-page decode attention over INT4 factor pages (Section 4.3): the
 // balanced factors L~ = U Sigma^(1/2), R~ = Sigma^(1/2) W^T are stored as
-// 4-bit codes with fp16 scales (layout: int4_layout). Per factor page the
-// four products of Eq. (4) run on the matrix cores with the codes turned
-// into exact small integers in registers, and every scale applied where it
-// is a diagonal of the product:
-//   Z^T = R~_K Q^T       fp16 MFMA, A = code x scale (one rounding), B = q
-//   S^T = L~_K Z^T       fp16 MFMA, A = code x scale, B = Z as fp16 hi/lo
-//   Y^T = L~_V^T E'^T    bf16 MFMA, A = 136 + code (exact), B = E' hi/lo with
-//                        E' = E x (row scale of L~_V); the 136 x sum(E')
-//                        offset is removed with a ones x E' product
-//   O^T += s .* (R~_V^T Y^T)  bf16 MFMA, A = 136 + code, B = Y hi/lo, output
-//                        row c scaled by the column scale of R~_V (offset
-//                        removed the same way)
-// Unpacking a word of eight codes: XOR 0x88888888 maps a two's-complement
-// nibble c to c + 8 in [1, 15]. Masked into the low mantissa bits of 1024.0
-// (fp16, quantum 1) that is 1032 + c; minus 1032 it is c exactly, and one
-// multiply by the scale rounds c x s once. Masked into the mantissa of 128.0
-// (bf16, quantum 1) it is 136 + c. Dense pages (bf16) are queued and done
-// after the stream. Included by attention_mfma.inl.
+// 4-bit codes (offset-binary, nibble c + 8) with fp16 scales (layout:
+// int4_layout). Per factor page the four products of Eq. (4) run on the
+// matrix cores with the codes turned into exact small numbers in registers,
+// and every scale applied where it is a diagonal of the product:
+//   Z^T = R~_K Q^T       fp16 MFMA, A = raw code word (exact), B = q o s_K
+//                        (the R~_K column scale folded into the query); the
+//                        raw words' offset is one more product, -beta x B,
+//                        used as the accumulator's start
+//   S^T = L~_K Z^T       fp16 MFMA, A = code x scale (rounded once), B = Z
+//                        as fp16 hi/lo
+//   Y^T = L~_V^T E'^T    fp16 MFMA, A = raw code word, B = E' = E x (row
+//                        scale of L~_V) in fp16; started from -beta x E'
+//   O^T += s .* (R~_V^T Y^T)  fp16 MFMA, A = raw code word, B = Y hi/lo,
+//                        started from -beta x Y; output row c scaled by the
+//                        column scale of R~_V
+// The exp weights, l and O^T are kept in units of 2^-4 so every fp16 operand
+// stays in range and out of the subnormals.
+// Unpacking a word of eight nibbles n = c + 8 takes one and-or per pair of
+// codes: masked into the low mantissa of 1024.0 (fp16, quantum 1) a nibble
+// at bits 0-3 gives 1024 + n and one at bits 4-7 gives 1024 + 16 n, both
+// exact. Elements whose nibble sits at bits 4-7 carry the factor 16, which
+// the other operand (or the scale) divides out exactly. Dense pages (bf16) are queued and done after the stream.
+// Included by attention_mfma.inl.
 
 namespace pkv {
 
@@ -28,40 +33,74 @@ __device__ inline f32x4 mfma_f16(const f16x8 &a, const f16x8 &b, const f32x4 &c)
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
 
-// Eight codes -> fp16 (code x scale); sc: the scales of the eight elements
-// as four fp16 pairs. In the low mantissa bits of 1024.0 (quantum 1) the
-// biased nibble c + 8 gives 1032 + c exactly; subtracting 1032 leaves c
-// exactly, and its product with the scale is rounded once.
-__device__ inline f16x8 q4_frag_scaled(uint32_t word, const u32x4 &sc) {
-    const uint32_t x = word ^ 0x88888888u;
-    const f16x2 bias = f16x2{(_Float16)-1032.f, (_Float16)-1032.f};
-    f16x2 r[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const uint32_t p = ((x >> (4 * k)) & 0x000f000fu) | 0x64006400u;
-        // the element goes through a scalar first: a bit_cast of a vector
-        // element expression reads element 0 whatever the index
-        const uint32_t s = sc[k];
-        r[k] = (__builtin_bit_cast(f16x2, p) + bias) * __builtin_bit_cast(f16x2, s);
-    }
-    return f16x8{r[0][0], r[0][1], r[1][0], r[1][1], r[2][0], r[2][1], r[3][0], r[3][1]};
-}
-// Eight codes -> bf16 (136 + code), exact.
-__device__ inline bf16x8 q4_frag_offset(uint32_t word) {
-    const uint32_t x = word ^ 0x88888888u;
-    u32x4 p;
-    p[0] = (x & 0x000f000fu) | 0x43004300u;
-    p[1] = ((x >> 4) & 0x000f000fu) | 0x43004300u;
-    p[2] = ((x >> 8) & 0x000f000fu) | 0x43004300u;
-    p[3] = ((x >> 12) & 0x000f000fu) | 0x43004300u;
-    return __builtin_bit_cast(bf16x8, p);
+// Loop-invariant unpack constants, held in registers (kept opaque so the
+// compiler forms one v_and_or_b32 per pair of codes).
+struct Q4Consts {
+    uint32_t m0, m1;     // masks of the nibbles at bits 0-3 and 4-7 of each half
+    uint32_t h16;        // fp16 1024.0 in both halves
+    uint32_t h16y;       // Y^T rows: 1024.0, or 64.0 in lanes whose row (rank) is 2 or 3 mod 4
+    f16x8 nbeta_y;       // -beta, divided by 16 in the same lanes
+};
+__device__ inline Q4Consts q4_consts(int n) {
+    Q4Consts k;
+    k.m0 = 0x000f000fu;
+    k.m1 = 0x00f000f0u;
+    k.h16 = 0x64006400u;
+    k.h16y = (n & 2) ? 0x54005400u : 0x64006400u;
+    k.nbeta_y = f16x8{-1032, -1032, -1152, -1152, -1032, -1032, -1152, -1152} *
+                ((n & 2) ? (_Float16)0.0625f : (_Float16)1.f);
+    asm("" : "+s"(k.m0));
+    asm("" : "+s"(k.m1));
+    asm("" : "+v"(k.h16));
+    asm("" : "+v"(k.h16y));
+    return k;
 }
 
+// Element e of a word sits at bit int4_nib(e); the pairs (0,1), (2,3), (4,5),
+// (6,7) sit at bits (0, 16), (4, 20), (8, 24), (12, 28).
+// Eight codes -> fp16 1024 + n (pairs 0 and 2) and 1024 + 16 n (pairs 1 and 3), exact.
+// With the magic 64.0 instead (quantum 1/16) the same word gives those
+// values divided by 16, also exact.
+__device__ inline f16x8 q4_frag_raw(uint32_t x, const Q4Consts &k, uint32_t magic) {
+    const uint32_t y = x >> 8;
+    u32x4 p;
+    p[0] = (x & k.m0) | magic;
+    p[1] = (x & k.m1) | magic;
+    p[2] = (y & k.m0) | magic;
+    p[3] = (y & k.m1) | magic;
+    return __builtin_bit_cast(f16x8, p);
+}
+__device__ inline f16x8 q4_frag_raw(uint32_t x, const Q4Consts &k) { return q4_frag_raw(x, k, k.h16); }
+// Eight codes -> fp16 code x scale, rounded once: (1024 + n) - 1032 = c and
+// (1024 + 16 n) - 1152 = 16 c are exact; sc holds the scales as four fp16
+// pairs, those of pairs 1 and 3 already divided by 16.
+__device__ inline f16x8 q4_frag_scaled(uint32_t x, const u32x4 &sc, const Q4Consts &k) {
+    const f16x8 h = q4_frag_raw(x, k);
+    const f16x8 bias = f16x8{-1032, -1032, -1152, -1152, -1032, -1032, -1152, -1152};
+    // the scale words go through scalars: a bit_cast of a vector element
+    // expression reads element 0 whatever the index
+    const uint32_t s0 = sc[0], s1 = sc[1], s2 = sc[2], s3 = sc[3];
+    const f16x8 s = __builtin_bit_cast(f16x8, u32x4{s0, s1, s2, s3});
+    return (h + bias) * s;
+}
+// Scale words of one lane with pairs 1 and 3 divided by 16 (exact unless subnormal).
+__device__ inline u32x4 q4_scale_div16(const u32x4 &sc) {
+    const f16x2 r16 = f16x2{(_Float16)0.0625f, (_Float16)0.0625f};
+    const uint32_t s1 = sc[1], s3 = sc[3];
+    u32x4 o = sc;
+    o[1] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, s1) * r16);
+    o[3] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, s3) * r16);
+    return o;
+}
 // fp32 pair -> fp16 hi (toward zero) and lo (the remainder), as packed words.
+// The remainder a - hi is one mixed-precision fma with hi as its fp16
+// operand (the -1 is kept opaque so the compiler keeps the fma form).
 __device__ inline void split2_f16(float a, float b, uint32_t &hi, uint32_t &lo) {
     const f16x2 h = __builtin_bit_cast(f16x2, __builtin_amdgcn_cvt_pkrtz(a, b));
+    float m1 = -1.f;
+    asm("" : "+v"(m1));
     hi = __builtin_bit_cast(uint32_t, h);
-    lo = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(a - (float)h[0], b - (float)h[1]));
+    lo = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(fmaf((float)h[0], m1, a), fmaf((float)h[1], m1, b)));
 }
 __device__ inline void split_tiles_f16(const f32x4 &x0, const f32x4 &x1, f16x8 &hi, f16x8 &lo) {
     uint32_t h0, h1, h2, h3, l0, l1, l2, l3;
@@ -80,11 +119,15 @@ struct Q4Key {
     u32x4 akc;      // L~_K codes, word tt = token row token_row(tt, n), ranks 8q .. +7
     u32x4 aks[2];   // L~_K scales of those ranks, run 0 (tiles 0, 1) and run 1 (tiles 2, 3)
 };
-struct Q4Val {
-    u32x4 bvc[2];   // R~_V^T codes, word dt = dim 16 dt + n, ranks 8q .. +7
-    u32x4 bvs[4];   // R~_V scales of the lane's output rows 16 dt + 4q + v: word (2 dt + v/2)
+// Value operands in two parts: those of Y^T (used right after the page's
+// softmax) and those of O^T (used one pipeline step later).
+struct Q4ValY {
     u32x4 avc;      // L~_V^T codes, word 2 rt + ks = rank row rank_row(rt, n), tokens 32 ks + 8q .. +7
     u32x4 avs[2];   // L~_V scales of the lane's score rows token_row(tt, 4q + v): word (2 tt + v/2)
+};
+struct Q4ValO {
+    u32x4 bvc[2];   // R~_V^T codes, word dt = dim 16 dt + n, ranks 8q .. +7
+    u32x4 bvs[4];   // R~_V scales of the lane's output rows 16 dt + 4q + v: word (2 dt + v/2)
 };
 
 // Per page: one resource for the key half and one for the value half (each
@@ -92,7 +135,7 @@ struct Q4Val {
 struct Q4Res {
     __amdgpu_buffer_rsrc_t k, v;
     uint32_t bkc, bks, aks;        // key half (akc starts at 0)
-    uint32_t bvs, avs, avc;        // value half (bvc starts at 0)
+    uint32_t bvs, avs, avc, pad;   // value half (bvc starts at 0)
     int kqk, kqv;                  // groups of 8 ranks present
 };
 __device__ inline Q4Res q4_res(const char *factor, int64_t slot_bytes, const pkv_page &e) {
@@ -109,6 +152,7 @@ __device__ inline Q4Res q4_res(const char *factor, int64_t slot_bytes, const pkv
     r.bvs = (uint32_t)(f.bvs - f.bvc);
     r.avs = (uint32_t)(f.avs - f.bvc);
     r.avc = (uint32_t)(f.avc - f.bvc);
+    r.pad = (uint32_t)(f.pad - f.bvc);
     r.kqk = r8(rk) / 8;
     r.kqv = r8(rv) / 8;
     return r;
@@ -130,96 +174,180 @@ __device__ inline void q4_issue_key_loads(Q4Key &f, const Q4Res &r, int n, int q
 #pragma unroll
     for (int u = 0; u < 2; ++u) f.aks[u] = bld16(r.k, q < r.kqk ? 32u * q + 16u * u + r.aks : kOOB, 0u);
 }
-__device__ inline void q4_issue_value_loads(Q4Val &f, const Q4Res &r, int n, int q) {
-#pragma unroll
-    for (int h = 0; h < 2; ++h) f.bvc[h] = bld16(r.v, q < r.kqv ? 32u * (16 * q + n) + 16u * h : kOOB, 0u);
-#pragma unroll
-    for (int k = 0; k < 4; ++k) f.bvs[k] = bld16(r.v, 64u * q + 16u * k, r.bvs);
-    f.avc = bld16(r.v, r.avc + 16u * (4 * n + q), 0u);
+// Value words past the rank read the pad (zero codes): A_V^T rank rows at or
+// past r8(r_V), and B_V^T groups of 8 ranks at or past r8(r_V).
+__device__ inline void q4_issue_y_loads(Q4ValY &f, const Q4Res &r, int n, int q) {
+    f.avc = bld16(r.v, n < 4 * r.kqv ? r.avc + 16u * (4 * n + q) : r.pad, 0u);
 #pragma unroll
     for (int k = 0; k < 2; ++k) f.avs[k] = bld16(r.v, 32u * q + 16u * k, r.avs);
 }
+__device__ inline void q4_issue_o_loads(Q4ValO &f, const Q4Res &r, int n, int q) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) f.bvc[h] = bld16(r.v, (q < r.kqv ? 32u * (16 * q + n) : r.pad) + 16u * h, 0u);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) f.bvs[k] = bld16(r.v, 64u * q + 16u * k, r.bvs);
+}
 
-// Phase 1 of an INT4 factor page: Z^T, S^T, softmax; the exp weights stay in
-// st (fp32) for phase 2, which folds the L~_V row scales into them.
-template <int D>
-__device__ inline void q4_phase1(WaveState<D> &w, const Q4Key &f, const f16x8 (&qh)[4], f32x4 (&st)[4], int q,
-                                 float c2) {
+// The INT4 kernel's exp weights, l and O^T are in units of 2^-4, and its
+// running max is raised once a score passes it by 2^4: every weight is then
+// at most 1 (unit), so E x s and Y stay far inside fp16 range for row scales
+// below ~140, while the weights of the page holding the current maximum stay
+// at or above 1/16 and keep the fp16 hi/lo splits out of the subnormal range.
+constexpr float kQ4UnitLog2 = 4.f;
+constexpr float kQ4Unit = 16.f;
+
+// Running state of one wave of the INT4 kernel: the lane's share of the
+// normalizer and the running max (log2 units) in registers, the O^T
+// accumulators in LDS (the wave's block of the merge buffer, rows of D + 4
+// floats): lane (n, q) owns o[16 dt + 4q .. +3] of row n, at ol + 16 dt.
+struct Q4State {
+    float *ol;
+    float l, m_run;
+};
+__device__ inline f32x4 lds_ld4(const float *p) { return *(const f32x4 *)p; }
+__device__ inline void lds_st4(float *p, const f32x4 &v) { *(f32x4 *)p = v; }
+
+// Online softmax over one page's raw scores (Eq. (5) state update) with a
+// lazy running max: it is raised (and O^T, l rescaled) only when a score
+// exceeds it by 2^4, so the exp weights, in units of 2^-4, stay at most 1.
+// Rows at or past `rows` are masked (dense pages).
+template <int D, int P, bool MASK>
+__device__ inline void q4_exp(Q4State &w, f32x4 (&st)[P / 16], int rows, int q, float c2) {
+    constexpr int TT = P / 16;
+    float pm = -INFINITY;
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            if (MASK && token_row<P>(tt, 4 * q + v) >= rows) st[tt][v] = -INFINITY;
+            pm = fmaxf(pm, st[tt][v]);
+        }
+    if (__builtin_amdgcn_ballot_w64(pm * c2 > w.m_run + kLazyLog2Q4) != 0) {
+        pm = fmaxf(pm, __shfl_xor(pm, 16, 64));
+        pm = fmaxf(pm, __shfl_xor(pm, 32, 64));
+        const float m_new = fmaxf(w.m_run, pm * c2);
+        const float alpha = w.m_run == -INFINITY ? 0.f : exp2f(w.m_run - m_new);
+#pragma unroll
+        for (int dt = 0; dt < D / 16; ++dt) lds_st4(w.ol + 16 * dt, lds_ld4(w.ol + 16 * dt) * alpha);
+        w.l *= alpha;
+        w.m_run = m_new;
+    }
+    // weights in units of 2^-4 (an exponent offset); l and O^T share the unit
+    const float nm = -(w.m_run + kQ4UnitLog2);
+    float sum = 0.f;
+#pragma unroll
+    for (int tt = 0; tt < TT; ++tt) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) st[tt][v] = __builtin_amdgcn_exp2f(fmaf(st[tt][v], c2, nm));
+        sum += (st[tt][0] + st[tt][1]) + (st[tt][2] + st[tt][3]);
+    }
+    w.l += sum;
+}
+
+// Scores of an INT4 factor page: Z^T, then S^T into st (raw, fp32). qh16
+// (LDS, [s][lane]): the query group as fp16 B operands, elements of pairs 1
+// and 3 divided by 16.
+__device__ inline void q4_scores(const Q4Key &f, const f16x8 (&qh16)[4][64], int lane, f32x4 (&st)[4],
+                                 const Q4Consts &k) {
+    f16x8 qs[4];
+#pragma unroll
+    for (int s = 0; s < 4; ++s) qs[s] = qh16[s][lane] * __builtin_bit_cast(f16x8, f.bks[s]);
+    // the raw words' offset (1032 per code of pairs 0, 2; 1152 / 16 per code
+    // of pairs 1, 3) is removed by starting both rank tiles from -beta x B
+    const f16x8 nbeta = f16x8{-1032, -1032, -1152, -1152, -1032, -1032, -1152, -1152};
+    f32x4 z0 = zero_f4();
+#pragma unroll
+    for (int s = 0; s < 4; ++s) z0 = mfma_f16(nbeta, qs[s], z0);
     f32x4 z[2];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
-        z[rt] = zero_f4();
+        z[rt] = z0;
 #pragma unroll
-        for (int s = 0; s < 4; ++s) z[rt] = mfma_f16(q4_frag_scaled(f.bkc[rt][s], f.bks[s]), qh[s], z[rt]);
+        for (int s = 0; s < 4; ++s) z[rt] = mfma_f16(q4_frag_raw(f.bkc[rt][s], k), qs[s], z[rt]);
     }
     f16x8 zh, zl;
     split_tiles_f16(z[0], z[1], zh, zl);
+    const u32x4 ak0 = q4_scale_div16(f.aks[0]), ak1 = q4_scale_div16(f.aks[1]);
 #pragma unroll
     for (int tt = 0; tt < 4; ++tt) {
-        const f16x8 a = q4_frag_scaled(f.akc[tt], tt < 2 ? f.aks[0] : f.aks[1]);
+        const f16x8 a = q4_frag_scaled(f.akc[tt], tt < 2 ? ak0 : ak1, k);
         st[tt] = mfma_f16(a, zh, zero_f4());
         st[tt] = mfma_f16(a, zl, st[tt]);
     }
-    page_softmax_exp<D, 64, false>(w, st, 64, q, c2);
 }
 
-// Phase 2 of an INT4 factor page: E' = E x row scale, Y^T, O^T.
-template <int D>
-__device__ inline void q4_phase2(WaveState<D> &w, const Q4Val &f, const f32x4 (&st)[4]) {
-    const bf16x8 ones = bf16x8{1, 1, 1, 1, 1, 1, 1, 1};
-    f32x4 ep[4];
+// Y^T of an INT4 factor page from its exp weights st (units of 2^-4):
+// E' = E x (row scale of L~_V) in fp16, then L~_V^T E'^T from raw code words;
+// returned as the fp16 hi/lo B operands of O^T, with the rows of ranks 2 and
+// 3 mod 4 (elements e = 2, 3, 6, 7 of each lane) divided by 16 for the raw
+// R~_V words, by the magic 64.0 in those lanes' A operand.
+__device__ inline void q4_values_y(const Q4ValY &f, const f32x4 (&st)[4], f16x8 &yh, f16x8 &yl,
+                                   const Q4Consts &k) {
+    // E' (fp16): token 32 ks + 8q + e in element e of eb[ks]; tokens whose
+    // code nibble sits at bits 4-7 of the L~_V^T word (e = 2, 3, 6, 7, i.e.
+    // v = 2, 3) take the scale / 16
+    // The product E x s is formed in fp32 (one mixed-precision fma with s as
+    // its fp16 operand; the zero addend is kept opaque so the fma stays) and
+    // rounded to fp16 once.
+    const u32x4 sv[2] = {q4_scale_div16(f.avs[0]), q4_scale_div16(f.avs[1])};
+    float z0 = 0.f;
+    asm("" : "+v"(z0));
+    f16x8 eb[2];
 #pragma unroll
     for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
-        for (int v = 0; v < 4; ++v) {
-            const uint32_t pair = f.avs[tt >> 1][2 * (tt & 1) + (v >> 1)];
-            const float sc = (float)__builtin_bit_cast(f16x2, pair)[v & 1];
-            ep[tt][v] = st[tt][v] * sc;
+        for (int v = 0; v < 4; v += 2) {
+            const uint32_t pair = sv[tt >> 1][2 * (tt & 1) + (v >> 1)];
+            const f16x2 sc = __builtin_bit_cast(f16x2, pair);
+            const f32x2 e = f32x2{fmaf(st[tt][v], (float)sc[0], z0), fmaf(st[tt][v + 1], (float)sc[1], z0)};
+            const f16x2 h = __builtin_convertvector(e, f16x2);
+            eb[tt >> 1][4 * (tt & 1) + v] = h[0];
+            eb[tt >> 1][4 * (tt & 1) + v + 1] = h[1];
         }
-    bf16x8 eh[2], el[2];
-    split_tiles(ep[0], ep[1], eh[0], el[0]);
-    split_tiles(ep[2], ep[3], eh[1], el[1]);
-    f32x4 cse = zero_f4();
+    // started from -beta x E' (divided by 16 in the lanes that divide their row)
+    f32x4 y0 = zero_f4();
 #pragma unroll
-    for (int ks = 0; ks < 2; ++ks) {
-        cse = mfma_bf16(ones, eh[ks], cse);
-        cse = mfma_bf16(ones, el[ks], cse);
-    }
+    for (int ks = 0; ks < 2; ++ks) y0 = mfma_f16(k.nbeta_y, eb[ks], y0);
     f32x4 y[2];
 #pragma unroll
     for (int rt = 0; rt < 2; ++rt) {
-        y[rt] = zero_f4();
+        y[rt] = y0;
 #pragma unroll
-        for (int ks = 0; ks < 2; ++ks) {
-            const bf16x8 a = q4_frag_offset(f.avc[2 * rt + ks]);
-            y[rt] = mfma_bf16(a, eh[ks], y[rt]);
-            y[rt] = mfma_bf16(a, el[ks], y[rt]);
-        }
-        y[rt] -= 136.f * cse;
+        for (int ks = 0; ks < 2; ++ks)
+            y[rt] = mfma_f16(q4_frag_raw(f.avc[2 * rt + ks], k, k.h16y), eb[ks], y[rt]);
     }
-    bf16x8 yh, yl;
-    split_tiles(y[0], y[1], yh, yl);
-    f32x4 csy = mfma_bf16(ones, yh, zero_f4());
-    csy = mfma_bf16(ones, yl, csy);
-    const f32x4 off = 136.f * csy;
+    split_tiles_f16(y[0], y[1], yh, yl);
+}
+
+// O^T += s .* (R~_V^T Y^T) from raw R~_V^T code words, each dim tile started
+// from -beta x Y so the product is the codes' alone; output row c scaled by
+// the column scale of R~_V.
+template <int D>
+__device__ inline void q4_values_o(Q4State &w, const Q4ValO &f, const f16x8 &yh, const f16x8 &yl,
+                                   const Q4Consts &k) {
+    const f16x8 nbeta = f16x8{-1032, -1032, -1152, -1152, -1032, -1032, -1152, -1152};
+    f32x4 ob = mfma_f16(nbeta, yh, zero_f4());
+    ob = mfma_f16(nbeta, yl, ob);
 #pragma unroll
     for (int dt = 0; dt < D / 16; ++dt) {
-        const bf16x8 a = q4_frag_offset(f.bvc[dt >> 2][dt & 3]);
-        f32x4 pr = mfma_bf16(a, yh, zero_f4());
-        pr = mfma_bf16(a, yl, pr);
+        const f16x8 a = q4_frag_raw(f.bvc[dt >> 2][dt & 3], k);
+        f32x4 pr = mfma_f16(a, yh, ob);
+        pr = mfma_f16(a, yl, pr);
+        f32x4 o = lds_ld4(w.ol + 16 * dt);
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
             const uint32_t pair = f.bvs[dt >> 1][2 * (dt & 1) + (v >> 1)];
             const float sc = (float)__builtin_bit_cast(f16x2, pair)[v & 1];
-            w.o[dt][v] = fmaf(sc, pr[v] - off[v], w.o[dt][v]);
+            o[v] = fmaf(sc, pr[v], o[v]);
         }
+        lds_st4(w.ol + 16 * dt, o);
     }
 }
 
 // A dense page, loaded and computed in place in units of 32 tokens (used for
 // the few dense pages after the INT4 stream).
 template <int D>
-__device__ inline void q4_dense_page(WaveState<D> &w, const bf16x8 (&qb)[D / 32], const char *dense,
+__device__ inline void q4_dense_page(Q4State &w, const bf16x8 (&qb)[D / 32], const char *dense,
                                      int64_t slot_bytes, int slot, int rows_page, int n, int q, float c2) {
     const uint16_t *K = (const uint16_t *)(dense + slot * slot_bytes);
     const uint16_t *Vt = K + (int64_t)64 * D;
@@ -233,7 +361,7 @@ __device__ inline void q4_dense_page(WaveState<D> &w, const bf16x8 (&qb)[D / 32]
 #pragma unroll
             for (int s = 0; s < D / 32; ++s) st[tt] = mfma_bf16(ld_b8(kp + 32 * s), qb[s], st[tt]);
         }
-        page_softmax_exp<D, 32, true>(w, st, rows, q, c2);
+        q4_exp<D, 32, true>(w, st, rows, q, c2);
         bf16x8 eh, el;
         split_tiles(st[0], st[1], eh, el);
 #pragma unroll
@@ -242,8 +370,10 @@ __device__ inline void q4_dense_page(WaveState<D> &w, const bf16x8 (&qb)[D / 32]
 #pragma unroll
             for (int u = 0; u < 8; ++u)
                 if (8 * q + u >= rows) vv[u] = (__bf16)0.f;
-            w.o[dt] = mfma_bf16(vv, eh, w.o[dt]);
-            w.o[dt] = mfma_bf16(vv, el, w.o[dt]);
+            f32x4 o = lds_ld4(w.ol + 16 * dt);
+            o = mfma_bf16(vv, eh, o);
+            o = mfma_bf16(vv, el, o);
+            lds_st4(w.ol + 16 * dt, o);
         }
     }
 }

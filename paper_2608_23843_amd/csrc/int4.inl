@@ -84,10 +84,10 @@ __device__ inline int q4_code(float x, float s) {
     const double qv = rint((double)x / (double)s);
     return (int)fmax(-kQ4Max, fmin((double)kQ4Max, qv));
 }
-__device__ inline int q4_nibble(uint32_t word, int shift) {
-    const int v = (int)((word >> shift) & 0xfu);
-    return v >= 8 ? v - 16 : v;
-}
+// Offset-binary nibbles: code c is stored as c + 8.
+__device__ inline uint32_t q4_nib(int code) { return (uint32_t)(code + 8) & 0xfu; }
+__device__ inline int q4_nibble(uint32_t word, int shift) { return (int)((word >> shift) & 0xfu) - 8; }
+constexpr uint32_t kQ4ZeroWord = 0x88888888u;   // eight zero codes
 
 // ---- quantizer (page compression) -------------------------------------------
 //
@@ -136,7 +136,7 @@ __device__ void q4_quantize_store(char *slot, const Int4Layout &f, int P, int d,
             for (int e = 0; e < 8; ++e) {
                 const int a = 8 * kq + e;
                 const int code = a < r ? q4_code(sL[t * 32 + a], sScale[u * r8(r) + a]) : 0;
-                word |= (uint32_t)(code & 0xf) << int4_nib(e);
+                word |= q4_nib(code) << int4_nib(e);
             }
             *(uint32_t *)(slot + f.akc + 4LL * w) = word;
         }
@@ -146,7 +146,7 @@ __device__ void q4_quantize_store(char *slot, const Int4Layout &f, int P, int d,
             uint32_t word = 0;
             for (int e = 0; e < 8; ++e) {
                 const int c = 32 * s + 8 * kq + e;
-                word |= (uint32_t)(q4_code(sR[a * d + c], sScale[n_lruns + c]) & 0xf) << int4_nib(e);
+                word |= q4_nib(q4_code(sR[a * d + c], sScale[n_lruns + c])) << int4_nib(e);
             }
             *(uint32_t *)(slot + f.bkc + 4LL * w) = word;
         }
@@ -160,7 +160,7 @@ __device__ void q4_quantize_store(char *slot, const Int4Layout &f, int P, int d,
             for (int e = 0; e < 8; ++e) {
                 const int a = 8 * kq + e;
                 const int code = a < r ? q4_code(sR[a * d + c], sScale[n_lruns + c]) : 0;
-                word |= (uint32_t)(code & 0xf) << int4_nib(e);
+                word |= q4_nib(code) << int4_nib(e);
             }
             *(uint32_t *)(slot + f.bvc + 4LL * w) = word;
         }
@@ -170,13 +170,13 @@ __device__ void q4_quantize_store(char *slot, const Int4Layout &f, int P, int d,
             const int i = w / 16, kq = (w / 4) % 4, rt = (w / 2) % 2, ks = w % 2;
             const int a = tile_rank_row(rt, i);
             uint32_t word = 0;
-            if (a < r)
-                for (int e = 0; e < 8; ++e) {
-                    const int t = 32 * ks + 8 * kq + e;
-                    word |= (uint32_t)(q4_code(sL[t * 32 + a], sScale[t]) & 0xf) << int4_nib(e);
-                }
+            for (int e = 0; e < 8; ++e) {
+                const int t = 32 * ks + 8 * kq + e;
+                word |= q4_nib(a < r ? q4_code(sL[t * 32 + a], sScale[t]) : 0) << int4_nib(e);
+            }
             *(uint32_t *)(slot + f.avc + 4LL * w) = word;
         }
+        for (int w = lane; w < kInt4Pad / 4; w += 64) *(uint32_t *)(slot + f.pad + 4LL * w) = kQ4ZeroWord;
     }
 }
 
@@ -206,14 +206,14 @@ __device__ void q4_import_page(char *slot, const char *blob, int P, int d, int r
         uint32_t word = 0;
         for (int e = 0; e < 8; ++e) {
             const int a = 8 * kq + e;
-            if (a < rk) word |= (uint32_t)(clk[t * rk + a] & 0xf) << int4_nib(e);
+            word |= q4_nib(a < rk ? clk[t * rk + a] : 0) << int4_nib(e);
         }
         *(uint32_t *)(slot + f.akc + 4LL * w) = word;
     }
     for (int w = threadIdx.x; w < rk * (d / 8); w += blockDim.x) {
         const int a = w / (d / 8), kq = (w % (d / 8)) / 4, s = w % 4;
         uint32_t word = 0;
-        for (int e = 0; e < 8; ++e) word |= (uint32_t)(crk[a * d + 32 * s + 8 * kq + e] & 0xf) << int4_nib(e);
+        for (int e = 0; e < 8; ++e) word |= q4_nib(crk[a * d + 32 * s + 8 * kq + e]) << int4_nib(e);
         *(uint32_t *)(slot + f.bkc + 4LL * w) = word;
     }
     for (int w = threadIdx.x; w < (r8(rv) / 8) * 128; w += blockDim.x) {
@@ -222,7 +222,7 @@ __device__ void q4_import_page(char *slot, const char *blob, int P, int d, int r
         uint32_t word = 0;
         for (int e = 0; e < 8; ++e) {
             const int a = 8 * kq + e;
-            if (a < rv) word |= (uint32_t)(crv[a * d + c] & 0xf) << int4_nib(e);
+            word |= q4_nib(a < rv ? crv[a * d + c] : 0) << int4_nib(e);
         }
         *(uint32_t *)(slot + f.bvc + 4LL * w) = word;
     }
@@ -230,10 +230,10 @@ __device__ void q4_import_page(char *slot, const char *blob, int P, int d, int r
         const int i = w / 16, kq = (w / 4) % 4, rt = (w / 2) % 2, ks = w % 2;
         const int a = tile_rank_row(rt, i);
         uint32_t word = 0;
-        if (a < rv)
-            for (int e = 0; e < 8; ++e) word |= (uint32_t)(clv[(32 * ks + 8 * kq + e) * rv + a] & 0xf) << int4_nib(e);
+        for (int e = 0; e < 8; ++e) word |= q4_nib(a < rv ? clv[(32 * ks + 8 * kq + e) * rv + a] : 0) << int4_nib(e);
         *(uint32_t *)(slot + f.avc + 4LL * w) = word;
     }
+    for (int w = threadIdx.x; w < kInt4Pad / 4; w += blockDim.x) *(uint32_t *)(slot + f.pad + 4LL * w) = kQ4ZeroWord;
 }
 
 // ---- export: slot -> canonical blob, or dequantized fp32 block ---------------

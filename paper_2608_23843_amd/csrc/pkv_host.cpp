@@ -67,9 +67,15 @@ pkv_status check_geometry(const pkv_cache *c) {
     return PKV_OK;
 }
 
+// Stored bytes of one factor page pair (codes and scales for INT4); a slot
+// adds the INT4 pad.
 int64_t factor_page_bytes_of(int dtype, int P, int d, int rk, int rv) {
-    if (dtype == PKV_INT4) return int4_layout(P, d, rk, rv).end;
+    if (dtype == PKV_INT4) return int4_layout(P, d, rk, rv).pad;
     return factor_page_elems(P, d, rk, rv) * elem_size(dtype);
+}
+int64_t factor_slot_bytes_of(int dtype, int P, int d, int r) {
+    if (dtype == PKV_INT4) return int4_layout(P, d, r, r).end;
+    return factor_page_bytes_of(dtype, P, d, r, r);
 }
 
 Geo make_geo(const pkv_cache *c) {
@@ -92,7 +98,7 @@ Geo make_geo(const pkv_cache *c) {
     g.dense_dtype = c->dense_dtype;
     g.factor_dtype = c->factor_dtype;
     g.dense_slot_bytes = 2LL * g.P * g.d * g.dense_es;
-    int64_t fb = factor_page_bytes_of(c->factor_dtype, g.P, g.d, g.max_rank, g.max_rank);
+    int64_t fb = factor_slot_bytes_of(c->factor_dtype, g.P, g.d, g.max_rank);
     g.factor_slot_bytes = (fb + 255) / 256 * 256;
     g.layer_entries = (int64_t)g.B * g.Hkv * g.max_pages;
     g.layer_dense_bytes = (int64_t)g.B * g.Hkv * g.dslots * g.dense_slot_bytes;

@@ -39,8 +39,9 @@ __host__ __device__ inline FactorLayout factor_layout(int P, int d, int rk, int 
 }
 
 // INT4 factor slot (factor dtype PKV_INT4; P = 64, d = 128, ranks <= 32).
-// Codes are 4-bit two's complement, eight to a dword with element e at bit
-// int4_nib(e); scales are fp16. Byte offsets of the sections, in order:
+// Codes c in [-7, 7] are stored offset-binary (nibble c + 8), eight to a
+// dword with element e at bit int4_nib(e); scales are fp16. Byte offsets of
+// the sections, in order:
 //   akc  A_K codes      [kq][i][tt] dwords: token row tau(tt, i), ranks 8kq + e
 //   aks  A_K scales     [kq][run][e]: column-wise runs of 32 tokens, rank 8kq + e
 //   bks  B_K scales     [kq][s][e]: dim 32s + 8kq + e (column-wise, one run)
@@ -49,15 +50,18 @@ __host__ __device__ inline FactorLayout factor_layout(int P, int d, int rk, int 
 //   bvs  B_V scales     [q][dt][v]: dim 16dt + 4q + v (column-wise, one run)
 //   avs  A_V scales     [q][tt][v]: token tau(tt, 4q + v) (row-wise, one run)
 //   avc  A_V^T codes    [i][kq][rt][ks] dwords: rank row pi(rt, i), tokens 32ks + 8kq + e
+//   pad  32 bytes of 0x88 (eight zero codes per dword)
 // where pi and tau are the attention kernel's tile row maps. Each section is
 // ordered so that one lane of that kernel reads its operand slice as one
-// 16-byte piece, and the sections whose rows can pass the page's rank (bkc,
-// avc) end the key and value halves, so those reads fall outside the page.
+// 16-byte piece. Reads of key rows past the rank fall outside the key half
+// and return zero words; value reads past the rank are pointed at the pad,
+// so they decode as zero codes.
 __host__ __device__ inline int r8(int r) { return (r + 7) & ~7; }
 __host__ __device__ inline int int4_nib(int e) { return 4 * (e >> 1) + 16 * (e & 1); }
 struct Int4Layout {
-    int64_t akc, aks, bks, bkc, keys_end, bvc, bvs, avs, avc, end;
+    int64_t akc, aks, bks, bkc, keys_end, bvc, bvs, avs, avc, pad, end;
 };
+constexpr int kInt4Pad = 32;
 __host__ __device__ inline Int4Layout int4_layout(int P, int d, int rk, int rv) {
     Int4Layout f;
     f.akc = 0;
@@ -69,7 +73,8 @@ __host__ __device__ inline Int4Layout int4_layout(int P, int d, int rk, int rv) 
     f.bvs = f.bvc + (int64_t)r8(rv) * d / 2;
     f.avs = f.bvs + 2LL * d;
     f.avc = f.avs + 2LL * P;
-    f.end = f.avc + (int64_t)r8(rv) * P / 2;
+    f.pad = f.avc + (int64_t)r8(rv) * P / 2;
+    f.end = f.pad + kInt4Pad;
     return f;
 }
 // Tile row maps shared by the INT4 layout and the attention kernel: rank tile
