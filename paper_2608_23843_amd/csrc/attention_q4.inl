@@ -8,8 +8,9 @@
 //                        (the R~_K column scale folded into the query); the
 //                        raw words' offset is one more product, -beta x B,
 //                        used as the accumulator's start
-//   S^T = L~_K Z^T       fp16 MFMA, A = code x scale (rounded once), B = Z
-//                        as fp16 hi/lo
+//   S^T = L~_K Z^T       fp16 MFMA, A = raw code word, B = s o Z (the L~_K
+//                        scale folded into Z in fp32, one B per 32-token run)
+//                        as fp16 hi/lo; started from -beta x B
 //   Y^T = L~_V^T E'^T    fp16 MFMA, A = raw code word, B = E' = E x (row
 //                        scale of L~_V) in fp16; started from -beta x E'
 //   O^T += s .* (R~_V^T Y^T)  fp16 MFMA, A = raw code word, B = Y hi/lo,
@@ -71,18 +72,6 @@ __device__ inline f16x8 q4_frag_raw(uint32_t x, const Q4Consts &k, uint32_t magi
     return __builtin_bit_cast(f16x8, p);
 }
 __device__ inline f16x8 q4_frag_raw(uint32_t x, const Q4Consts &k) { return q4_frag_raw(x, k, k.h16); }
-// Eight codes -> fp16 code x scale, rounded once: (1024 + n) - 1032 = c and
-// (1024 + 16 n) - 1152 = 16 c are exact; sc holds the scales as four fp16
-// pairs, those of pairs 1 and 3 already divided by 16.
-__device__ inline f16x8 q4_frag_scaled(uint32_t x, const u32x4 &sc, const Q4Consts &k) {
-    const f16x8 h = q4_frag_raw(x, k);
-    const f16x8 bias = f16x8{-1032, -1032, -1152, -1152, -1032, -1032, -1152, -1152};
-    // the scale words go through scalars: a bit_cast of a vector element
-    // expression reads element 0 whatever the index
-    const uint32_t s0 = sc[0], s1 = sc[1], s2 = sc[2], s3 = sc[3];
-    const f16x8 s = __builtin_bit_cast(f16x8, u32x4{s0, s1, s2, s3});
-    return (h + bias) * s;
-}
 // Scale words of one lane with pairs 1 and 3 divided by 16 (exact unless subnormal).
 __device__ inline u32x4 q4_scale_div16(const u32x4 &sc) {
     const f16x2 r16 = f16x2{(_Float16)0.0625f, (_Float16)0.0625f};
@@ -265,14 +254,36 @@ __device__ inline void q4_scores(const Q4Key &f, const f16x8 (&qh16)[4][64], int
 #pragma unroll
         for (int s = 0; s < 4; ++s) z[rt] = mfma_f16(q4_frag_raw(f.bkc[rt][s], k), qs[s], z[rt]);
     }
-    f16x8 zh, zl;
-    split_tiles_f16(z[0], z[1], zh, zl);
-    const u32x4 ak0 = q4_scale_div16(f.aks[0]), ak1 = q4_scale_div16(f.aks[1]);
+    // S^T = L~_K Z^T with the L~_K scale (per 32-token run u and rank) folded
+    // into Z in fp32: Z_u = s_u o Z, split into fp16 hi/lo (ranks of pairs 1
+    // and 3 also / 16, through the scale), and A = raw code words, each token
+    // tile started from -beta x Z_u of its run. Every product is then exact.
+    float zero = 0.f;
+    asm("" : "+v"(zero));
+    f16x8 zh[2], zl[2];
+    f32x4 sb[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+        const u32x4 sc = q4_scale_div16(f.aks[u]);
+        f32x4 zs[2];
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+            for (int v = 0; v < 4; v += 2) {
+                const uint32_t pair = sc[2 * rt + (v >> 1)];
+                const f16x2 s2 = __builtin_bit_cast(f16x2, pair);
+                zs[rt][v] = fmaf(z[rt][v], (float)s2[0], zero);
+                zs[rt][v + 1] = fmaf(z[rt][v + 1], (float)s2[1], zero);
+            }
+        split_tiles_f16(zs[0], zs[1], zh[u], zl[u]);
+        sb[u] = mfma_f16(nbeta, zh[u], zero_f4());
+        sb[u] = mfma_f16(nbeta, zl[u], sb[u]);
+    }
 #pragma unroll
     for (int tt = 0; tt < 4; ++tt) {
-        const f16x8 a = q4_frag_scaled(f.akc[tt], tt < 2 ? ak0 : ak1, k);
-        st[tt] = mfma_f16(a, zh, zero_f4());
-        st[tt] = mfma_f16(a, zl, st[tt]);
+        const f16x8 a = q4_frag_raw(f.akc[tt], k);
+        st[tt] = mfma_f16(a, zh[tt >> 1], sb[tt >> 1]);
+        st[tt] = mfma_f16(a, zl[tt >> 1], st[tt]);
     }
 }
 
