@@ -115,51 +115,97 @@ __global__ __launch_bounds__(64) void k_compress(Geo g, pkv_page *table, const c
     }
 
     // ---- one-sided Jacobi on G ---------------------------------------------
+    // Columns are carried as d_c * g~_c (and d_c * j~_c: J takes the same
+    // rotations, so the same scale). Rotating the pair (c, p) by (cs, sn) is
+    // then g~_c += mu g~_p, d_c *= cs with mu = +-tan * d_p / d_c: one fma per
+    // element of G and of J instead of two. |g_c|^2 is carried along (from
+    // the pair's alpha, beta, gamma) and recomputed, with the scales folded
+    // back in, at the start of every sweep. G is first divided by its
+    // Frobenius norm, so no scaled entry can overflow within a sweep
+    // (d_c >= 2^-32 after 63 rotations).
     float nrm2 = 0.f;
 #pragma unroll
     for (int k = 0; k < P; ++k) nrm2 = fmaf(gcol[k], gcol[k], nrm2);
     float fro2 = nrm2;
     for (int m = 1; m < P; m <<= 1) fro2 += wave_shfl_xor(fro2, m);
+    const float gnorm = sqrtf(fro2);
+    const float ginv = fro2 > 0.f ? 1.f / gnorm : 0.f;
+#pragma unroll
+    for (int k = 0; k < P; ++k) gcol[k] *= ginv;
     const float tol = (float)P * 1.1920929e-7f;        // P * 2^-23
-    const float tiny2 = tol * tol * fro2;
+    const float tiny2 = fro2 > 0.f ? tol * tol : 0.f;  // relative to |G|_F^2 = 1
 
+    // Only the top r eigenvectors are stored, and a column whose G-image is
+    // orthogonal to every other column's is an exact eigenvector whatever
+    // the remaining pairs do (G j_c _|_ G j_p for all p gives G^2 j_c || j_c).
+    // So a sweep counts as converged when no pair involving one of the r
+    // columns of largest |G j| (ranked during the previous sweep; all
+    // columns in the first) still needed a rotation.
+    const int r_need = which == 0 ? rk : rv;
+    float dsc = 1.f, alpha = 0.f;
+    bool top = true;
     int sweeps = 0;
     bool more = true;
     while (more && sweeps < kMaxSweeps) {
         ++sweeps;
+        int larger = 0;   // columns ranked above this one during this sweep
+        alpha = 0.f;
+#pragma unroll
+        for (int k = 0; k < P; ++k) {
+            gcol[k] *= dsc;
+            jcol[k] *= dsc;
+            alpha = fmaf(gcol[k], gcol[k], alpha);
+        }
+        dsc = 1.f;
         int rotated = 0;
         for (int m = 1; m < P; ++m) {
             float pg[P];
-            float alpha = 0.f, gamma = 0.f;
+            float gt = 0.f;
 #pragma unroll
             for (int k = 0; k < P; ++k) {
                 pg[k] = wave_shfl_xor(gcol[k], m);
-                alpha = fmaf(gcol[k], gcol[k], alpha);
-                gamma = fmaf(gcol[k], pg[k], gamma);
+                gt = fmaf(gcol[k], pg[k], gt);
             }
             const float beta = wave_shfl_xor(alpha, m);
+            const float dp = wave_shfl_xor(dsc, m);
+            const int top_p = __shfl_xor(top ? 1 : 0, m, 64);
+            larger += (beta > alpha || (beta == alpha && (c ^ m) < c)) ? 1 : 0;
+            const float gamma = gt * dsc * dp;
             const bool lo = c < (c ^ m);
             const float a_lo = lo ? alpha : beta, a_hi = lo ? beta : alpha;
-            float cs = 1.f, sn = 0.f;
-            if (a_lo > tiny2 && a_hi > tiny2 && fabsf(gamma) > tol * sqrtf(a_lo * a_hi)) {
-                const float zeta = (a_hi - a_lo) / (2.f * gamma);
-                const float t = (zeta >= 0.f ? 1.f : -1.f) / (fabsf(zeta) + sqrtf(fmaf(zeta, zeta, 1.f)));
-                cs = 1.f / sqrtf(fmaf(t, t, 1.f));
-                sn = cs * t;
-                rotated = 1;
-            }
-            const float s_eff = lo ? -sn : sn;
+            // rotation parameters without branches; the hardware reciprocal
+            // and reciprocal square root (about 1 ulp) suffice here, the
+            // eigenvectors are renormalized at the end
+            const bool rot = a_lo > tiny2 && a_hi > tiny2 && fabsf(gamma) > tol * sqrtf(a_lo * a_hi);
+            const float zeta = (a_hi - a_lo) * __builtin_amdgcn_rcpf(2.f * gamma);
+            const float tz = __builtin_copysignf(
+                __builtin_amdgcn_rcpf(fabsf(zeta) + __builtin_amdgcn_sqrtf(fmaf(zeta, zeta, 1.f))), zeta);
+            const float t = rot ? tz : 0.f;
+            const float cs = rot ? __builtin_amdgcn_rsqf(fmaf(t, t, 1.f)) : 1.f;
+            rotated |= (rot && (top || top_p)) ? 1 : 0;
+            const float t_eff = lo ? -t : t;       // the lower column takes -sn
+            const float mu = t_eff * (dp * __builtin_amdgcn_rcpf(dsc));
 #pragma unroll
-            for (int k = 0; k < P; ++k) gcol[k] = fmaf(cs, gcol[k], s_eff * pg[k]);
+            for (int k = 0; k < P; ++k) gcol[k] = fmaf(mu, pg[k], gcol[k]);
 #pragma unroll
             for (int k = 0; k < P; ++k) {
                 const float pj = wave_shfl_xor(jcol[k], m);
-                jcol[k] = fmaf(cs, jcol[k], s_eff * pj);
+                jcol[k] = fmaf(mu, pj, jcol[k]);
             }
+            const float s_eff = cs * t_eff;
+            alpha = fmaf(cs * cs, alpha, fmaf(2.f * cs * s_eff, gamma, s_eff * s_eff * beta));
+            dsc *= cs;
         }
-        more = __any(rotated);
+        const bool top_new = larger < r_need;
+        more = __any(rotated || top_new != top);   // converged only on a settled ranking
+        top = top_new;
     }
     if (more && active && c == 0) raise_status(PKV_DEV_NO_CONVERGE);
+#pragma unroll
+    for (int k = 0; k < P; ++k) {
+        gcol[k] *= dsc * gnorm;   // back to G J
+        jcol[k] *= dsc;
+    }
 
     // ---- eigenvalues, order (descending; ties keep the lower index) --------
     // Rotations by tiny angles round cos to 1 and grow |j_c| slightly, so each
