@@ -117,3 +117,90 @@ def test_fullsize_qwen32b_128k_bf16():
 def test_fullsize_qwen32b_int4():
     """B=8, same heads and length, INT4 factors with fp16 scales."""
     _run("qwen32b_int4", [(0, 0), (4, 3), (7, 7)], 0)
+
+
+def test_fullsize_llama8b_32k_all_heads():
+    """B=1, 32 q / 8 kv heads, d=128, P=64, T=32768, S=64, W=256, r=24: every KV head."""
+    checked = _run("llama8b_32k", [(0, h) for h in range(8)], 2)
+    assert checked == 8 * 2 * 2
+
+
+def test_fullsize_incremental_window_boundary():
+    """Incremental decode at full size: batch 32, Llama-3-8B heads, prefill
+    16K, then 65 decode steps. Each step appends one token per sequence;
+    when pages leave the window (once here, at the 64th step) all 32 x 8
+    newly eligible pages are compressed before that step's attention. The
+    page table, the new factor pages and sampled heads' attention after the
+    boundary are checked against the oracle."""
+    import torch
+    import paper_2608_23843_amd as pk
+    wl = synth.WORKLOADS["llama8b_incremental"]
+    B, Hkv, Hq, d, P, T, S, W = (wl.batch, wl.kv_heads, wl.q_heads, wl.head_dim, wl.page, wl.tokens, wl.sink,
+                                 wl.window)
+    steps = 65
+    max_pages = -(-(T + steps + 1) // P) + 1
+    K, V = synth.kv_layer(wl, 0, 0, T, workers=16)
+    ranks = synth.page_ranks(wl, 0, 0, max_pages)
+    r = int(wl.ranks[0])
+    cache = pk.PuzzleKVCache(1, B, Hkv, Hq, d, P, max_pages, r, S, W, wl.dtype, wl.factors)
+    kt = torch.from_numpy(K).to("cuda", torch.bfloat16)
+    vt = torch.from_numpy(V).to("cuda", torch.bfloat16)
+    rt = torch.from_numpy(ranks).cuda().contiguous()
+    cache.prefill(0, kt, vt, [T] * B, rank_k=rt, rank_v=rt)
+    del kt, vt
+    ws = cache.workspace(pk.PKV_OP_ATTENTION, T + steps + 1)
+    new_pages = []
+    Kd, Vd = {}, {}
+    for s in range(steps):
+        pos = T + s
+        kn, vn = synth.decode_kv(wl, 0, 0, pos)
+        Kd[pos], Vd[pos] = kn, vn
+        cache.append(0, torch.from_numpy(kn).to("cuda", torch.bfloat16).contiguous(),
+                     torch.from_numpy(vn).to("cuda", torch.bfloat16).contiguous(), [pos] * B)
+        el = pk.eligible_pages(pos, pos + 1, P, S, W)
+        if len(el):
+            bb, hh, jj = zip(*[(b, h, int(j)) for b in range(B) for h in range(Hkv) for j in el])
+            cache.compress_pages(0, bb, hh, jj, r, r)
+            new_pages += list(el)
+        out, lse = cache.attention(0, torch.from_numpy(synth.queries(wl, 0, s)).to("cuda", torch.bfloat16).contiguous(),
+                                   [pos + 1] * B, workspace=ws)
+    torch.cuda.synchronize()
+    assert cache.device_status() == 0
+    assert new_pages == [(T - W) // P]          # one page leaves the window in 65 steps
+    Tn = T + steps
+    n = -(-Tn // P)
+    kinds = oracle.plan_pages(Tn, P, S, W, n)
+    _, kind, rk, rv = cache.page_table_host(0)
+    assert np.array_equal(kind[:, :, :n], np.broadcast_to(kinds, (B, Hkv, n)))
+    fac = kinds == oracle.FACTOR
+    assert np.all(rk[:, :, :n][:, :, fac] == r) and np.all(rv[:, :, :n][:, :, fac] == r)
+    q = synth.queries(wl, 0, steps - 1)
+    out = out.cpu().numpy().astype(np.float64)
+    lse = lse.cpu().numpy().astype(np.float64)
+    g = wl.group
+    for (b, h) in [(0, 0), (13, 4), (31, 7)]:
+        blk = cache.export_pages(0, [b] * n, [h] * n, list(range(n))).cpu().numpy().astype(np.float64)
+        pages = []
+        for j in range(n):
+            o = blk[j]
+            if kinds[j] == oracle.FACTOR:
+                pages.append(("factor", o[:P * r].reshape(P, r), o[P * r:P * r + r * d].reshape(r, d),
+                              o[P * r + r * d:2 * P * r + r * d].reshape(P, r),
+                              o[2 * P * r + r * d:2 * P * r + 2 * r * d].reshape(r, d)))
+            else:
+                pages.append(("dense", o[:P * d].reshape(P, d), o[P * d:2 * P * d].reshape(P, d)))
+        # the dense pages hold the appended tokens as stored (bf16)
+        for pos in range(T, Tn):
+            j, row = divmod(pos, P)
+            assert np.array_equal(pages[j][1][row], synth.round_storage(Kd[pos][b, h], "bf16").astype(np.float64))
+            assert np.array_equal(pages[j][2][row], synth.round_storage(Vd[pos][b, h], "bf16").astype(np.float64))
+        # the page compressed during decode is the decomposition of its stored page
+        j = new_pages[0]
+        _check_factor(pages[j][1], pages[j][2], K[b, h, j * P:(j + 1) * P].astype(np.float64), r, 6e-3, 1e-2, 4e-3)
+        _check_factor(pages[j][3], pages[j][4], V[b, h, j * P:(j + 1) * P].astype(np.float64), r, 6e-3, 1e-2, 4e-3)
+        head = oracle.HeadCache(Tn, P, d, pages)
+        ro, rl = oracle.attention(head, q[b, h * g:(h + 1) * g].astype(np.float64))
+        ma, mr = errors(out[b, h * g:(h + 1) * g], ro)
+        print("llama8b_incremental head (%d, %d) at T=%d: max-abs %.3e, normwise mean-relative %.3e" % (b, h, Tn, ma, mr))
+        assert ma <= MAX_ABS and mr <= MEAN_REL, (b, h, ma, mr)
+        assert np.abs(lse[b, h * g:(h + 1) * g] - rl).max() <= 1e-3
