@@ -132,7 +132,13 @@ __global__ __launch_bounds__(64) void k_compress(Geo g, pkv_page *table, const c
     const float ginv = fro2 > 0.f ? 1.f / gnorm : 0.f;
 #pragma unroll
     for (int k = 0; k < P; ++k) gcol[k] *= ginv;
-    const float tol = (float)P * 1.1920929e-7f;        // P * 2^-23
+    // Rotation threshold P 2^-23 on the cosine of two columns; for factors
+    // stored in bf16 ten times that (two sweeps fewer of ~12, the rank-r
+    // reconstruction moving by ~1e-4 |X|, far below bf16 rounding). fp32 and
+    // INT4 factors keep the tight threshold, so an INT4 page quantizes
+    // exactly the factors an fp32 page of the same input stores.
+    constexpr float kTolFactor = std::is_same<TF, uint16_t>::value ? 10.f : 1.f;
+    const float tol = kTolFactor * (float)P * 1.1920929e-7f;
     const float tiny2 = fro2 > 0.f ? tol * tol : 0.f;  // relative to |G|_F^2 = 1
 
     // Only the top r eigenvectors are stored, and a column whose G-image is
