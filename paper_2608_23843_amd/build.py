@@ -13,7 +13,7 @@ INCLUDE = os.path.join(ROOT, "include")
 LIB = os.path.join(HERE, "libpuzzlekv.so")
 
 SOURCES = ["pkv_kernels.hip", "pkv_host.cpp"]
-DEPS = ["pkv_internal.h", "cache_ops.inl", "int4.inl", "compress.inl", "attention.inl", "attention_mfma.inl", "attention_q4.inl",
+DEPS = ["pkv_internal.h", "cache_ops.inl", "int4.inl", "compress.inl", "compress_qr.inl", "attention.inl", "attention_mfma.inl", "attention_q4.inl",
         "attention_launch.inl"]
 
 
@@ -33,6 +33,10 @@ def flags() -> list[str]:
         # later; the wave-level atomic rewrite would read it at once, waiting
         # for every load issued before it
         "-mllvm", "-amdgpu-atomic-optimizer-strategy=None",
+        # matrix-core accumulators in VGPRs: the decomposition's Gram tiles are
+        # short-lived and AGPRs would cost it a wave per SIMD (every other
+        # kernel compiles to the same code either way)
+        "-mllvm", "-amdgpu-mfma-vgpr-form=1",
         "-Wno-unused-command-line-argument",
         "-I", INCLUDE, "-I", CSRC,
     ]

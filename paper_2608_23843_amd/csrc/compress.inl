@@ -33,6 +33,62 @@ struct q4_t {};
 template <typename TF> struct is_q4 { static constexpr bool value = false; };
 template <> struct is_q4<q4_t> { static constexpr bool value = true; };
 
+// One decomposition of a compress or prefill launch: which page, which half
+// (K or V), its ranks and where its P x d values are. A page that is not
+// dense (compress mode) raises PKV_DEV_NOT_DENSE when `report` is set and
+// leaves the decomposition inactive.
+struct DecompRef {
+    bool active;
+    int b, h, j, rk, rv, which;
+    const void *X;
+    bool transposed;   // X is V^T (d x P), the dense slot's value layout
+};
+
+template <typename TX>
+__device__ inline DecompRef decode_decomp(const Geo &g, const pkv_page *table, const char *dense,
+                                          const CompressItems &items, const CompressSrc &src, int64_t q,
+                                          int64_t n_decomp, bool report) {
+    DecompRef r{};
+    r.active = q < n_decomp;
+    r.rk = r.rv = 1;
+    r.which = (int)(q & 1);
+    if (!r.active) return r;
+    const int64_t item = q >> 1;
+    if (src.mode == SRC_CACHE) {
+        const CompressItem it = items.it[item];
+        r.b = it.b; r.h = it.h; r.j = it.j; r.rk = it.rk; r.rv = it.rv;
+        const pkv_page e = table[g.head_index(r.b, r.h) * g.max_pages + r.j];
+        if (e.kind != PKV_DENSE) {
+            if (report) raise_status(PKV_DEV_NOT_DENSE);
+            r.active = false;
+        } else {
+            const TX *slot = (const TX *)(dense + e.slot * g.dense_slot_bytes);
+            r.X = r.which == 0 ? slot : slot + (int64_t)g.P * g.d;
+            r.transposed = r.which == 1;
+        }
+    } else {
+        int bb = 0;
+        while (bb + 1 < src.off.n - 1 && src.off.len[bb + 1] <= item) ++bb;
+        const int64_t local = item - src.off.len[bb];
+        const int64_t nf = (src.off.len[bb + 1] - src.off.len[bb]) / g.Hkv;
+        r.b = bb;
+        r.h = (int)(local / nf);
+        r.j = g.sink_pages + (int)(local % nf);
+        const int64_t head = g.head_index(r.b, r.h);
+        if (src.rank_k) {
+            const int rmax = min(g.max_rank, min(g.P, g.d));
+            r.rk = max(1, min((int)src.rank_k[head * g.max_pages + r.j], rmax));
+            r.rv = max(1, min((int)src.rank_v[head * g.max_pages + r.j], rmax));
+        } else {
+            r.rk = src.def_rk;
+            r.rv = src.def_rv;
+        }
+        const TX *base = (const TX *)(r.which == 0 ? src.k : src.v);
+        r.X = base + (head * src.src_tokens + (int64_t)r.j * g.P) * g.d;
+    }
+    return r;
+}
+
 template <typename TX, typename TF, int P>
 __global__ __launch_bounds__(64) void k_compress(Geo g, pkv_page *table, const char *dense, char *factor,
                                                  CompressItems items, CompressSrc src, int64_t n_decomp) {
@@ -48,46 +104,11 @@ __global__ __launch_bounds__(64) void k_compress(Geo g, pkv_page *table, const c
     TX *sX = sX_all + (int64_t)grp * P * ld_x;
 
     // ---- which page, which half (K or V), ranks, source --------------------
-    bool active = q < n_decomp;
-    int b = 0, h = 0, j = 0, rk = 1, rv = 1;
-    const int which = (int)(q & 1);
-    const TX *X = nullptr;
-    bool transposed = false;
-    if (active) {
-        const int64_t item = q >> 1;
-        if (src.mode == SRC_CACHE) {
-            const CompressItem it = items.it[item];
-            b = it.b; h = it.h; j = it.j; rk = it.rk; rv = it.rv;
-            const pkv_page e = table[g.head_index(b, h) * g.max_pages + j];
-            if (e.kind != PKV_DENSE) {
-                if (c == 0) raise_status(PKV_DEV_NOT_DENSE);
-                active = false;
-            } else {
-                const TX *slot = (const TX *)(dense + e.slot * g.dense_slot_bytes);
-                X = which == 0 ? slot : slot + (int64_t)g.P * d;
-                transposed = which == 1;
-            }
-        } else {
-            int bb = 0;
-            while (bb + 1 < src.off.n - 1 && src.off.len[bb + 1] <= item) ++bb;
-            const int64_t local = item - src.off.len[bb];
-            const int64_t nf = (src.off.len[bb + 1] - src.off.len[bb]) / g.Hkv;
-            b = bb;
-            h = (int)(local / nf);
-            j = g.sink_pages + (int)(local % nf);
-            const int64_t head = g.head_index(b, h);
-            if (src.rank_k) {
-                const int rmax = min(g.max_rank, min(g.P, g.d));
-                rk = max(1, min((int)src.rank_k[head * g.max_pages + j], rmax));
-                rv = max(1, min((int)src.rank_v[head * g.max_pages + j], rmax));
-            } else {
-                rk = src.def_rk;
-                rv = src.def_rv;
-            }
-            const TX *base = (const TX *)(which == 0 ? src.k : src.v);
-            X = base + (head * src.src_tokens + (int64_t)j * P) * d;
-        }
-    }
+    const DecompRef ref = decode_decomp<TX>(g, table, dense, items, src, q, n_decomp, c == 0);
+    bool active = ref.active;
+    const int b = ref.b, h = ref.h, j = ref.j, rk = ref.rk, rv = ref.rv, which = ref.which;
+    const TX *X = (const TX *)ref.X;
+    const bool transposed = ref.transposed;
 
     // ---- stage X (P x d) in LDS -------------------------------------------
     if (active) {
@@ -328,9 +349,16 @@ hipError_t launch_compress_p(const LaunchCtx &L, const CompressItems &items, con
     }
 }
 
+inline bool compress_qr_supported(const Geo &g);
+hipError_t launch_compress_qr(const LaunchCtx &L, const CompressItems &items, const CompressSrc &src,
+                              int64_t n_decomp);
+
+// bf16 pages of 32 or 64 tokens take the matrix-core path (k_compress_qr);
+// fp32 pages and 16-token pages the one-wave Gram + Jacobi kernel above.
 hipError_t launch_compress_any(const LaunchCtx &L, const CompressItems &items, const CompressSrc &src,
                                int64_t n_decomp) {
     if (n_decomp <= 0) return hipSuccess;
+    if (compress_qr_supported(L.geo)) return launch_compress_qr(L, items, src, n_decomp);
     if (L.geo.factor_dtype == PKV_INT4) {   // validated: bf16 dense pages, P = 64
         if (L.geo.P != 64 || L.geo.dense_dtype != PKV_BF16) return hipErrorInvalidValue;
         return launch_compress_t<uint16_t, q4_t, 64>(L, items, src, n_decomp);

@@ -1,0 +1,506 @@
+// Batched per-page truncated decomposition for bf16 pages of P = 32 or 64
+// tokens: the path pkv_compress_pages and pkv_prefill take for bf16 dense
+// pages (Section 3.3, Eq. (2)). The result is the one k_compress computes --
+// the top-r eigenvectors L of the page's Gram matrix G = X X^T and R = L^T X,
+// the rank-r truncated-SVD factors -- reached in four phases per wavefront
+// (one page half for P = 64, two for P = 32, one per 32-lane half):
+//
+//  1. G by matrix-core products (32x32x16 bf16: exact products, fp32
+//     accumulation) with operands loaded straight from the page, then one
+//     permlane32 swap per pair of accumulator registers so that lane c holds
+//     all of column c of G (rows in the accumulator's row order, which no
+//     later step depends on).
+//  2. A backward-stable QR of G: modified Gram-Schmidt with the columns taken
+//     in order of decreasing norm, keeping only R. The computed R is the exact
+//     R of G + dG with |dG| ~ eps |G| (Bjorck), and with G Pi = Q R the matrix
+//     G Q = Pi R^T has the eigenvectors of G as its left singular vectors and
+//     the eigenvalues as its singular values. Its rows are graded, so the
+//     Jacobi iteration converges in about half the sweeps it needs on G
+//     itself. Row k of R is written to LDS and read by the lane pivoted at
+//     step k, which no longer needs its column of G: no register indexing,
+//     no transposition buffer.
+//  3. One-sided Jacobi on the columns of Pi R^T (xor pairing: step m pairs
+//     lane c with lane c ^ m; the partner column is fetched with ds_swizzle
+//     inside a 32-lane half and with ds_bpermute across halves, the swizzle
+//     being three times cheaper), without accumulating the rotations: at
+//     convergence the columns are lambda_c u_c with u_c the eigenvectors, so
+//     L is the normalized columns, orthonormal to the rotation threshold.
+//  4. Ranking and eigenvectors; then R = L^T X with L staged in LDS and
+//     each lane owning two output dims (coalesced page-row reads), stores.
+// Included by pkv_kernels.hip after compress.inl.
+
+namespace pkv {
+
+typedef __bf16 cq_bf16x8 __attribute__((ext_vector_type(8)));
+typedef float cq_f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr float kCqTiny2 = 3.5527137e-15f;   // (2^-24)^2: a column below this (|G|_F = 1) is zero
+
+// Eight consecutive dims of page row `row`, dims k0..k0+7, as an MFMA operand.
+__device__ inline cq_bf16x8 cq_load8(const uint16_t *X, bool transposed, int P, int d, int row, int k0) {
+    if (!transposed) return __builtin_bit_cast(cq_bf16x8, *(const uint4 *)(X + (int64_t)row * d + k0));
+    uint32_t w[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+        w[u] = (uint32_t)X[(int64_t)(k0 + 2 * u) * P + row] | ((uint32_t)X[(int64_t)(k0 + 2 * u + 1) * P + row] << 16);
+    return __builtin_bit_cast(cq_bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
+}
+
+// Page element (t, k) as fp32.
+__device__ inline float cq_elem(const uint16_t *X, bool transposed, int P, int d, int t, int k) {
+    return bf16_to_f32(transposed ? X[(int64_t)k * P + t] : X[(int64_t)t * d + k]);
+}
+
+__device__ inline float cq_f(int v) { return __int_as_float(v); }
+__device__ inline int cq_i(float v) { return __float_as_int(v); }
+
+// Partner values for xor pairing step M < 32 (inside each 32-lane half).
+template <int P, int M>
+__device__ __forceinline__ void cq_swz(const float (&a)[P], float (&pa)[P], float s0, float &p0, float s1, float &p1,
+                                       int s2, int &p2) {
+    constexpr int pat = (M << 10) | 0x1f;   // bitmask mode: and 0x1f, or 0, xor M
+#pragma unroll
+    for (int k = 0; k < P; ++k) pa[k] = cq_f(__builtin_amdgcn_ds_swizzle(cq_i(a[k]), pat));
+    p0 = cq_f(__builtin_amdgcn_ds_swizzle(cq_i(s0), pat));
+    p1 = cq_f(__builtin_amdgcn_ds_swizzle(cq_i(s1), pat));
+    p2 = __builtin_amdgcn_ds_swizzle(s2, pat);
+}
+
+// Partner values for a step that crosses the 32-lane halves (P = 64).
+template <int P>
+__device__ __forceinline__ void cq_bperm(const float (&a)[P], float (&pa)[P], float s0, float &p0, float s1, float &p1,
+                                         int s2, int &p2, int addr) {
+#pragma unroll
+    for (int k = 0; k < P; ++k) pa[k] = cq_f(__builtin_amdgcn_ds_bpermute(addr, cq_i(a[k])));
+    p0 = cq_f(__builtin_amdgcn_ds_bpermute(addr, cq_i(s0)));
+    p1 = cq_f(__builtin_amdgcn_ds_bpermute(addr, cq_i(s1)));
+    p2 = __builtin_amdgcn_ds_bpermute(addr, s2);
+}
+
+// Value of lane `src` (within this lane's P-lane group) of every group.
+template <int P>
+__device__ __forceinline__ float cq_group_bcast(float v, int src0, int src1, int grp) {
+    if constexpr (P == 64) {
+        return cq_f(__builtin_amdgcn_readlane(cq_i(v), src0));
+    } else {
+        const float a = cq_f(__builtin_amdgcn_readlane(cq_i(v), src0));
+        const float b = cq_f(__builtin_amdgcn_readlane(cq_i(v), src1));
+        return grp ? b : a;
+    }
+}
+
+// Sum over the lanes of a P-lane group.
+template <int P>
+__device__ __forceinline__ float cq_group_sum(float v) {
+    v += cq_f(__builtin_amdgcn_ds_swizzle(cq_i(v), (1 << 10) | 0x1f));
+    v += cq_f(__builtin_amdgcn_ds_swizzle(cq_i(v), (2 << 10) | 0x1f));
+    v += cq_f(__builtin_amdgcn_ds_swizzle(cq_i(v), (4 << 10) | 0x1f));
+    v += cq_f(__builtin_amdgcn_ds_swizzle(cq_i(v), (8 << 10) | 0x1f));
+    v += cq_f(__builtin_amdgcn_ds_swizzle(cq_i(v), (16 << 10) | 0x1f));
+    if constexpr (P == 64) v += cq_f(__builtin_amdgcn_ds_bpermute((int)((threadIdx.x ^ 32) << 2), cq_i(v)));
+    return v;
+}
+
+// Rank of `key` among the P lanes of the group: descending, ties to the lower lane.
+template <int P>
+__device__ __forceinline__ int cq_rank(float key, int c, int grp) {
+    int rho = 0;
+    for (int k = 0; k < P; ++k) {
+        const float kk = cq_group_bcast<P>(key, k, 32 + k, grp);
+        rho += (kk > key) || (kk == key && k < c);
+    }
+    return rho;
+}
+
+template <typename TF, int P>
+__global__ __launch_bounds__(64) void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor,
+                                                    CompressItems items, CompressSrc src, int64_t n_decomp) {
+    static_assert(P == 32 || P == 64, "P = 32 or 64");
+    constexpr int D = 64 / P;
+    extern __shared__ float cq_smem[];
+    const int d = g.d;
+    const int lane = threadIdx.x;
+    const int grp = P == 64 ? 0 : lane >> 5;
+    const int c = P == 64 ? lane : lane & 31;
+    const int64_t q = (int64_t)blockIdx.x * D + grp;
+
+    const DecompRef ref = decode_decomp<uint16_t>(g, table, dense, items, src, q, n_decomp, c == 0);
+    const bool active = ref.active;
+    const uint16_t *X = (const uint16_t *)ref.X;
+
+    // ---- 1. Gram matrix by MFMA, lane c <- column c ------------------------
+    float gc[P];
+    {
+        const int row = lane & 31, kh = lane >> 5;
+        if constexpr (P == 64) {
+            cq_f32x16 c00 = {}, c01 = {}, c10 = {}, c11 = {};
+            if (active) {
+                for (int s = 0; s < d / 16; ++s) {
+                    const int k0 = 16 * s + 8 * kh;
+                    const cq_bf16x8 a0 = cq_load8(X, ref.transposed, P, d, row, k0);
+                    const cq_bf16x8 a1 = cq_load8(X, ref.transposed, P, d, 32 + row, k0);
+                    c00 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, a0, c00, 0, 0, 0);
+                    c01 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, a1, c01, 0, 0, 0);
+                    c10 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, a0, c10, 0, 0, 0);
+                    c11 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, a1, c11, 0, 0, 0);
+                }
+            }
+            // C[m][n] sits in lane 32 (m/4 % 2) + n; swapping the upper half of
+            // the column-tile-0 accumulator with the lower half of column tile 1
+            // gives lane c all of column c (rows 0..31), likewise for rows 32..63.
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const auto r0 = __builtin_amdgcn_permlane32_swap(__float_as_uint(c00[i]), __float_as_uint(c01[i]), false, false);
+                const auto r1 = __builtin_amdgcn_permlane32_swap(__float_as_uint(c10[i]), __float_as_uint(c11[i]), false, false);
+                gc[i] = __uint_as_float(r0[0]);
+                gc[16 + i] = __uint_as_float(r0[1]);
+                gc[32 + i] = __uint_as_float(r1[0]);
+                gc[48 + i] = __uint_as_float(r1[1]);
+            }
+        } else {
+            // two pages per wave: each lane feeds both pages' operands
+            const uint64_t xbits = (uint64_t)(uintptr_t)X;
+            const uint64_t x0 = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(xbits >> 32), 0) << 32) |
+                                (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)xbits, 0);
+            const uint64_t x1 = ((uint64_t)(uint32_t)__builtin_amdgcn_readlane((int)(xbits >> 32), 32) << 32) |
+                                (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)xbits, 32);
+            const int act0 = __builtin_amdgcn_readlane(active ? 1 : 0, 0);
+            const int act1 = __builtin_amdgcn_readlane(active ? 1 : 0, 32);
+            const int tr0 = __builtin_amdgcn_readlane(ref.transposed ? 1 : 0, 0);
+            const int tr1 = __builtin_amdgcn_readlane(ref.transposed ? 1 : 0, 32);
+            cq_f32x16 cg0 = {}, cg1 = {};
+            for (int s = 0; s < d / 16; ++s) {
+                const int k0 = 16 * s + 8 * kh;
+                if (act0) {
+                    const cq_bf16x8 a = cq_load8((const uint16_t *)(uintptr_t)x0, tr0, P, d, row, k0);
+                    cg0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, a, cg0, 0, 0, 0);
+                }
+                if (act1) {
+                    const cq_bf16x8 a = cq_load8((const uint16_t *)(uintptr_t)x1, tr1, P, d, row, k0);
+                    cg1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, a, cg1, 0, 0, 0);
+                }
+            }
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(cg0[i]), __float_as_uint(cg1[i]), false, false);
+                gc[i] = __uint_as_float(r[0]);
+                gc[16 + i] = __uint_as_float(r[1]);
+            }
+        }
+    }
+
+    // ---- 2. QR of G by modified Gram-Schmidt, R only -----------------------
+    float nrm2 = 0.f;
+#pragma unroll
+    for (int e = 0; e < P; ++e) nrm2 = fmaf(gc[e], gc[e], nrm2);
+    const float fro2 = cq_group_sum<P>(nrm2);
+    const float gnorm = sqrtf(fro2);
+    const float ginv = fro2 > 0.f ? 1.f / gnorm : 0.f;
+#pragma unroll
+    for (int e = 0; e < P; ++e) gc[e] *= ginv;
+    nrm2 *= ginv * ginv;
+    const int prank = cq_rank<P>(nrm2, c, grp);   // pivot order: decreasing column norm
+    float *rowbuf = cq_smem + grp * P;
+    bool done = false;
+    for (int k = 0; k < P; ++k) {
+        const uint64_t bal = __ballot(prank == k);   // one lane per group
+        const int piv0 = __builtin_ctzll(bal);
+        const int piv1 = P == 64 ? piv0 : 32 + __builtin_ctzll(bal >> 32);
+        float x[P];
+#pragma unroll
+        for (int e = 0; e < P; ++e) x[e] = cq_group_bcast<P>(gc[e], piv0, piv1, grp);
+        float nx2a = 0.f, nx2b = 0.f, da = 0.f, db = 0.f;
+#pragma unroll
+        for (int e = 0; e < P; e += 2) {
+            nx2a = fmaf(x[e], x[e], nx2a);
+            nx2b = fmaf(x[e + 1], x[e + 1], nx2b);
+            da = fmaf(x[e], gc[e], da);
+            db = fmaf(x[e + 1], gc[e + 1], db);
+        }
+        const float nx2 = nx2a + nx2b, dot = da + db;
+        const float inv = nx2 > kCqTiny2 ? __builtin_amdgcn_rsqf(nx2) : 0.f;
+        const float rk = done ? 0.f : dot * inv;          // R[k][c]
+        const float f = done ? 0.f : rk * inv;            // projection coefficient
+#pragma unroll
+        for (int e = 0; e < P; ++e) gc[e] = fmaf(-f, x[e], gc[e]);
+        rowbuf[c] = rk;
+        __builtin_amdgcn_wave_barrier();
+        if (prank == k) {   // the pivot's column is finished: it takes row k of R
+#pragma unroll
+            for (int e = 0; e < P; ++e) gc[e] = rowbuf[e];
+            done = true;
+        }
+        __builtin_amdgcn_wave_barrier();
+    }
+
+    // ---- 3. one-sided Jacobi on the columns of Pi R^T -----------------------
+    // Columns are carried as d_c * a~_c: rotating the pair (c, p) is then
+    // a~_c += mu a~_p, d_c *= cos, one fma per element. |a_c|^2 is carried
+    // along and recomputed with the scales folded back in every sweep.
+    constexpr float kTolFactor = std::is_same<TF, uint16_t>::value ? 10.f : 1.f;
+    const float tol = kTolFactor * (float)P * 1.1920929e-7f;
+    const int r_need = ref.which == 0 ? ref.rk : ref.rv;
+    float dsc = 1.f, alpha = 0.f;
+    int topi = 1;
+    int sweeps = 0;
+    bool more = true;
+    while (more && sweeps < kMaxSweeps) {
+        ++sweeps;
+        int larger = 0;
+        float aa = 0.f, ab = 0.f;
+#pragma unroll
+        for (int e = 0; e < P; e += 2) {
+            gc[e] *= dsc;
+            gc[e + 1] *= dsc;
+            aa = fmaf(gc[e], gc[e], aa);
+            ab = fmaf(gc[e + 1], gc[e + 1], ab);
+        }
+        alpha = aa + ab;
+        dsc = 1.f;
+        int rotated = 0;
+        for (int m = 1; m < P; ++m) {
+            float pg[P], beta, dp;
+            int top_p;
+            switch (m) {
+#define PKV_CQ_CASE(M) \
+    case M: cq_swz<P, M>(gc, pg, alpha, beta, dsc, dp, topi, top_p); break;
+                PKV_CQ_CASE(1) PKV_CQ_CASE(2) PKV_CQ_CASE(3) PKV_CQ_CASE(4) PKV_CQ_CASE(5) PKV_CQ_CASE(6)
+                PKV_CQ_CASE(7) PKV_CQ_CASE(8) PKV_CQ_CASE(9) PKV_CQ_CASE(10) PKV_CQ_CASE(11) PKV_CQ_CASE(12)
+                PKV_CQ_CASE(13) PKV_CQ_CASE(14) PKV_CQ_CASE(15) PKV_CQ_CASE(16) PKV_CQ_CASE(17) PKV_CQ_CASE(18)
+                PKV_CQ_CASE(19) PKV_CQ_CASE(20) PKV_CQ_CASE(21) PKV_CQ_CASE(22) PKV_CQ_CASE(23) PKV_CQ_CASE(24)
+                PKV_CQ_CASE(25) PKV_CQ_CASE(26) PKV_CQ_CASE(27) PKV_CQ_CASE(28) PKV_CQ_CASE(29) PKV_CQ_CASE(30)
+                PKV_CQ_CASE(31)
+#undef PKV_CQ_CASE
+            default:
+                cq_bperm<P>(gc, pg, alpha, beta, dsc, dp, topi, top_p, (lane ^ m) << 2);
+                break;
+            }
+            float ga = 0.f, gb = 0.f, gcc = 0.f, gd = 0.f;
+#pragma unroll
+            for (int e = 0; e < P; e += 4) {
+                ga = fmaf(gc[e], pg[e], ga);
+                gb = fmaf(gc[e + 1], pg[e + 1], gb);
+                gcc = fmaf(gc[e + 2], pg[e + 2], gcc);
+                gd = fmaf(gc[e + 3], pg[e + 3], gd);
+            }
+            const float gt = (ga + gb) + (gcc + gd);
+            const int partner = c ^ m;
+            larger += (beta > alpha || (beta == alpha && partner < c)) ? 1 : 0;
+            const float gamma = gt * dsc * dp;
+            const bool lo = c < partner;
+            const float a_lo = lo ? alpha : beta, a_hi = lo ? beta : alpha;
+            const bool rot = a_lo > kCqTiny2 && a_hi > kCqTiny2 && fabsf(gamma) > tol * sqrtf(a_lo * a_hi);
+            const float zeta = (a_hi - a_lo) * __builtin_amdgcn_rcpf(2.f * gamma);
+            const float tz = __builtin_copysignf(
+                __builtin_amdgcn_rcpf(fabsf(zeta) + __builtin_amdgcn_sqrtf(fmaf(zeta, zeta, 1.f))), zeta);
+            const float t = rot ? tz : 0.f;
+            const float cs = rot ? __builtin_amdgcn_rsqf(fmaf(t, t, 1.f)) : 1.f;
+            rotated |= (rot && (topi || top_p)) ? 1 : 0;
+            const float t_eff = lo ? -t : t;   // the lower column takes -sin
+            const float mu = t_eff * (dp * __builtin_amdgcn_rcpf(dsc));
+#pragma unroll
+            for (int e = 0; e < P; ++e) gc[e] = fmaf(mu, pg[e], gc[e]);
+            const float s_eff = cs * t_eff;
+            alpha = fmaf(cs * cs, alpha, fmaf(2.f * cs * s_eff, gamma, s_eff * s_eff * beta));
+            dsc *= cs;
+        }
+        const int top_new = larger < r_need ? 1 : 0;
+        more = __any(rotated || top_new != topi);   // converged only on a settled ranking
+        topi = top_new;
+    }
+    if (more && active && c == 0) raise_status(PKV_DEV_NO_CONVERGE);
+
+    // ---- 4. eigenvalues, ranking, eigenvectors -----------------------------
+    float an2a = 0.f, an2b = 0.f;
+#pragma unroll
+    for (int e = 0; e < P; e += 2) {
+        gc[e] *= dsc;
+        gc[e + 1] *= dsc;
+        an2a = fmaf(gc[e], gc[e], an2a);
+        an2b = fmaf(gc[e + 1], gc[e + 1], an2b);
+    }
+    const float an2 = an2a + an2b;
+    const float lam = sqrtf(an2) * gnorm;   // eigenvalue of G (column norm of G Q J)
+    const int rho = cq_rank<P>(an2, c, grp);
+    const bool tinycol = !(an2 > kCqTiny2);
+    {
+        const float inv = tinycol ? 0.f : __builtin_amdgcn_rsqf(an2);
+#pragma unroll
+        for (int e = 0; e < P; ++e) gc[e] = tinycol ? (e == c ? 1.f : 0.f) : gc[e] * inv;
+    }
+    // A column at rounding level (rank-deficient page) has no direction of
+    // its own: it takes a unit vector, made orthogonal to the columns ranked
+    // above it by Gram-Schmidt in rank order (twice).
+    if (__any(tinycol && rho < r_need)) {
+        const int rmax = max(__builtin_amdgcn_readlane(r_need, 0), __builtin_amdgcn_readlane(r_need, 63));
+        for (int pass = 0; pass < 2; ++pass) {
+            for (int i = 0; i < rmax; ++i) {
+                const uint64_t bal = __ballot(rho == i);
+                const int piv0 = __builtin_ctzll(bal);
+                const int piv1 = P == 64 ? piv0 : 32 + __builtin_ctzll(bal >> 32);
+                float x[P];
+#pragma unroll
+                for (int e = 0; e < P; ++e) x[e] = cq_group_bcast<P>(gc[e], piv0, piv1, grp);
+                float dot = 0.f;
+#pragma unroll
+                for (int e = 0; e < P; ++e) dot = fmaf(x[e], gc[e], dot);
+                if (rho > i && tinycol)
+#pragma unroll
+                    for (int e = 0; e < P; ++e) gc[e] = fmaf(-dot, x[e], gc[e]);
+                __builtin_amdgcn_wave_barrier();
+                if (rho == i + 1 && tinycol) {
+                    float n2 = 0.f;
+#pragma unroll
+                    for (int e = 0; e < P; ++e) n2 = fmaf(gc[e], gc[e], n2);
+                    const float inv = n2 > 0.f ? __builtin_amdgcn_rsqf(n2) : 0.f;
+#pragma unroll
+                    for (int e = 0; e < P; ++e) gc[e] *= inv;
+                }
+            }
+        }
+    }
+    // ---- 5. R = L^T X and the stores -----------------------------------------
+    // L goes to LDS (sL[t][rank], 32 ranks, zero past r). Each lane then owns
+    // two output dims for every rank: one 4-byte load per page row (a row is
+    // one coalesced 256-byte read across the lanes) and 64 fmas against the
+    // row's L entries, read as broadcasts.
+    const int which = ref.which, rk = ref.rk, rv = ref.rv;
+    const int r = which == 0 ? rk : rv;
+    constexpr bool kQ4 = is_q4<TF>::value;
+    float *sL = cq_smem + 64 + grp * (P * 32);   // this group's P x 32 block
+    float *sInvSig = cq_smem + 64 + 64 * 32 + grp * 32;
+    {
+        const float sig = sqrtf(fmaxf(lam, 0.f));
+        const float scale = kQ4 ? sqrtf(sig) : 1.f;   // INT4: L~ = U Sigma^(1/2)
+        if (rho < 32) {
+#pragma unroll
+            for (int t = 0; t < P; ++t) sL[t * 32 + rho] = (rho < r && active) ? gc[t] * scale : 0.f;
+            sInvSig[rho] = sig > 0.f ? 1.f / sig : 0.f;
+        }
+    }
+    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+    __builtin_amdgcn_wave_barrier();
+    if (!active) return;
+
+    const int64_t slot_off = (g.head_index(ref.b, ref.h) * g.max_pages + ref.j) * g.factor_slot_bytes;
+    constexpr int kCols = 2;                      // dims per lane per pass
+    float *sR = cq_smem + 64 + 64 * 32 + 64;      // INT4 only: 32 x d (one group: P = 64)
+    for (int k0 = 0; k0 < d; k0 += kCols * P) {
+        const int k = k0 + kCols * c;
+        const bool kin = k < d;
+        float acc[kCols][32];
+#pragma unroll
+        for (int u = 0; u < kCols; ++u)
+#pragma unroll
+            for (int a = 0; a < 32; ++a) acc[u][a] = 0.f;
+        for (int t = 0; t < P; ++t) {
+            float x0 = 0.f, x1 = 0.f;
+            if (kin) {
+                if (!ref.transposed) {
+                    const uint32_t w = *(const uint32_t *)(X + (int64_t)t * d + k);
+                    x0 = __uint_as_float(w << 16);
+                    x1 = __uint_as_float(w & 0xffff0000u);
+                } else {
+                    x0 = bf16_to_f32(X[(int64_t)k * P + t]);
+                    x1 = bf16_to_f32(X[(int64_t)(k + 1) * P + t]);
+                }
+            }
+            const float4 *lrow = (const float4 *)(sL + t * 32);
+#pragma unroll
+            for (int a4 = 0; a4 < 8; ++a4) {
+                const float4 l = lrow[a4];
+                acc[0][4 * a4 + 0] = fmaf(l.x, x0, acc[0][4 * a4 + 0]);
+                acc[0][4 * a4 + 1] = fmaf(l.y, x0, acc[0][4 * a4 + 1]);
+                acc[0][4 * a4 + 2] = fmaf(l.z, x0, acc[0][4 * a4 + 2]);
+                acc[0][4 * a4 + 3] = fmaf(l.w, x0, acc[0][4 * a4 + 3]);
+                acc[1][4 * a4 + 0] = fmaf(l.x, x1, acc[1][4 * a4 + 0]);
+                acc[1][4 * a4 + 1] = fmaf(l.y, x1, acc[1][4 * a4 + 1]);
+                acc[1][4 * a4 + 2] = fmaf(l.z, x1, acc[1][4 * a4 + 2]);
+                acc[1][4 * a4 + 3] = fmaf(l.w, x1, acc[1][4 * a4 + 3]);
+            }
+        }
+        if (!kin) continue;
+        if constexpr (kQ4) {
+            // R~ = Sigma^(-1/2) R: the accumulation used L~ = L Sigma^(1/2), so divide by sigma
+#pragma unroll
+            for (int u = 0; u < kCols; ++u)
+#pragma unroll
+                for (int a = 0; a < 32; ++a) sR[a * d + k + u] = acc[u][a] * sInvSig[a];
+        } else {
+            const int rk4 = r4(rk), rv4 = r4(rv);
+            const FactorLayout fl = factor_layout(P, d, rk, rv);
+            TF *Ak = (TF *)(factor + slot_off);
+            if (which == 0) {
+                TF *Bk = Ak + fl.bk;                       // R_K, rk x d
+#pragma unroll
+                for (int a = 0; a < 32; ++a)
+                    if (a < rk) {
+                        st(Bk, (int64_t)a * d + k, acc[0][a]);
+                        st(Bk, (int64_t)a * d + k + 1, acc[1][a]);
+                    }
+            } else {
+                TF *Bvt = Ak + fl.bvt;                     // R_V^T, d x r4(rv), zero past rv
+#pragma unroll
+                for (int a = 0; a < 32; ++a)
+                    if (a < rv4) {
+                        st(Bvt, (int64_t)k * rv4 + a, acc[0][a]);
+                        st(Bvt, (int64_t)(k + 1) * rv4 + a, acc[1][a]);
+                    }
+            }
+        }
+    }
+    if constexpr (kQ4) {
+        __builtin_amdgcn_s_waitcnt(0xc07f);
+        __builtin_amdgcn_wave_barrier();
+        float *sScale = sR + 32 * d;
+        const Int4Layout f4 = int4_layout(P, d, rk, rv);
+        q4_quantize_store(factor + slot_off, f4, P, d, r, which, sL, sR, sScale, lane);
+    } else {
+        // L: A_K = L_K (P x r4(rk), zero past rk) row by row, A_V^T = L_V^T (rv x P)
+        const FactorLayout fl = factor_layout(P, d, rk, rv);
+        TF *Ak = (TF *)(factor + slot_off);
+        const int t = c;
+        if (which == 0) {
+            const int rk4 = r4(rk);
+            for (int a = 0; a < rk4; ++a) st(Ak, (int64_t)t * rk4 + a, sL[t * 32 + a]);
+        } else {
+            TF *Avt = Ak + fl.avt;
+            for (int a = 0; a < rv; ++a) st(Avt, (int64_t)a * P + t, sL[t * 32 + a]);
+        }
+    }
+}
+
+// Whether the matrix-core decomposition covers this geometry.
+inline bool compress_qr_supported(const Geo &g) {
+    return g.dense_dtype == PKV_BF16 && (g.P == 32 || g.P == 64) && g.d % 16 == 0 && g.d <= 256;
+}
+
+template <typename TF, int P>
+hipError_t launch_compress_qr_t(const LaunchCtx &L, const CompressItems &items, const CompressSrc &src,
+                                int64_t n_decomp) {
+    constexpr int D = 64 / P;
+    // row buffers (64) + L blocks (64 x 32) + inverse sigmas (64); INT4 adds R~ (32 x d) and scales
+    size_t smem = (64 + 64 * 32 + 64) * sizeof(float);
+    if (is_q4<TF>::value) smem += (size_t)(32 * L.geo.d + 64 + L.geo.d) * sizeof(float);
+    const int64_t blocks = ceil_div(n_decomp, D);
+    LayerPtrs p = layer_ptrs(L);
+    hipLaunchKernelGGL((k_compress_qr<TF, P>), dim3((unsigned)blocks), dim3(64), smem, L.stream, L.geo, p.table,
+                       p.dense, p.factor, items, src, n_decomp);
+    return hipGetLastError();
+}
+
+hipError_t launch_compress_qr(const LaunchCtx &L, const CompressItems &items, const CompressSrc &src,
+                              int64_t n_decomp) {
+    const int ft = L.geo.factor_dtype;
+    if (ft == PKV_INT4) {
+        if (L.geo.P != 64) return hipErrorInvalidValue;
+        return launch_compress_qr_t<q4_t, 64>(L, items, src, n_decomp);
+    }
+    if (L.geo.P == 64)
+        return ft == PKV_BF16 ? launch_compress_qr_t<uint16_t, 64>(L, items, src, n_decomp)
+                              : launch_compress_qr_t<float, 64>(L, items, src, n_decomp);
+    return ft == PKV_BF16 ? launch_compress_qr_t<uint16_t, 32>(L, items, src, n_decomp)
+                          : launch_compress_qr_t<float, 32>(L, items, src, n_decomp);
+}
+
+}  // namespace pkv

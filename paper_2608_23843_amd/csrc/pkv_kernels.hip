@@ -12,6 +12,7 @@
 #include "cache_ops.inl"
 #include "int4.inl"
 #include "compress.inl"
+#include "compress_qr.inl"
 #include "attention.inl"
 #include "attention_mfma.inl"
 #include "attention_launch.inl"

@@ -220,3 +220,89 @@ def test_zero_page():
     Lk, Rk, Lv, Rv = _unpack_factor(blk, P, d, 4)
     assert np.all(Rk == 0) and np.all(Rv == 0)
     assert np.abs(Lk.T @ Lk - np.eye(4)).max() < 1e-6
+
+
+def test_prefill_bf16_pages_rank_above_signal():
+    """Rank 32 on rank-24 + noise key and value pages (bf16 pages, fp32 factors,
+    P = 64). The eight directions past the planted rank are noise directions
+    whose Gram eigenvalues sit four to five decades below the largest one; the
+    decomposition must still resolve them, so the Eckart-Young error is the
+    optimal tail to 1e-4 and every singular value is right to fp32 Gram
+    accuracy."""
+    B, Hkv, d, P, S, W, r = 1, 2, 128, 64, 64, 256, 32
+    T = 64 * 10
+    cache, K, V, npg = _prefill_case(B, Hkv, d, P, T, S, W, r, "bf16", "f32", 24, rope=1e6, outliers=4)
+    assert cache.device_status() == 0
+    kind = oracle.plan_pages(T, P, S, W, npg)
+    refs = [(0, h, j) for h in range(Hkv) for j in range(npg) if kind[j] == oracle.FACTOR]
+    blocks = _export(cache, refs)
+    for (b, h, j), blk in zip(refs, blocks):
+        Lk, Rk, Lv, Rv = _unpack_factor(blk, P, d, r)
+        for L, Rm, X in ((Lk, Rk, K[b, h, j * P:(j + 1) * P]), (Lv, Rv, V[b, h, j * P:(j + 1) * P])):
+            X = X.astype(np.float64)
+            _check_factor(L, Rm, X, r, 1e-4, 1e-4, 1e-5)
+            _, s, _, _ = oracle.svd_rows(X)
+            tail = np.sqrt(np.sum(s[r:] ** 2))
+            assert np.linalg.norm(X - L @ Rm) <= (1 + 1e-4) * tail, (j, np.linalg.norm(X - L @ Rm) / tail)
+
+
+@pytest.mark.parametrize("P", [32, 64])
+def test_prefill_bf16_pages_variable_ranks(P):
+    """bf16 pages on the matrix-core decomposition (two pages per wavefront at
+    P = 32), fp32 factors, per-page ranks including 1 and 32 (full rank at
+    P = 32)."""
+    B, Hkv, d, S, W = 2, 2, 128, P, P
+    T = P * 9 + 5
+    npg = 10
+    rng = np.random.default_rng(7)
+    table = rng.choice([1, 5, 16, 32], size=(B, Hkv, npg))
+    cache, K, V, npg = _prefill_case(B, Hkv, d, P, T, S, W, 0, "bf16", "f32", 24, rank_table=table,
+                                     rope=5e5, outliers=4)
+    assert cache.device_status() == 0
+    kind = oracle.plan_pages(T, P, S, W, npg)
+    refs = [(b, h, j) for b in range(B) for h in range(Hkv) for j in range(npg) if kind[j] == oracle.FACTOR]
+    blocks = _export(cache, refs)
+    R = cache.c.max_rank
+    for (b, h, j), blk in zip(refs, blocks):
+        r = int(table[b, h, j])
+        Lk, Rk, Lv, Rv = _unpack_factor(blk, P, d, R)
+        for L, Rm, X in ((Lk, Rk, K[b, h, j * P:(j + 1) * P]), (Lv, Rv, V[b, h, j * P:(j + 1) * P])):
+            _check_factor(L[:, :r], Rm[:r], X.astype(np.float64), r, 1e-4, 1e-4, 1e-5)
+            assert np.all(L[:, r:] == 0) and np.all(Rm[r:] == 0)
+            if r == P:
+                assert np.abs(L[:, :r] @ Rm[:r] - X).max() <= 1e-5 * np.abs(X).max()
+
+
+def test_rank_deficient_and_zero_pages_bf16():
+    """A zero page and an exactly rank-5 page decomposed at rank 8 (bf16 pages,
+    fp32 factors, P = 64). Directions past the page's rank have no eigenvalue
+    of their own: L is completed to an orthonormal set, the matching rows of R
+    vanish, and L R reproduces the page."""
+    import torch
+    import paper_2608_23843_amd as pk
+    P, d, r = 64, 128, 8
+    rng = np.random.default_rng(11)
+    K = np.zeros((1, 1, 4 * P, d), dtype=np.float32)
+    K[0, 0, P + 3:P + 8] = storage_round(rng.standard_normal((5, d)), "bf16")   # five nonzero rows
+    K[0, 0, 2 * P:3 * P] = storage_round(rng.standard_normal((P, 5)) @ rng.standard_normal((5, d)), "bf16")
+    V = np.zeros_like(K)
+    cache = pk.PuzzleKVCache(1, 1, 1, 1, d, P, 4, r, 0, 0, "bf16", "f32")
+    kt = torch.from_numpy(K).to("cuda", torch.bfloat16).contiguous()
+    vt = torch.from_numpy(V).to("cuda", torch.bfloat16).contiguous()
+    cache.prefill(0, kt, vt, [4 * P], default_rank=(r, r))
+    torch.cuda.synchronize()
+    assert cache.device_status() == 0
+    blocks = _export(cache, [(0, 0, 0), (0, 0, 1), (0, 0, 2)])
+    for j, blk in enumerate(blocks):
+        Lk, Rk, Lv, Rv = _unpack_factor(blk, P, d, r)
+        X = K[0, 0, j * P:(j + 1) * P].astype(np.float64)
+        for L, Rm, Xp in ((Lk, Rk, X), (Lv, Rv, np.zeros_like(X))):
+            assert np.abs(L.T @ L - np.eye(r)).max() <= 1e-5, j
+            if j == 2 and Xp is X:   # bf16 rounding makes this page full rank: a true rank-8 tail
+                _check_factor(L, Rm, Xp, r, 1e-4, 1e-5, 1e-5)
+            else:
+                assert np.abs(L @ Rm - Xp).max() <= 1e-5 * max(np.abs(Xp).max(), 1.0), j
+        if j == 0:
+            assert np.all(Rk == 0) and np.all(Rv == 0)
+        if j == 1:   # the five nonzero rows span the page: ranks 6..8 carry nothing
+            assert np.abs(Rk[5:]).max() <= 1e-5 * np.abs(Rk).max()
