@@ -19,10 +19,10 @@
 //     itself. Row k of R is written to LDS and read by the lane pivoted at
 //     step k, which no longer needs its column of G: no register indexing,
 //     no transposition buffer.
-//  3. One-sided Jacobi on the columns of Pi R^T (xor pairing: step m pairs
-//     lane c with lane c ^ m; the partner column is fetched with ds_swizzle
-//     inside a 32-lane half and with ds_bpermute across halves, the swizzle
-//     being three times cheaper), without accumulating the rotations: at
+//  3. One-sided Jacobi on the columns of Pi R^T (xor pairing inside 32-lane
+//     halves, partner columns fetched with ds_swizzle, which costs a third of
+//     a ds_bpermute; pairs across halves are met by swapping 16-lane rows
+//     between groups of steps), without accumulating the rotations: at
 //     convergence the columns are lambda_c u_c with u_c the eigenvectors, so
 //     L is the normalized columns, orthonormal to the rotation threshold.
 //  4. Ranking and eigenvectors; then R = L^T X with L staged in LDS and
@@ -64,17 +64,6 @@ __device__ __forceinline__ void cq_swz(const float (&a)[P], float (&pa)[P], floa
     p0 = cq_f(__builtin_amdgcn_ds_swizzle(cq_i(s0), pat));
     p1 = cq_f(__builtin_amdgcn_ds_swizzle(cq_i(s1), pat));
     p2 = __builtin_amdgcn_ds_swizzle(s2, pat);
-}
-
-// Partner values for a step that crosses the 32-lane halves (P = 64).
-template <int P>
-__device__ __forceinline__ void cq_bperm(const float (&a)[P], float (&pa)[P], float s0, float &p0, float s1, float &p1,
-                                         int s2, int &p2, int addr) {
-#pragma unroll
-    for (int k = 0; k < P; ++k) pa[k] = cq_f(__builtin_amdgcn_ds_bpermute(addr, cq_i(a[k])));
-    p0 = cq_f(__builtin_amdgcn_ds_bpermute(addr, cq_i(s0)));
-    p1 = cq_f(__builtin_amdgcn_ds_bpermute(addr, cq_i(s1)));
-    p2 = __builtin_amdgcn_ds_bpermute(addr, s2);
 }
 
 // Value of lane `src` (within this lane's P-lane group) of every group.
@@ -237,16 +226,77 @@ __global__ __launch_bounds__(64) void k_compress_qr(Geo g, pkv_page *table, cons
     // Columns are carried as d_c * a~_c: rotating the pair (c, p) is then
     // a~_c += mu a~_p, d_c *= cos, one fma per element. |a_c|^2 is carried
     // along and recomputed with the scales folded back in every sweep.
+    //
+    // Sweep order at P = 64: the xor steps m = 1..31 pair lanes inside each
+    // 32-lane half (ds_swizzle). The pairs across the halves are met by
+    // moving columns instead of fetching across halves: with the 16-lane rows
+    // holding quarters [A B | C D], swapping rows 1 and 2 gives [A C | B D]
+    // and steps m = 16..31 pair A-C and B-D; swapping rows 0 and 2 then gives
+    // [B C | A D] for A-D and B-C. Every pair meets once per sweep, all 63
+    // steps are swizzles, and a row swap costs about one permlane per value.
+    //
+    // Convergence: the iteration stops after a sweep in which the ranking of
+    // the r largest columns did not change and no pair touching them needed a
+    // rotation by more than sqrt(tol) in cosine: Jacobi converges
+    // quadratically, so what such a sweep leaves is below tol.
     constexpr float kTolFactor = std::is_same<TF, uint16_t>::value ? 10.f : 1.f;
     const float tol = kTolFactor * (float)P * 1.1920929e-7f;
+    const float stop_tol = sqrtf(tol);
     const int r_need = ref.which == 0 ? ref.rk : ref.rv;
+    // tag = top flag << 8 | column id: the id travels with the column, so
+    // equal norms (zero columns) are ranked the same way wherever they sit
     float dsc = 1.f, alpha = 0.f;
-    int topi = 1;
+    int tag = (1 << 8) | c, larger = 0;
     int sweeps = 0;
     bool more = true;
+    int rotated = 0;
+    auto step = [&](int m) {
+        float pg[P], beta, dp;
+        int tag_p;
+        switch (m) {
+#define PKV_CQ_CASE(M) \
+    case M: cq_swz<P, M>(gc, pg, alpha, beta, dsc, dp, tag, tag_p); break;
+            PKV_CQ_CASE(1) PKV_CQ_CASE(2) PKV_CQ_CASE(3) PKV_CQ_CASE(4) PKV_CQ_CASE(5) PKV_CQ_CASE(6)
+            PKV_CQ_CASE(7) PKV_CQ_CASE(8) PKV_CQ_CASE(9) PKV_CQ_CASE(10) PKV_CQ_CASE(11) PKV_CQ_CASE(12)
+            PKV_CQ_CASE(13) PKV_CQ_CASE(14) PKV_CQ_CASE(15) PKV_CQ_CASE(16) PKV_CQ_CASE(17) PKV_CQ_CASE(18)
+            PKV_CQ_CASE(19) PKV_CQ_CASE(20) PKV_CQ_CASE(21) PKV_CQ_CASE(22) PKV_CQ_CASE(23) PKV_CQ_CASE(24)
+            PKV_CQ_CASE(25) PKV_CQ_CASE(26) PKV_CQ_CASE(27) PKV_CQ_CASE(28) PKV_CQ_CASE(29) PKV_CQ_CASE(30)
+            default: cq_swz<P, 31>(gc, pg, alpha, beta, dsc, dp, tag, tag_p); break;
+#undef PKV_CQ_CASE
+        }
+        float ga = 0.f, gb = 0.f, gcc = 0.f, gd = 0.f;
+#pragma unroll
+        for (int e = 0; e < P; e += 4) {
+            ga = fmaf(gc[e], pg[e], ga);
+            gb = fmaf(gc[e + 1], pg[e + 1], gb);
+            gcc = fmaf(gc[e + 2], pg[e + 2], gcc);
+            gd = fmaf(gc[e + 3], pg[e + 3], gd);
+        }
+        const float gt = (ga + gb) + (gcc + gd);
+        const int partner = c ^ m;
+        larger += (beta > alpha || (beta == alpha && (tag_p & 255) < (tag & 255))) ? 1 : 0;
+        const float gamma = gt * dsc * dp;
+        const bool lo = c < partner;
+        const float a_lo = lo ? alpha : beta, a_hi = lo ? beta : alpha;
+        const float norm_pair = sqrtf(a_lo * a_hi);
+        const bool rot = a_lo > kCqTiny2 && a_hi > kCqTiny2 && fabsf(gamma) > tol * norm_pair;
+        const float zeta = (a_hi - a_lo) * __builtin_amdgcn_rcpf(2.f * gamma);
+        const float tz = __builtin_copysignf(
+            __builtin_amdgcn_rcpf(fabsf(zeta) + __builtin_amdgcn_sqrtf(fmaf(zeta, zeta, 1.f))), zeta);
+        const float t = rot ? tz : 0.f;
+        const float cs = rot ? __builtin_amdgcn_rsqf(fmaf(t, t, 1.f)) : 1.f;
+        rotated |= (rot && ((tag | tag_p) >> 8) && fabsf(gamma) > stop_tol * norm_pair) ? 1 : 0;
+        const float t_eff = lo ? -t : t;   // the lower column takes -sin
+        const float mu = t_eff * (dp * __builtin_amdgcn_rcpf(dsc));
+#pragma unroll
+        for (int e = 0; e < P; ++e) gc[e] = fmaf(mu, pg[e], gc[e]);
+        const float s_eff = cs * t_eff;
+        alpha = fmaf(cs * cs, alpha, fmaf(2.f * cs * s_eff, gamma, s_eff * s_eff * beta));
+        dsc *= cs;
+    };
     while (more && sweeps < kMaxSweeps) {
         ++sweeps;
-        int larger = 0;
+        larger = 0;
         float aa = 0.f, ab = 0.f;
 #pragma unroll
         for (int e = 0; e < P; e += 2) {
@@ -257,56 +307,46 @@ __global__ __launch_bounds__(64) void k_compress_qr(Geo g, pkv_page *table, cons
         }
         alpha = aa + ab;
         dsc = 1.f;
-        int rotated = 0;
-        for (int m = 1; m < P; ++m) {
-            float pg[P], beta, dp;
-            int top_p;
-            switch (m) {
-#define PKV_CQ_CASE(M) \
-    case M: cq_swz<P, M>(gc, pg, alpha, beta, dsc, dp, topi, top_p); break;
-                PKV_CQ_CASE(1) PKV_CQ_CASE(2) PKV_CQ_CASE(3) PKV_CQ_CASE(4) PKV_CQ_CASE(5) PKV_CQ_CASE(6)
-                PKV_CQ_CASE(7) PKV_CQ_CASE(8) PKV_CQ_CASE(9) PKV_CQ_CASE(10) PKV_CQ_CASE(11) PKV_CQ_CASE(12)
-                PKV_CQ_CASE(13) PKV_CQ_CASE(14) PKV_CQ_CASE(15) PKV_CQ_CASE(16) PKV_CQ_CASE(17) PKV_CQ_CASE(18)
-                PKV_CQ_CASE(19) PKV_CQ_CASE(20) PKV_CQ_CASE(21) PKV_CQ_CASE(22) PKV_CQ_CASE(23) PKV_CQ_CASE(24)
-                PKV_CQ_CASE(25) PKV_CQ_CASE(26) PKV_CQ_CASE(27) PKV_CQ_CASE(28) PKV_CQ_CASE(29) PKV_CQ_CASE(30)
-                PKV_CQ_CASE(31)
-#undef PKV_CQ_CASE
-            default:
-                cq_bperm<P>(gc, pg, alpha, beta, dsc, dp, topi, top_p, (lane ^ m) << 2);
-                break;
-            }
-            float ga = 0.f, gb = 0.f, gcc = 0.f, gd = 0.f;
+        rotated = 0;
+        for (int m = 1; m < 32; ++m) step(m);
+        if constexpr (P == 64) {
+            // rows 1 <-> 2: three permlanes move two values
+            auto swap12 = [](float &x, float &y) {
+                const auto t1 = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(y), false, false);
+                const auto t2 = __builtin_amdgcn_permlane16_swap(t1[0], t1[1], false, false);
+                const auto t3 = __builtin_amdgcn_permlane32_swap(t2[0], t2[1], false, false);
+                x = __uint_as_float(t3[0]);
+                y = __uint_as_float(t3[1]);
+            };
+            // rows 0 <-> 2: one permlane and one select per value
+            const bool keep = ((lane >> 4) & 1) == ((lane >> 5) & 1);   // rows 0 and 3 take the second half-copy
+            auto swap02 = [keep](float &x) {
+                const auto t = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+                x = __uint_as_float(keep ? t[1] : t[0]);
+            };
+            float ti = __int_as_float(tag), li = __int_as_float(larger);
 #pragma unroll
-            for (int e = 0; e < P; e += 4) {
-                ga = fmaf(gc[e], pg[e], ga);
-                gb = fmaf(gc[e + 1], pg[e + 1], gb);
-                gcc = fmaf(gc[e + 2], pg[e + 2], gcc);
-                gd = fmaf(gc[e + 3], pg[e + 3], gd);
-            }
-            const float gt = (ga + gb) + (gcc + gd);
-            const int partner = c ^ m;
-            larger += (beta > alpha || (beta == alpha && partner < c)) ? 1 : 0;
-            const float gamma = gt * dsc * dp;
-            const bool lo = c < partner;
-            const float a_lo = lo ? alpha : beta, a_hi = lo ? beta : alpha;
-            const bool rot = a_lo > kCqTiny2 && a_hi > kCqTiny2 && fabsf(gamma) > tol * sqrtf(a_lo * a_hi);
-            const float zeta = (a_hi - a_lo) * __builtin_amdgcn_rcpf(2.f * gamma);
-            const float tz = __builtin_copysignf(
-                __builtin_amdgcn_rcpf(fabsf(zeta) + __builtin_amdgcn_sqrtf(fmaf(zeta, zeta, 1.f))), zeta);
-            const float t = rot ? tz : 0.f;
-            const float cs = rot ? __builtin_amdgcn_rsqf(fmaf(t, t, 1.f)) : 1.f;
-            rotated |= (rot && (topi || top_p)) ? 1 : 0;
-            const float t_eff = lo ? -t : t;   // the lower column takes -sin
-            const float mu = t_eff * (dp * __builtin_amdgcn_rcpf(dsc));
+            for (int e = 0; e < P; e += 2) swap12(gc[e], gc[e + 1]);
+            swap12(alpha, dsc);
+            swap12(ti, li);
+            tag = __float_as_int(ti);
+            larger = __float_as_int(li);
+            for (int m = 16; m < 32; ++m) step(m);
+            ti = __int_as_float(tag);
+            li = __int_as_float(larger);
 #pragma unroll
-            for (int e = 0; e < P; ++e) gc[e] = fmaf(mu, pg[e], gc[e]);
-            const float s_eff = cs * t_eff;
-            alpha = fmaf(cs * cs, alpha, fmaf(2.f * cs * s_eff, gamma, s_eff * s_eff * beta));
-            dsc *= cs;
+            for (int e = 0; e < P; ++e) swap02(gc[e]);
+            swap02(alpha);
+            swap02(dsc);
+            swap02(ti);
+            swap02(li);
+            tag = __float_as_int(ti);
+            larger = __float_as_int(li);
+            for (int m = 16; m < 32; ++m) step(m);
         }
         const int top_new = larger < r_need ? 1 : 0;
-        more = __any(rotated || top_new != topi);   // converged only on a settled ranking
-        topi = top_new;
+        more = __any(rotated || top_new != (tag >> 8));   // converged only on a settled ranking
+        tag = (top_new << 8) | (tag & 255);
     }
     if (more && active && c == 0) raise_status(PKV_DEV_NO_CONVERGE);
 
