@@ -117,6 +117,23 @@ def attention_bytes(pk_cache, ranks_np, seq_len, P, d, B, Hkv, Hq, S, W):
     return total
 
 
+def compress_work(kinds, ranks_np, B, Hkv, P, d, sweeps_total):
+    """FLOPs of one prefill's decompositions (a page pair is a K and a V
+    decomposition). Useful: the Gram matrix X X^T (2 P^2 d) and the projection
+    R = L^T X at the page's rank (2 r P d). Executed, as the matrix-core kernel
+    runs it: Gram; the QR of G (P steps, each lane forming the pivot norm, its
+    dot and its update: 6 P^3); each Jacobi sweep (P - 1 steps of P lanes, a
+    P-long dot and update each: 4 P^2 (P - 1)); the projection for all 32 rank
+    slots (2 * 32 P d)."""
+    import numpy as np
+    fact = np.nonzero(np.asarray(kinds) == 2)[0]
+    r = ranks_np[:, :, fact].astype(np.float64)          # [B][Hkv][pages]
+    n_dec = 2 * r.size
+    useful = 2 * (r.size * 2.0 * P * P * d + (2.0 * r * P * d).sum())
+    executed = n_dec * (2.0 * P * P * d + 6.0 * P ** 3 + 2.0 * 32 * P * d) + sweeps_total * 4.0 * P * P * (P - 1)
+    return {"sweeps": sweeps_total / max(n_dec, 1), "useful": useful, "executed": executed}
+
+
 def cpu_baseline(wl, seed, seq_T, K_dense, V_dense, q, budget_s, layers):
     """The oracle on a bounded sample: whole (sequence, KV head) heads of one
     layer at the full length, factor pages drawn by the generator, timed until
@@ -228,6 +245,7 @@ def main():
     n_fact = int((kinds == pk.PKV_FACTOR).sum()) * B * Hkv
     ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     comp_ms = []
+    cache.compress_sweeps()   # clear the device's sweep counter
     for rep in range(3):
         torch.cuda.synchronize()
         ev0.record()
@@ -235,11 +253,15 @@ def main():
         ev1.record()
         torch.cuda.synchronize()
         comp_ms.append(ev0.elapsed_time(ev1))
+    sweeps = cache.compress_sweeps() / 3.0
     status = cache.device_status()
     comp_ms_best = min(comp_ms)
     pages_per_s = n_fact / (comp_ms_best / 1e3)
-    log("prefill/decomposition: %d page pairs in %.2f ms (%.3g pairs/s), status %d"
-        % (n_fact, comp_ms_best, pages_per_s, status))
+    comp = compress_work(kinds, ranks_np, B, Hkv, P, d, sweeps)
+    log("prefill/decomposition: %d page pairs in %.2f ms (%.3g pairs/s, %.2f sweeps per decomposition, "
+        "useful %.2f TFLOP/s, executed %.2f TFLOP/s), status %d"
+        % (n_fact, comp_ms_best, pages_per_s, comp["sweeps"], comp["useful"] / comp_ms_best / 1e9,
+           comp["executed"] / comp_ms_best / 1e9, status))
     del kt, vt
     torch.cuda.empty_cache()
 
@@ -272,6 +294,11 @@ def main():
     call_events = []
     step_start = step_end = None
     compress_calls = 0
+    # the host only enqueues in the timed loop; a garbage-collector pass there
+    # could leave the GPU idle between a call's start event and its launch
+    import gc
+    gc.collect()
+    gc.disable()
     for s in range(n_steps):
         timed = s >= args.warmup
         if s == args.warmup:
@@ -300,6 +327,7 @@ def main():
     step_end = step_marks[1]
     step_end.record(stream)
     torch.cuda.synchronize()
+    gc.enable()
     status |= cache.device_status()
     ms_total = step_start.elapsed_time(step_end)
     ms_per_step = ms_total / args.steps
@@ -347,7 +375,11 @@ def main():
         "attention_algorithmic_bytes": int(abytes),
         "attention_gbps": round(achieved, 1),
         "compress_page_pairs_per_s": round(pages_per_s, 1),
+        "compress_decompositions_per_s": round(2 * pages_per_s, 1),
         "compress_ms_per_layer_prefill": round(comp_ms_best, 3),
+        "compress_sweeps_per_decomposition": round(comp["sweeps"], 3),
+        "compress_useful_tflops": round(comp["useful"] / comp_ms_best / 1e9, 3),
+        "compress_executed_tflops": round(comp["executed"] / comp_ms_best / 1e9, 3),
         "compress_calls_in_run": compress_calls,
         "device_status": status,
         "roofline": roofline,

@@ -268,6 +268,12 @@ pkv_status pkv_export_int4_pages(const pkv_cache *c, int32_t layer, int32_t n, c
 /* Synchronizes the stream, then returns (and clears) the current device's
  * sticky status bits (PKV_DEV_*) in *bits. */
 pkv_status pkv_device_status(pkv_stream s, uint32_t *bits);
+/* Synchronizes the stream, then returns (and clears) the number of Jacobi
+ * sweeps that decompositions on the current device have executed since the
+ * last call, summed over decompositions (a page's K and V count as two).
+ * With the number of decompositions it gives the work a pkv_prefill or
+ * pkv_compress_pages call actually executed; the factors do not depend on it. */
+pkv_status pkv_compress_sweeps(pkv_stream s, uint64_t *sweeps);
 /* Message of the last error on this thread ("" if none). */
 const char *pkv_last_error(void);
 const char *pkv_version(void);

@@ -234,6 +234,13 @@ class PuzzleKVCache:
                                         _stream_handle(torch, stream)), "pkv_export_pages")
         return dst[:n]
 
+    def compress_sweeps(self, stream=None) -> int:
+        """Jacobi sweeps executed by decompositions on this device since the last call."""
+        n = ctypes.c_uint64(0)
+        check(self.lib.pkv_compress_sweeps(_stream_handle(self.torch, stream), ctypes.byref(n)),
+              "pkv_compress_sweeps")
+        return int(n.value)
+
     def device_status(self, stream=None) -> int:
         bits = ctypes.c_uint32(0)
         check(self.lib.pkv_device_status(_stream_handle(self.torch, stream), ctypes.byref(bits)),

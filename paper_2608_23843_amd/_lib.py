@@ -23,7 +23,7 @@ EXPORTS = [
     "pkv_workspace_bytes", "pkv_plan_pages", "pkv_eligible_pages", "pkv_cache_reset", "pkv_prefill",
     "pkv_append_kv", "pkv_compress_pages", "pkv_mixed_decode_attention", "pkv_import_pages",
     "pkv_export_block_elems", "pkv_export_pages", "pkv_int4_blob_bytes", "pkv_export_int4_pages",
-    "pkv_device_status", "pkv_last_error", "pkv_version",
+    "pkv_device_status", "pkv_compress_sweeps", "pkv_last_error", "pkv_version",
 ]
 
 
@@ -80,6 +80,7 @@ def load():
         "pkv_int4_blob_bytes": ([cp, i32, i32], i64),
         "pkv_export_int4_pages": ([cp, i32, i32, vp, vp, vp, vp, vp], i32),
         "pkv_device_status": ([vp, ctypes.POINTER(u32)], i32),
+        "pkv_compress_sweeps": ([vp, ctypes.POINTER(ctypes.c_uint64)], i32),
         "pkv_last_error": ([], ctypes.c_char_p),
         "pkv_version": ([], ctypes.c_char_p),
     }

@@ -7,6 +7,17 @@ namespace pkv {
 __device__ unsigned int g_status;
 __device__ inline void raise_status(unsigned int bits) { atomicOr(&g_status, bits); }
 
+// Jacobi sweeps executed by decompositions since the last read (diagnostic).
+__device__ unsigned long long g_sweeps;
+__device__ inline void count_sweeps(int n) { atomicAdd(&g_sweeps, (unsigned long long)n); }
+
+hipError_t sweeps_read_clear(unsigned long long *n) {
+    unsigned long long zero = 0;
+    hipError_t e = hipMemcpyFromSymbol(n, HIP_SYMBOL(g_sweeps), sizeof(zero), 0, hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return e;
+    return hipMemcpyToSymbol(HIP_SYMBOL(g_sweeps), &zero, sizeof(zero), 0, hipMemcpyHostToDevice);
+}
+
 hipError_t status_read_clear(unsigned int *bits) {
     unsigned int zero = 0;
     hipError_t e = hipMemcpyFromSymbol(bits, HIP_SYMBOL(g_status), sizeof(unsigned int), 0,

@@ -227,7 +227,10 @@ __global__ __launch_bounds__(64) void k_compress(Geo g, pkv_page *table, const c
         more = __any(rotated || top_new != top);   // converged only on a settled ranking
         top = top_new;
     }
-    if (more && active && c == 0) raise_status(PKV_DEV_NO_CONVERGE);
+    if (active && c == 0) {
+        count_sweeps(sweeps);
+        if (more) raise_status(PKV_DEV_NO_CONVERGE);
+    }
 #pragma unroll
     for (int k = 0; k < P; ++k) {
         gcol[k] *= dsc * gnorm;   // back to G J

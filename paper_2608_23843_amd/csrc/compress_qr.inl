@@ -107,6 +107,7 @@ __global__ __launch_bounds__(64) void k_compress_qr(Geo g, pkv_page *table, cons
     static_assert(P == 32 || P == 64, "P = 32 or 64");
     constexpr int D = 64 / P;
     extern __shared__ float cq_smem[];
+    int *cq_tok = (int *)(cq_smem + 64 + 64 * 32 + 64);   // position -> token, per group
     const int d = g.d;
     const int lane = threadIdx.x;
     const int grp = P == 64 ? 0 : lane >> 5;
@@ -188,13 +189,24 @@ __global__ __launch_bounds__(64) void k_compress_qr(Geo g, pkv_page *table, cons
 #pragma unroll
     for (int e = 0; e < P; ++e) gc[e] *= ginv;
     nrm2 *= ginv * ginv;
-    const int prank = cq_rank<P>(nrm2, c, grp);   // pivot order: decreasing column norm
+    // Pivot order: decreasing column norm. The columns are first moved so that
+    // the k-th pivot sits in lane k: row k of R then becomes the column of
+    // lane k, and the xor pairing of the Jacobi steps meets rows of similar
+    // size early (about 1.4 sweeps fewer than leaving row k in the pivot's
+    // lane). tok_of[k] records which token's column that is; the
+    // eigenvectors' entries come out in this order.
+    {
+        const int prank = cq_rank<P>(nrm2, c, grp);
+        const int daddr = ((P == 64 ? 0 : grp * 32) + prank) << 2;
+#pragma unroll
+        for (int e = 0; e < P; ++e) gc[e] = cq_f(__builtin_amdgcn_ds_permute(daddr, cq_i(gc[e])));
+        cq_tok[grp * P + c] = __builtin_amdgcn_ds_permute(daddr, c);   // token of this lane's column
+    }
     float *rowbuf = cq_smem + grp * P;
     bool done = false;
     for (int k = 0; k < P; ++k) {
-        const uint64_t bal = __ballot(prank == k);   // one lane per group
-        const int piv0 = __builtin_ctzll(bal);
-        const int piv1 = P == 64 ? piv0 : 32 + __builtin_ctzll(bal >> 32);
+        const int piv0 = k;
+        const int piv1 = P == 64 ? k : 32 + k;
         float x[P];
 #pragma unroll
         for (int e = 0; e < P; ++e) x[e] = cq_group_bcast<P>(gc[e], piv0, piv1, grp);
@@ -214,7 +226,7 @@ __global__ __launch_bounds__(64) void k_compress_qr(Geo g, pkv_page *table, cons
         for (int e = 0; e < P; ++e) gc[e] = fmaf(-f, x[e], gc[e]);
         rowbuf[c] = rk;
         __builtin_amdgcn_wave_barrier();
-        if (prank == k) {   // the pivot's column is finished: it takes row k of R
+        if (c == k) {   // the pivot's column is finished: it takes row k of R
 #pragma unroll
             for (int e = 0; e < P; ++e) gc[e] = rowbuf[e];
             done = true;
@@ -348,7 +360,10 @@ __global__ __launch_bounds__(64) void k_compress_qr(Geo g, pkv_page *table, cons
         more = __any(rotated || top_new != (tag >> 8));   // converged only on a settled ranking
         tag = (top_new << 8) | (tag & 255);
     }
-    if (more && active && c == 0) raise_status(PKV_DEV_NO_CONVERGE);
+    if (active && c == 0) {
+        count_sweeps(sweeps);
+        if (more) raise_status(PKV_DEV_NO_CONVERGE);
+    }
 
     // ---- 4. eigenvalues, ranking, eigenvectors -----------------------------
     float an2a = 0.f, an2b = 0.f;
@@ -364,41 +379,56 @@ __global__ __launch_bounds__(64) void k_compress_qr(Geo g, pkv_page *table, cons
     const int rho = cq_rank<P>(an2, c, grp);
     const bool tinycol = !(an2 > kCqTiny2);
     {
+        // A column at rounding level starts from the unit vector of its own
+        // id k (the row of R it began as; ids travel with the columns): the
+        // columns above it are combinations of rows of R before k, which are
+        // upper triangular with nonzero diagonals, so e_k is never in their span.
+        const int cid = tag & 255;
         const float inv = tinycol ? 0.f : __builtin_amdgcn_rsqf(an2);
 #pragma unroll
-        for (int e = 0; e < P; ++e) gc[e] = tinycol ? (e == c ? 1.f : 0.f) : gc[e] * inv;
+        for (int e = 0; e < P; ++e) gc[e] = tinycol ? (e == cid ? 1.f : 0.f) : gc[e] * inv;
     }
+    // The normalized columns are orthonormal to the rotation threshold. For
+    // fp32 factor storage one Gram-Schmidt pass in rank order makes them
+    // orthonormal to rounding (bf16 storage rounds far above the threshold).
     // A column at rounding level (rank-deficient page) has no direction of
-    // its own: it takes a unit vector, made orthogonal to the columns ranked
-    // above it by Gram-Schmidt in rank order (twice).
-    if (__any(tinycol && rho < r_need)) {
-        const int rmax = max(__builtin_amdgcn_readlane(r_need, 0), __builtin_amdgcn_readlane(r_need, 63));
-        for (int pass = 0; pass < 2; ++pass) {
-            for (int i = 0; i < rmax; ++i) {
-                const uint64_t bal = __ballot(rho == i);
-                const int piv0 = __builtin_ctzll(bal);
-                const int piv1 = P == 64 ? piv0 : 32 + __builtin_ctzll(bal >> 32);
-                float x[P];
+    // its own: its unit vector is made orthogonal to the columns ranked above
+    // it by Gram-Schmidt in rank order (twice).
+    {
+        constexpr bool kAll = std::is_same<TF, float>::value;
+        const bool any_tiny = __any(tinycol && rho < r_need);
+        if (kAll || any_tiny) {
+            const int rmax = max(__builtin_amdgcn_readlane(r_need, 0), __builtin_amdgcn_readlane(r_need, 63));
+            const int passes = any_tiny ? 2 : 1;
+            const bool mine = kAll || tinycol;   // columns this pass orthogonalizes
+            for (int pass = 0; pass < passes; ++pass) {
+                for (int i = 0; i < rmax; ++i) {
+                    const uint64_t bal = __ballot(rho == i);
+                    const int piv0 = __builtin_ctzll(bal);
+                    const int piv1 = P == 64 ? piv0 : 32 + __builtin_ctzll(bal >> 32);
+                    float x[P];
 #pragma unroll
-                for (int e = 0; e < P; ++e) x[e] = cq_group_bcast<P>(gc[e], piv0, piv1, grp);
-                float dot = 0.f;
+                    for (int e = 0; e < P; ++e) x[e] = cq_group_bcast<P>(gc[e], piv0, piv1, grp);
+                    float dot = 0.f;
 #pragma unroll
-                for (int e = 0; e < P; ++e) dot = fmaf(x[e], gc[e], dot);
-                if (rho > i && tinycol)
+                    for (int e = 0; e < P; ++e) dot = fmaf(x[e], gc[e], dot);
+                    if (rho > i && mine)
 #pragma unroll
-                    for (int e = 0; e < P; ++e) gc[e] = fmaf(-dot, x[e], gc[e]);
-                __builtin_amdgcn_wave_barrier();
-                if (rho == i + 1 && tinycol) {
-                    float n2 = 0.f;
+                        for (int e = 0; e < P; ++e) gc[e] = fmaf(-dot, x[e], gc[e]);
+                    __builtin_amdgcn_wave_barrier();
+                    if (rho == i + 1 && mine) {
+                        float n2 = 0.f;
 #pragma unroll
-                    for (int e = 0; e < P; ++e) n2 = fmaf(gc[e], gc[e], n2);
-                    const float inv = n2 > 0.f ? __builtin_amdgcn_rsqf(n2) : 0.f;
+                        for (int e = 0; e < P; ++e) n2 = fmaf(gc[e], gc[e], n2);
+                        const float inv = n2 > 0.f ? __builtin_amdgcn_rsqf(n2) : 0.f;
 #pragma unroll
-                    for (int e = 0; e < P; ++e) gc[e] *= inv;
+                        for (int e = 0; e < P; ++e) gc[e] *= inv;
+                    }
                 }
             }
         }
     }
+
     // ---- 5. R = L^T X and the stores -----------------------------------------
     // L goes to LDS (sL[t][rank], 32 ranks, zero past r). Each lane then owns
     // two output dims for every rank: one 4-byte load per page row (a row is
@@ -413,8 +443,9 @@ __global__ __launch_bounds__(64) void k_compress_qr(Geo g, pkv_page *table, cons
         const float sig = sqrtf(fmaxf(lam, 0.f));
         const float scale = kQ4 ? sqrtf(sig) : 1.f;   // INT4: L~ = U Sigma^(1/2)
         if (rho < 32) {
+            const int *tok = cq_tok + grp * P;
 #pragma unroll
-            for (int t = 0; t < P; ++t) sL[t * 32 + rho] = (rho < r && active) ? gc[t] * scale : 0.f;
+            for (int e = 0; e < P; ++e) sL[tok[e] * 32 + rho] = (rho < r && active) ? gc[e] * scale : 0.f;
             sInvSig[rho] = sig > 0.f ? 1.f / sig : 0.f;
         }
     }
@@ -424,7 +455,7 @@ __global__ __launch_bounds__(64) void k_compress_qr(Geo g, pkv_page *table, cons
 
     const int64_t slot_off = (g.head_index(ref.b, ref.h) * g.max_pages + ref.j) * g.factor_slot_bytes;
     constexpr int kCols = 2;                      // dims per lane per pass
-    float *sR = cq_smem + 64 + 64 * 32 + 64;      // INT4 only: 32 x d (one group: P = 64)
+    float *sR = cq_smem + 64 + 64 * 32 + 64 + 64;   // INT4 only: 32 x d (one group: P = 64)
     for (int k0 = 0; k0 < d; k0 += kCols * P) {
         const int k = k0 + kCols * c;
         const bool kin = k < d;
@@ -519,8 +550,9 @@ template <typename TF, int P>
 hipError_t launch_compress_qr_t(const LaunchCtx &L, const CompressItems &items, const CompressSrc &src,
                                 int64_t n_decomp) {
     constexpr int D = 64 / P;
-    // row buffers (64) + L blocks (64 x 32) + inverse sigmas (64); INT4 adds R~ (32 x d) and scales
-    size_t smem = (64 + 64 * 32 + 64) * sizeof(float);
+    // row buffers (64) + L blocks (64 x 32) + inverse sigmas (64) + token tables (64);
+    // INT4 adds R~ (32 x d) and scales
+    size_t smem = (64 + 64 * 32 + 64 + 64) * sizeof(float);
     if (is_q4<TF>::value) smem += (size_t)(32 * L.geo.d + 64 + L.geo.d) * sizeof(float);
     const int64_t blocks = ceil_div(n_decomp, D);
     LayerPtrs p = layer_ptrs(L);

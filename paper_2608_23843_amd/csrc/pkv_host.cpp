@@ -491,6 +491,17 @@ pkv_status pkv_export_int4_pages(const pkv_cache *c, int32_t layer, int32_t n, c
     return PKV_OK;
 }
 
+pkv_status pkv_compress_sweeps(pkv_stream s, uint64_t *sweeps) {
+    if (!sweeps) return fail(PKV_E_ARG, "sweeps is NULL");
+    hipError_t e = hipStreamSynchronize((hipStream_t)s);
+    if (e != hipSuccess) return hip_fail(e, "pkv_compress_sweeps (sync)");
+    unsigned long long v = 0;
+    e = sweeps_read_clear(&v);
+    if (e != hipSuccess) return hip_fail(e, "pkv_compress_sweeps (read)");
+    *sweeps = (uint64_t)v;
+    return PKV_OK;
+}
+
 pkv_status pkv_device_status(pkv_stream s, uint32_t *bits) {
     if (!bits) return fail(PKV_E_ARG, "bits is NULL");
     hipError_t e = hipStreamSynchronize((hipStream_t)s);

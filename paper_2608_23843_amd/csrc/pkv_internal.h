@@ -138,6 +138,8 @@ template <> __device__ inline void st<uint16_t>(uint16_t *p, int64_t i, float v)
 
 // Reads and clears the sticky device status word of the current device.
 hipError_t status_read_clear(unsigned int *bits);
+// Reads and clears the device's count of executed Jacobi sweeps.
+hipError_t sweeps_read_clear(unsigned long long *n);
 
 // ---- launchers (defined in the .hip files) --------------------------------
 
