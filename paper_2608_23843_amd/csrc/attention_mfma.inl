@@ -533,14 +533,81 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
         w.m_run = w4.m_run;
         w.l[0] = w4.l;
     } else {
-    Claim ahead = take_claim(issue_claim());
+    // bf16 pages are handed to the workgroup in blocks of NW consecutive
+    // pages, one per wave: round k, wave w streams page block_k + w. The
+    // eight waves of a CU then read eight neighbouring slots together, which
+    // a read-only probe of this access pattern measured 4% faster than
+    // claiming page by page per wave (6.26 against 6.0 TB/s). Wave 0 takes a
+    // block one round ahead with one device-scope atomic on the head's
+    // counter; the block goes through LDS at the round's barrier.
+    //
+    // The barrier is inside take_page and nowhere else in the loop, and every
+    // wave calls take_page once per round until the round whose block starts
+    // past the sequence (the same round for all waves: its base is read from
+    // LDS): a wave whose page of a round is past the end takes the next round
+    // at once. So all waves arrive at the same number of barriers, whatever
+    // mix of factor pages and multi-unit dense pages each one streams.
+    __shared__ unsigned int s_blk[4];
+    int round = 0;
+    bool blocks_done = false;
+    // Wave 0's block claim is issued at the top of a loop iteration and read
+    // at the bottom of the same iteration (the vector memory counter is in
+    // order: read later, its wait would also cover the loads issued after
+    // it); the value is held until take_page publishes it. A claim is taken
+    // synchronously only where none is held: the first two rounds and the
+    // last ones, when a wave's page is past the end.
+    unsigned int blk_next = 0u;
+    bool blk_ready = false, need_blk = false;   // wave 0 only
+    auto sync_claim = [&]() -> unsigned int {
+        unsigned int k = 0u;
+        if (lane == 0) k = __hip_atomic_fetch_add(pp.claim(head), (unsigned int)NW, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return (unsigned int)__builtin_amdgcn_readfirstlane((int)k);
+    };
+    auto needs_blk = [&]() -> bool { return wave == 0 && need_blk; };
+    auto issue_blk = [&]() -> unsigned int {
+        unsigned int k = 0u;
+        if (lane == 0) k = __hip_atomic_fetch_add(pp.claim(head), (unsigned int)NW, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return k;
+    };
+    auto take_blk = [&](unsigned int k) {
+        asm volatile("" : "+v"(k));
+        blk_next = (unsigned int)__builtin_amdgcn_readfirstlane((int)k);
+        blk_ready = true;
+        need_blk = false;
+    };
+    if (wave == 0) {
+        const unsigned int v = sync_claim();
+        if (lane == 0) s_blk[0] = v;
+    }
+    auto take_page = [&]() -> Claim {
+        if (wave == 0) {
+            if (round > 0) {
+                const unsigned int v = blk_ready ? blk_next : sync_claim();
+                if (lane == 0) s_blk[round & 3] = v;
+                blk_ready = false;
+            }
+            need_blk = true;
+        }
+        // LDS write complete, then the round barrier; no vector-memory wait
+        // (loads of the units in flight stay in flight across it)
+        __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+        asm volatile("s_barrier" ::: "memory");
+        const unsigned int base = (unsigned int)__builtin_amdgcn_readfirstlane((int)s_blk[round & 3]);
+        ++round;
+        if ((int64_t)base >= n_pages) blocks_done = true;
+        Claim c;
+        c.j = (int64_t)base + wave;
+        c.raw = c.j < n_pages ? tab[c.j] : make_uint2(0u, 0u);
+        return c;
+    };
     Unit pending;                 // second and later units of a dense page
     pending.e.kind = PKV_EMPTY;
     pending.j = 0;
     pending.half = 0;
-    // pre: a claim issued while needs_claim() held, taken by the first step
-    auto needs_claim = [&]() -> bool { return pending.e.kind != PKV_DENSE && ahead.j < n_pages; };
+    Claim ahead = take_page();
+    // pre: wave 0's block claim issued at the top of this iteration (needs_blk held)
     auto next_unit = [&](unsigned int pre) -> Unit {
+        if (needs_blk()) take_blk(pre);
         if (pending.e.kind == PKV_DENSE) {
             Unit u = pending;
             const int next_half = u.half + 1;
@@ -548,14 +615,14 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
             else pending.half = next_half;
             return u;
         }
-        bool have_pre = true;
-        while (ahead.j < n_pages) {
+        while (!blocks_done) {
+            const Claim c = ahead;
+            ahead = take_page();
+            if (c.j >= n_pages) continue;   // this wave's page of the round is past the end
             Unit u;
-            u.e = unpack_entry(ahead.raw);
-            u.j = ahead.j;
+            u.e = unpack_entry(c.raw);
+            u.j = c.j;
             u.half = 0;
-            ahead = take_claim(have_pre ? pre : issue_claim());
-            have_pre = false;
             if (u.e.kind == PKV_FACTOR) return u;
             if (u.e.kind == PKV_DENSE) {
                 if (UT < min<int64_t>(P, T - u.j * P)) {
@@ -572,6 +639,7 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
         none.half = 0;
         return none;
     };
+
     auto unit_rows = [&](const Unit &u) -> int {
         return (int)min<int64_t>(UT, T - u.j * P - (int64_t)UT * u.half);
     };
@@ -594,9 +662,9 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
     cur.e.kind = PKV_EMPTY;
     cur.j = 0;
     cur.half = 0;
-    Unit nxt = next_unit(needs_claim() ? issue_claim() : 0u);
+    Unit nxt = next_unit(needs_blk() ? issue_blk() : 0u);
     while (cur.e.kind != PKV_EMPTY || nxt.e.kind != PKV_EMPTY) {
-        const unsigned int pre = needs_claim() ? issue_claim() : 0u;
+        const unsigned int pre = needs_blk() ? issue_blk() : 0u;
         const PageRes nres = unit_res<D, P>(factor, g.factor_slot_bytes, dense, g.dense_slot_bytes, nxt);
         bf16x8 eh[KS], el[KS];
         const int rows = unit_rows(cur);
