@@ -91,7 +91,7 @@ def parse():
     return ap.parse_args()
 
 
-def attention_bytes(pk_cache, ranks_np, seq_len, P, d, B, Hkv, Hq, S, W):
+def attention_bytes(pk_cache, ranks_np, ranks_v_np, seq_len, P, d, B, Hkv, Hq, S, W):
     """Algorithmic bytes one attention launch must move: every stored byte of
     every page it reads (factor pairs at their ranks, dense pages up to the
     sequence length), the page-table entries, the queries, out and lse."""
@@ -105,9 +105,9 @@ def attention_bytes(pk_cache, ranks_np, seq_len, P, d, B, Hkv, Hq, S, W):
         for h in range(Hkv):
             for j in range(n):
                 if sink_pages <= j <= jmax:
-                    r = int(ranks_np[b, h, j])
+                    r = (int(ranks_np[b, h, j]), int(ranks_v_np[b, h, j]))
                     if r not in fpb:
-                        fpb[r] = pk_cache.factor_page_bytes(r, r)
+                        fpb[r] = pk_cache.factor_page_bytes(*r)
                     total += fpb[r]
                 else:
                     rows = min(P, T - j * P)
@@ -117,7 +117,7 @@ def attention_bytes(pk_cache, ranks_np, seq_len, P, d, B, Hkv, Hq, S, W):
     return total
 
 
-def compress_work(kinds, ranks_np, B, Hkv, P, d, sweeps_total):
+def compress_work(kinds, ranks_np, ranks_v_np, B, Hkv, P, d, sweeps_total):
     """FLOPs of one prefill's decompositions (a page pair is a K and a V
     decomposition). Useful: the Gram matrix X X^T (2 P^2 d) and the projection
     R = L^T X at the page's rank (2 r P d). Executed, as the matrix-core kernel
@@ -128,8 +128,9 @@ def compress_work(kinds, ranks_np, B, Hkv, P, d, sweeps_total):
     import numpy as np
     fact = np.nonzero(np.asarray(kinds) == 2)[0]
     r = ranks_np[:, :, fact].astype(np.float64)          # [B][Hkv][pages]
+    rv = ranks_v_np[:, :, fact].astype(np.float64)
     n_dec = 2 * r.size
-    useful = 2 * (r.size * 2.0 * P * P * d + (2.0 * r * P * d).sum())
+    useful = 2 * r.size * 2.0 * P * P * d + (2.0 * r * P * d).sum() + (2.0 * rv * P * d).sum()
     executed = n_dec * (2.0 * P * P * d + 6.0 * P ** 3 + 2.0 * 32 * P * d) + sweeps_total * 4.0 * P * P * (P - 1)
     return {"sweeps": sweeps_total / max(n_dec, 1), "useful": useful, "executed": executed}
 
@@ -146,6 +147,7 @@ def cpu_baseline(wl, seed, seq_T, K_dense, V_dense, q, budget_s, layers):
     int4 = wl.factors == "int4"
     kinds = oracle.plan_pages(seq_T, P, wl.sink, wl.window)
     ranks = synth.page_ranks(wl, seed, 0, len(kinds))
+    ranks_v = synth.page_ranks(wl, seed, 0, len(kinds), "v")
     times, heads = [], []
     for b in range(wl.batch):
         for h in range(wl.kv_heads):
@@ -153,8 +155,8 @@ def cpu_baseline(wl, seed, seq_T, K_dense, V_dense, q, budget_s, layers):
             encoded = {}
             for j, kd in enumerate(kinds):
                 if kd == oracle.FACTOR:
-                    r = int(ranks[b, h, j])
-                    Lk, Rk, Lv, Rv = synth.factor_page(wl, seed, 0, b, h, j, r, r)
+                    Lk, Rk, Lv, Rv = synth.factor_page(wl, seed, 0, b, h, j, int(ranks[b, h, j]),
+                                                       int(ranks_v[b, h, j]))
                     if int4:
                         encoded[j] = [q4.encode_page(w, L, R, np.linalg.norm(R, axis=1))
                                       for w, L, R in (("K", Lk, Rk), ("V", Lv, Rv))]
@@ -217,7 +219,7 @@ def main():
     S, W = wl.sink, wl.window
     n_steps = args.warmup + args.steps
     max_pages = -(-(T + n_steps + 1) // P) + 1
-    max_rank = max(wl.ranks)
+    max_rank = max(wl.ranks + wl.ranks_v)
     log("workload %s: B=%d Hq=%d Hkv=%d d=%d P=%d T=%d layers=%d" % (wl.name, B, Hq, Hkv, d, P, T, layers))
 
     # ---- inputs ----------------------------------------------------------------
@@ -235,7 +237,9 @@ def main():
     vt = torch.from_numpy(V).to("cuda", bf)
     del V
     ranks_np = synth.page_ranks(wl, args.seed, 0, max_pages)
+    ranks_v_np = synth.page_ranks(wl, args.seed, 0, max_pages, "v")
     ranks = torch.from_numpy(ranks_np).cuda().contiguous()
+    ranks_v = torch.from_numpy(ranks_v_np).cuda().contiguous()
 
     cache = pk.PuzzleKVCache(layers, B, Hkv, Hq, d, P, max_pages, max_rank, S, W, wl.dtype, wl.factors)
     log("cache: factor pool %.1f GB, dense pool %.2f GB" % (cache.factor_pool.numel() / 1e9,
@@ -249,7 +253,7 @@ def main():
     for rep in range(3):
         torch.cuda.synchronize()
         ev0.record()
-        cache.prefill(0, kt, vt, [T] * B, rank_k=ranks, rank_v=ranks)
+        cache.prefill(0, kt, vt, [T] * B, rank_k=ranks, rank_v=ranks_v)
         ev1.record()
         torch.cuda.synchronize()
         comp_ms.append(ev0.elapsed_time(ev1))
@@ -257,7 +261,7 @@ def main():
     status = cache.device_status()
     comp_ms_best = min(comp_ms)
     pages_per_s = n_fact / (comp_ms_best / 1e3)
-    comp = compress_work(kinds, ranks_np, B, Hkv, P, d, sweeps)
+    comp = compress_work(kinds, ranks_np, ranks_v_np, B, Hkv, P, d, sweeps)
     log("prefill/decomposition: %d page pairs in %.2f ms (%.3g pairs/s, %.2f sweeps per decomposition, "
         "useful %.2f TFLOP/s, executed %.2f TFLOP/s), status %d"
         % (n_fact, comp_ms_best, pages_per_s, comp["sweeps"], comp["useful"] / comp_ms_best / 1e9,
@@ -312,7 +316,8 @@ def main():
             if len(new_pages):
                 bb, hh, jj = zip(*[(b, h, int(j)) for b in range(B) for h in range(Hkv) for j in new_pages])
                 rr = [int(ranks_np[b, h, j]) for b, h, j in zip(bb, hh, jj)]
-                cache.compress_pages(layer, bb, hh, jj, rr, rr)
+                rv = [int(ranks_v_np[b, h, j]) for b, h, j in zip(bb, hh, jj)]
+                cache.compress_pages(layer, bb, hh, jj, rr, rv)
                 compress_calls += 1
             if timed:
                 e0, e1 = pool[len(call_events)]
@@ -342,7 +347,7 @@ def main():
         raise RuntimeError("non-finite attention output")
 
     mid_T = T + args.warmup + args.steps // 2 + 1
-    abytes = attention_bytes(cache, ranks_np, [mid_T] * B, P, d, B, Hkv, Hq, S, W)
+    abytes = attention_bytes(cache, ranks_np, ranks_v_np, [mid_T] * B, P, d, B, Hkv, Hq, S, W)
     achieved = abytes / (attn_us * 1e-6) / 1e9
     traffic = measured_traffic(wl.name)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
@@ -351,6 +356,8 @@ def main():
 
     metrics = {
         "qwen32b_128k": "mixed-page decode attention time per decode step (64 layers, Qwen3-32B heads, 128K context)",
+        "qwen8b_paper_default": "mixed-page decode attention time per decode step (36 layers, Qwen3-8B heads, "
+                                "16K context, pages of 32 tokens, (r_K, r_V) = (16, 14))",
         "qwen32b_int4": "mixed-page decode attention time per decode step (INT4 factor pages, Qwen3-32B heads, "
                         "128K context, batch 8)",
     }
@@ -368,7 +375,7 @@ def main():
         "dtype": "bf16" if wl.factors == "bf16" else "int4 factors, fp16/bf16 MFMA, fp32 accumulate",
         "data": "synthetic",
         "config": {"workload": wl.name, "batch": B, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d,
-                   "page": P, "tokens": T, "sink": S, "window": W, "ranks": list(wl.ranks),
+                   "page": P, "tokens": T, "sink": S, "window": W, "ranks": list(wl.ranks), "ranks_v": list(wl.ranks_v or wl.ranks),
                    "factor_storage": wl.factors,
                    "layers": layers, "step": "append + planner + compress-when-eligible + attention per layer"},
         "attention_us_per_layer": round(attn_us, 2),

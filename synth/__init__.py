@@ -50,6 +50,7 @@ class Workload:
     layers: int = 1
     decode_steps: int = 0
     factor_dtype: str = ""  # storage of factor pages when it differs from dtype ("int4")
+    ranks_v: tuple = ()     # rank choices of the value factors when they differ from the keys''' 
 
     @property
     def factors(self) -> str:
@@ -73,6 +74,12 @@ WORKLOADS = {
     # Incremental decode: Llama-3-8B heads, batch 32, prefill 16K then 512 steps, r=24.
     "llama8b_incremental": Workload("llama8b_incremental", 4, 32, 8, 32, 128, 64, 16384, 64,
                                     256, 24, (24,), "bf16", 5.0e5, 4, decode_steps=512),
+    # The paper's default configuration on Qwen3-8B heads (32 q / 8 kv, d=128,
+    # 36 layers): pages of 32 tokens, (r_K, r_V) = (16, 14), a 32-token sink
+    # and a dense region of the last completed page plus the partial page
+    # (W = P), 16K context, batch 1.
+    "qwen8b_paper_default": Workload("qwen8b_paper_default", 6, 1, 8, 32, 128, 32, 16384, 32, 32, 24,
+                                     (16,), "bf16", 1.0e6, 4, layers=36, ranks_v=(14,)),
     # INT4 factors: Qwen3-32B heads, batch 8, T=128K.
     "qwen32b_int4": Workload("qwen32b_int4", 5, 8, 8, 64, 128, 64, 131072, 64, 512, 24,
                              (16, 24, 32), "bf16", 1.0e6, 4, factor_dtype="int4"),
@@ -197,10 +204,15 @@ def queries(wl: Workload, seed: int, step: int = 0) -> np.ndarray:
     return round_storage(out, wl.dtype)
 
 
-def page_ranks(wl: Workload, seed: int, layer: int, n_pages: int) -> np.ndarray:
+def page_ranks(wl: Workload, seed: int, layer: int, n_pages: int, which: str = "k") -> np.ndarray:
     """Rank of every logical page, (batch, kv_heads, n_pages) uint8; uniform over
-    wl.ranks when it holds several choices."""
+    wl.ranks when it holds several choices. which="v" gives the value ranks,
+    which are the key ranks unless the workload sets ranks_v."""
     out = np.empty((wl.batch, wl.kv_heads, n_pages), dtype=np.uint8)
+    if which == "v" and wl.ranks_v:
+        assert len(wl.ranks_v) == 1, "value ranks: one fixed choice"
+        out[:] = wl.ranks_v[0]
+        return out
     choices = np.asarray(wl.ranks, dtype=np.uint8)
     for b in range(wl.batch):
         for h in range(wl.kv_heads):

@@ -34,15 +34,18 @@ def _build(name):
     max_pages = -(-T // P)
     K, V = synth.kv_layer(wl, 0, 0, T, workers=16)
     ranks = synth.page_ranks(wl, 0, 0, max_pages)
-    cache = pk.PuzzleKVCache(1, B, Hkv, Hq, d, P, max_pages, max(wl.ranks), S, W, wl.dtype, wl.factors)
+    ranks_v = synth.page_ranks(wl, 0, 0, max_pages, "v")
+    cache = pk.PuzzleKVCache(1, B, Hkv, Hq, d, P, max_pages, max(wl.ranks + wl.ranks_v), S, W, wl.dtype,
+                             wl.factors)
     kt = torch.from_numpy(K).to("cuda", torch.bfloat16)
     vt = torch.from_numpy(V).to("cuda", torch.bfloat16)
     rt = torch.from_numpy(ranks).cuda().contiguous()
-    cache.prefill(0, kt, vt, [T] * B, rank_k=rt, rank_v=rt)
+    rtv = torch.from_numpy(ranks_v).cuda().contiguous()
+    cache.prefill(0, kt, vt, [T] * B, rank_k=rt, rank_v=rtv)
     torch.cuda.synchronize()
     assert cache.device_status() == 0
     del kt, vt
-    return wl, cache, K, V, ranks
+    return wl, cache, K, V, ranks, ranks_v
 
 
 def _head_pages(cache, wl, b, h):
@@ -52,9 +55,9 @@ def _head_pages(cache, wl, b, h):
 
 def _run(name, heads, n_pages_checked):
     import torch
-    wl, cache, K, V, ranks = _build(name)
+    wl, cache, K, V, ranks, ranks_v = _build(name)
     B, Hkv, d, P, T = wl.batch, wl.kv_heads, wl.head_dim, wl.page, wl.tokens
-    g, R = wl.group, max(wl.ranks)
+    g, R = wl.group, max(wl.ranks + wl.ranks_v)
     n = -(-T // P)
     kinds = oracle.plan_pages(T, P, wl.sink, wl.window, n)
     # page table: kinds and ranks of every entry
@@ -62,7 +65,7 @@ def _run(name, heads, n_pages_checked):
     assert np.array_equal(kind[:, :, :n], np.broadcast_to(kinds, (B, Hkv, n)))
     fac = kinds == oracle.FACTOR
     assert np.array_equal(rk[:, :, :n][:, :, fac], ranks[:, :, :n][:, :, fac])
-    assert np.array_equal(rv[:, :, :n][:, :, fac], ranks[:, :, :n][:, :, fac])
+    assert np.array_equal(rv[:, :, :n][:, :, fac], ranks_v[:, :, :n][:, :, fac])
     # one attention call over the whole batch, as bench.py makes it
     q = synth.queries(wl, 0, 0)
     qt = torch.from_numpy(q).to("cuda", torch.bfloat16).contiguous()
@@ -82,11 +85,11 @@ def _run(name, heads, n_pages_checked):
         for j in range(n):
             o = blk[j]
             if kinds[j] == oracle.FACTOR:
-                r = int(ranks[b, h, j])
+                r, r_v = int(ranks[b, h, j]), int(ranks_v[b, h, j])
                 Lk = o[:P * R].reshape(P, R)[:, :r]
                 Rk = o[P * R:P * R + R * d].reshape(R, d)[:r]
-                Lv = o[P * R + R * d:2 * P * R + R * d].reshape(P, R)[:, :r]
-                Rv = o[2 * P * R + R * d:2 * P * R + 2 * R * d].reshape(R, d)[:r]
+                Lv = o[P * R + R * d:2 * P * R + R * d].reshape(P, R)[:, :r_v]
+                Rv = o[2 * P * R + R * d:2 * P * R + 2 * R * d].reshape(R, d)[:r_v]
                 pages.append(("factor", Lk, Rk, Lv, Rv))
             else:
                 pages.append(("dense", o[:P * d].reshape(P, d), o[P * d:2 * P * d].reshape(P, d)))
@@ -100,10 +103,11 @@ def _run(name, heads, n_pages_checked):
         # quantizer is checked against the oracle in test_gpu_int4)
         if wl.factors == "bf16":
             for j in rng.choice(np.flatnonzero(fac), n_pages_checked, replace=False):
-                r = int(ranks[b, h, j])
+                r, r_v = int(ranks[b, h, j]), int(ranks_v[b, h, j])
                 Lk, Rk, Lv, Rv = pages[j][1:]
-                for L, Rm, X in ((Lk, Rk, K[b, h, j * P:(j + 1) * P]), (Lv, Rv, V[b, h, j * P:(j + 1) * P])):
-                    _check_factor(L, Rm, X.astype(np.float64), r, 6e-3, 1e-2, 4e-3)
+                for L, Rm, X, rr in ((Lk, Rk, K[b, h, j * P:(j + 1) * P], r),
+                                     (Lv, Rv, V[b, h, j * P:(j + 1) * P], r_v)):
+                    _check_factor(L, Rm, X.astype(np.float64), rr, 6e-3, 1e-2, 4e-3)
                     checked += 1
     return checked
 
@@ -117,6 +121,15 @@ def test_fullsize_qwen32b_128k_bf16():
 def test_fullsize_qwen32b_int4():
     """B=8, same heads and length, INT4 factors with fp16 scales."""
     _run("qwen32b_int4", [(0, 0), (4, 3), (7, 7)], 0)
+
+
+def test_fullsize_paper_default_qwen8b_16k():
+    """The paper's default configuration: Qwen3-8B heads (32 q / 8 kv, d=128),
+    pages of 32 tokens, (r_K, r_V) = (16, 14), 32-token sink, dense region of
+    the last completed page plus the partial page, T=16384: every KV head,
+    three sampled decompositions each (two pages per wavefront at P = 32)."""
+    checked = _run("qwen8b_paper_default", [(0, h) for h in range(8)], 3)
+    assert checked == 8 * 3 * 2
 
 
 def test_fullsize_llama8b_32k_all_heads():
