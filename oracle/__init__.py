@@ -58,6 +58,8 @@ def _load():
     lib.orc_svd_rows.restype = i32
     lib.orc_truncated_factors.argtypes = [i32, i32, i32, p, p, p, p, i32]
     lib.orc_truncated_factors.restype = i32
+    lib.orc_adaptive_rank.argtypes = [i32, p, dbl, i32]
+    lib.orc_adaptive_rank.restype = i32
     lib.orc_truncated_factors_batch.argtypes = [i32, i32, i32, p, p, p, p, i32, p, p, i32]
     lib.orc_truncated_factors_batch.restype = None
     lib.orc_attention.argtypes = [i64, i32, i32, i32, i32, p, p, p, p, p, p, p, p]
@@ -129,6 +131,14 @@ def truncated_factors(X: np.ndarray, r: int, max_sweeps: int = MAX_SWEEPS):
     sw = _load().orc_truncated_factors(P, d, r, _ptr(X), _ptr(L), _ptr(R), _ptr(sig),
                                        max_sweeps)
     return L, R, sig, int(sw)
+
+
+def adaptive_rank(sig: np.ndarray, eps: float, cap: int) -> int:
+    """Smallest r >= 1 with |X - X_r|_F <= eps |X|_F given the page's singular
+    values in descending order (the reconstruction-accuracy reading of the
+    paper's Figure 2), capped at cap."""
+    sig = np.ascontiguousarray(sig, dtype=np.float64)
+    return int(_load().orc_adaptive_rank(len(sig), _ptr(sig), float(eps), int(cap)))
 
 
 def truncated_factors_batch(X: np.ndarray, ranks, max_sweeps: int = MAX_SWEEPS):

@@ -13,7 +13,7 @@
  *       "Incremental Cache Update"; Section 4.1 "Implementation" for the
  *       default dense region of one sink page, the last completed page and
  *       the current incomplete page).
- *   orc_svd_rows / orc_truncated_factors
+ *   orc_svd_rows / orc_truncated_factors / orc_adaptive_rank
  *       rank-r truncated SVD of one P x d page, computed without the Gram
  *       matrix by one-sided (Hestenes) Jacobi on the page rows, and the
  *       factor pair L = U_r, R = Sigma_r W_r^T (Section 3.2 "Truncated SVD";
@@ -199,6 +199,25 @@ int orc_truncated_factors(int P, int d, int r, const double *X, double *L, doubl
     memcpy(R, Rf, sizeof(double) * (size_t)r * d);
     free(U); free(Rf);
     return sw;
+}
+
+/* Adaptive page rank. The paper sizes ranks by reconstruction accuracy
+ * (Figure 2: the rank a page needs for 80% reconstruction accuracy), read
+ * here as the relative Frobenius error of the rank-r truncation: the rank is
+ * the smallest r >= 1 with |X - X_r|_F <= eps |X|_F, i.e. with
+ * sum_{i >= r} sig_i^2 <= eps^2 sum_i sig_i^2 (Eckart-Young), capped at cap.
+ * sig: the n singular values in descending order. */
+int orc_adaptive_rank(int n, const double *sig, double eps, int cap)
+{
+    double total = 0.0;
+    for (int i = 0; i < n; ++i) total += sig[i] * sig[i];
+    const double budget = eps * eps * total;
+    for (int r = 1; r <= cap && r <= n; ++r) {
+        double tail = 0.0;
+        for (int i = r; i < n; ++i) tail += sig[i] * sig[i];
+        if (tail <= budget) return r;
+    }
+    return cap < n ? cap : n;
 }
 
 /* Batched form over n pages for the CPU baseline and large test sweeps; page

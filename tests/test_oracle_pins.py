@@ -455,3 +455,61 @@ def test_int4_zero_and_exact_grid():
     x = c * 0.25
     codes, sc = int4.quantize_lines(x, 0)
     assert np.array_equal(codes[:, 0], c[:, 0].astype(np.int8)) and sc[0, 0] == 0.25
+
+
+# --------------------------------------------------------------------------
+# Adaptive page rank (reconstruction-accuracy reading of Figure 2)
+# --------------------------------------------------------------------------
+def _orthonormal(n, rng):
+    """An orthonormal basis from a Householder QR, independent of the oracle."""
+    q, r = np.linalg.qr(rng.standard_normal((n, n)))
+    return q * np.sign(np.diag(r))
+
+
+def test_adaptive_rank_hand_computed_spectrum():
+    """sigma = (4, 3, 2, 1): |X|_F^2 = 30 and the tails after r = 1, 2, 3 are
+    14, 5 and 1. With eps = 0.5 the budget is 7.5, first met at r = 2; with
+    eps = 0.2 it is 1.2, met at r = 3; with eps = 0.1 (0.3) only r = 4 meets
+    it. The page is built from that spectrum with independent orthonormal U
+    and W, so the oracle's SVD is part of what is checked."""
+    rng = np.random.default_rng(21)
+    U = _orthonormal(4, rng)
+    W = _orthonormal(12, rng)[:, :4]
+    X = U @ np.diag([4.0, 3.0, 2.0, 1.0]) @ W.T
+    _, s, _, _ = oracle.svd_rows(X)
+    for eps, r in ((0.5, 2), (0.2, 3), (0.1, 4), (0.9, 1)):
+        assert oracle.adaptive_rank(s, eps, 4) == r, (eps, r)
+    assert oracle.adaptive_rank(s, 0.1, 2) == 2          # capped
+
+
+def test_adaptive_rank_closed_forms():
+    """An orthogonal page (all sigma = 1, n x n) needs r = ceil(n (1 - eps^2));
+    a zero page needs rank 1; a rank-k page needs at most k at any eps > 0."""
+    rng = np.random.default_rng(22)
+    n = 16
+    Q = _orthonormal(n, rng)
+    _, s, _, _ = oracle.svd_rows(Q)
+    for eps in (0.2, 0.5, 0.7):
+        assert oracle.adaptive_rank(s, eps, n) == math.ceil(n * (1 - eps * eps) - 1e-9), eps
+    _, s0, _, _ = oracle.svd_rows(np.zeros((8, 16)))
+    assert oracle.adaptive_rank(s0, 0.2, 8) == 1
+    Xk = rng.standard_normal((32, 5)) @ rng.standard_normal((5, 64))
+    _, sk, _, _ = oracle.svd_rows(Xk)
+    assert oracle.adaptive_rank(sk, 1e-6, 32) <= 5
+
+
+@pytest.mark.parametrize("eps", [0.2, 0.05])
+def test_adaptive_rank_meets_the_bound_by_brute_force(eps):
+    """For random low-rank-plus-noise pages, the truncated factors at the
+    chosen rank meet |X - L R|_F <= eps |X|_F (measured on the factors, not on
+    the singular values), and one rank less does not."""
+    rng = np.random.default_rng(23)
+    for _ in range(6):
+        X = rng.standard_normal((32, 6)) @ rng.standard_normal((6, 64)) + 0.3 * rng.standard_normal((32, 64))
+        _, s, _, _ = oracle.svd_rows(X)
+        r = oracle.adaptive_rank(s, eps, 32)
+        L, R, _, _ = oracle.truncated_factors(X, r)
+        assert np.linalg.norm(X - L @ R) <= eps * np.linalg.norm(X) * (1 + 1e-12)
+        if r > 1:
+            L1, R1, _, _ = oracle.truncated_factors(X, r - 1)
+            assert np.linalg.norm(X - L1 @ R1) > eps * np.linalg.norm(X)
