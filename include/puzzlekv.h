@@ -127,6 +127,15 @@ typedef struct {
     void *dense_pool;      /* device */
     void *factor_pool;     /* device */
     pkv_page *page_table;  /* device */
+    /* Adaptive page ranks: 0 (off) or eps in (0, 1). When set, a rank request
+     * of 0 (a page's entry in pkv_prefill's rank tables, its default ranks, or
+     * pkv_compress_pages' rank arrays) asks the decomposition for the smallest
+     * r with |X - X_r|_F <= eps |X|_F, X the stored page, capped at
+     * min(P, d, max_rank): the rank a page needs for a reconstruction accuracy
+     * of 1 - eps (the criterion behind the paper's Figure 2; 80% is
+     * eps = 0.2). K and V choose independently; the chosen ranks are written
+     * to the page table. Needs bf16 dense pages with P = 32 or 64. */
+    float adaptive_rank_error;
 } pkv_cache;
 
 /* ---- geometry and sizing (host only, no device work) -------------------- */
@@ -174,7 +183,8 @@ pkv_status pkv_cache_reset(const pkv_cache *c, int32_t layer, pkv_stream s);
  * seq_len: host [batch], 0 <= seq_len[b] <= min(src_tokens, max_pages * P).
  * rank_k, rank_v: device [batch][n_kv_heads][max_pages] ranks of factor pages,
  * or NULL to use default_rank_k / default_rank_v for every page; a device rank
- * outside 1..max_rank is clamped and raises PKV_DEV_BAD_RANK.
+ * outside 1..max_rank is clamped and raises PKV_DEV_BAD_RANK. With adaptive
+ * ranks enabled (adaptive_rank_error > 0) a rank of 0 is chosen per page.
  * Pages of the plan for seq_len[b] are written: dense pages copied, factor
  * pages decomposed by the same kernel as pkv_compress_pages; pages past the
  * sequence become EMPTY. Workspace: pkv_workspace_bytes(PKV_OP_PREFILL, max T). */
@@ -197,7 +207,8 @@ pkv_status pkv_append_kv(const pkv_cache *c, int32_t layer, const void *k_new, c
  * L = its top-r eigenvectors, R = L^T X, which are the rank-r truncated-SVD
  * factors of Eq. (2)); K and V of a page are decomposed independently.
  * b, kv_head, page: host [n]; rank_k, rank_v: host [n], 1 <= r <= min(P, d,
- * max_rank). Each page must be complete and DENSE; the entry becomes FACTOR
+ * max_rank), or 0 for a rank chosen per page when adaptive ranks are enabled
+ * (adaptive_rank_error > 0). Each page must be complete and DENSE; the entry becomes FACTOR
  * with its ranks and its dense slot is free for reuse. A page found not dense
  * is left untouched and PKV_DEV_NOT_DENSE is raised. Duplicate pages in one
  * call are rejected (PKV_E_ARG). Workspace: pkv_workspace_bytes(PKV_OP_COMPRESS, n). */

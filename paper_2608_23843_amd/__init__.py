@@ -74,7 +74,7 @@ class PuzzleKVCache:
 
     def __init__(self, n_layers, batch, n_kv_heads, n_q_heads, head_dim, page_size, max_pages,
                  max_rank, sink_tokens, window_tokens, dense_dtype="bf16", factor_dtype="bf16",
-                 device="cuda"):
+                 device="cuda", adaptive_rank_error=0.0):
         import torch
         self.torch = torch
         self.lib = _lib.load()
@@ -83,6 +83,7 @@ class PuzzleKVCache:
         c.head_dim, c.page_size, c.max_pages, c.max_rank = head_dim, page_size, max_pages, max_rank
         c.sink_tokens, c.window_tokens = sink_tokens, window_tokens
         c.dense_dtype, c.factor_dtype = _DTYPES[dense_dtype], _DTYPES[factor_dtype]
+        c.adaptive_rank_error = float(adaptive_rank_error)   # > 0: rank requests of 0 are chosen per page
         self.c = c
         self.device = torch.device(device)
         lib = self.lib

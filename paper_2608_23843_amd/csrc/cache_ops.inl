@@ -108,9 +108,12 @@ __global__ __launch_bounds__(256) void k_prefill_pages(Geo g, pkv_page *table, c
             if (rank_k) {
                 rk = rank_k[head * g.max_pages + j];
                 rv = rank_v[head * g.max_pages + j];
-                if (rk < 1 || rk > rmax || rv < 1 || rv > rmax) raise_status(PKV_DEV_BAD_RANK);
-                rk = max(1, min(rk, rmax));
-                rv = max(1, min(rv, rmax));
+                // 0 with adaptive ranks: chosen by the decomposition, which
+                // writes it into this entry
+                const int rmin = g.rank_err > 0.f ? 0 : 1;
+                if (rk < rmin || rk > rmax || rv < rmin || rv > rmax) raise_status(PKV_DEV_BAD_RANK);
+                rk = max(rmin, min(rk, rmax));
+                rv = max(rmin, min(rv, rmax));
             }
             write_entry(e, (int)(head * g.max_pages + j), PKV_FACTOR, rk, rv);
         }
@@ -203,7 +206,11 @@ __global__ void k_compress_commit(Geo g, pkv_page *table, CompressItems items) {
     if (i >= items.n) return;
     const CompressItem it = items.it[i];
     const int64_t idx = g.head_index(it.b, it.h) * g.max_pages + it.j;
-    if (table[idx].kind == PKV_DENSE) write_entry(table + idx, (int)idx, PKV_FACTOR, it.rk, it.rv);
+    if (table[idx].kind == PKV_DENSE) {
+        // a requested rank of 0 was chosen by the decomposition and stored in the entry
+        const pkv_page cur = table[idx];
+        write_entry(table + idx, (int)idx, PKV_FACTOR, it.rk ? it.rk : cur.rank_k, it.rv ? it.rv : cur.rank_v);
+    }
 }
 
 hipError_t launch_compress_commit(const LaunchCtx &L, const CompressItems &items) {

@@ -77,8 +77,9 @@ __device__ inline DecompRef decode_decomp(const Geo &g, const pkv_page *table, c
         const int64_t head = g.head_index(r.b, r.h);
         if (src.rank_k) {
             const int rmax = min(g.max_rank, min(g.P, g.d));
-            r.rk = max(1, min((int)src.rank_k[head * g.max_pages + r.j], rmax));
-            r.rv = max(1, min((int)src.rank_v[head * g.max_pages + r.j], rmax));
+            const int rmin = g.rank_err > 0.f ? 0 : 1;   // 0: chosen per page
+            r.rk = max(rmin, min((int)src.rank_k[head * g.max_pages + r.j], rmax));
+            r.rv = max(rmin, min((int)src.rank_v[head * g.max_pages + r.j], rmax));
         } else {
             r.rk = src.def_rk;
             r.rv = src.def_rv;

@@ -86,9 +86,26 @@ __device__ __forceinline__ float cq_group_sum(float v) {
     v += cq_f(__builtin_amdgcn_ds_swizzle(cq_i(v), (4 << 10) | 0x1f));
     v += cq_f(__builtin_amdgcn_ds_swizzle(cq_i(v), (8 << 10) | 0x1f));
     v += cq_f(__builtin_amdgcn_ds_swizzle(cq_i(v), (16 << 10) | 0x1f));
-    if constexpr (P == 64) v += cq_f(__builtin_amdgcn_ds_bpermute((int)((threadIdx.x ^ 32) << 2), cq_i(v)));
+    if constexpr (P == 64) v += cq_f(__builtin_amdgcn_ds_bpermute((int)(((threadIdx.x & 63) ^ 32) << 2), cq_i(v)));
     return v;
 }
+
+// Minimum over the lanes of a P-lane group.
+template <int P>
+__device__ __forceinline__ int cq_group_min(int v) {
+    v = min(v, __builtin_amdgcn_ds_swizzle(v, (1 << 10) | 0x1f));
+    v = min(v, __builtin_amdgcn_ds_swizzle(v, (2 << 10) | 0x1f));
+    v = min(v, __builtin_amdgcn_ds_swizzle(v, (4 << 10) | 0x1f));
+    v = min(v, __builtin_amdgcn_ds_swizzle(v, (8 << 10) | 0x1f));
+    v = min(v, __builtin_amdgcn_ds_swizzle(v, (16 << 10) | 0x1f));
+    if constexpr (P == 64) v = min(v, __builtin_amdgcn_ds_bpermute((int)(((threadIdx.x & 63) ^ 32) << 2), v));
+    return v;
+}
+
+// LDS floats per wavefront: R's row buffer (64), L staged as 64 x 32, inverse
+// singular values (64), the position -> token table (64); INT4 adds R~
+// (32 x d) and the scales ((P/32) r8 + d <= 64 + d).
+__host__ __device__ inline int cq_wave_lds(int d, bool q4) { return 64 + 64 * 32 + 64 + 64 + (q4 ? 32 * d + 64 + d : 0); }
 
 // Rank of `key` among the P lanes of the group: descending, ties to the lower lane.
 template <int P>
@@ -101,18 +118,25 @@ __device__ __forceinline__ int cq_rank(float key, int c, int grp) {
     return rho;
 }
 
+// One workgroup per page: its K and V decompositions are two wavefronts at
+// P = 64 and the two halves of one wavefront at P = 32, so the pair can agree
+// on its ranks (adaptive ranks decide them here) before either stores.
 template <typename TF, int P>
-__global__ __launch_bounds__(64) void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor,
-                                                    CompressItems items, CompressSrc src, int64_t n_decomp) {
+__global__ __launch_bounds__(128) void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor,
+                                                     CompressItems items, CompressSrc src, int64_t n_decomp) {
     static_assert(P == 32 || P == 64, "P = 32 or 64");
-    constexpr int D = 64 / P;
-    extern __shared__ float cq_smem[];
-    int *cq_tok = (int *)(cq_smem + 64 + 64 * 32 + 64);   // position -> token, per group
+    constexpr int D = 64 / P;          // decompositions per wave
+    constexpr int WPB = 2 / D;         // waves per workgroup
+    constexpr bool kQ4 = is_q4<TF>::value;
+    extern __shared__ float cq_lds[];
     const int d = g.d;
-    const int lane = threadIdx.x;
+    const int wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    float *cq_smem = cq_lds + wave * cq_wave_lds(d, kQ4);
+    int *cq_tok = (int *)(cq_smem + 64 + 64 * 32 + 64);   // position -> token, per group
     const int grp = P == 64 ? 0 : lane >> 5;
     const int c = P == 64 ? lane : lane & 31;
-    const int64_t q = (int64_t)blockIdx.x * D + grp;
+    const int64_t q = ((int64_t)blockIdx.x * WPB + wave) * D + grp;
 
     const DecompRef ref = decode_decomp<uint16_t>(g, table, dense, items, src, q, n_decomp, c == 0);
     const bool active = ref.active;
@@ -120,15 +144,19 @@ __global__ __launch_bounds__(64) void k_compress_qr(Geo g, pkv_page *table, cons
 
     // ---- 1. Gram matrix by MFMA, lane c <- column c ------------------------
     float gc[P];
+    float xnorm2 = 0.f;   // |X|_F^2 of this lane's page half
     {
         const int row = lane & 31, kh = lane >> 5;
         if constexpr (P == 64) {
             cq_f32x16 c00 = {}, c01 = {}, c10 = {}, c11 = {};
+            float e2 = 0.f;
             if (active) {
                 for (int s = 0; s < d / 16; ++s) {
                     const int k0 = 16 * s + 8 * kh;
                     const cq_bf16x8 a0 = cq_load8(X, ref.transposed, P, d, row, k0);
                     const cq_bf16x8 a1 = cq_load8(X, ref.transposed, P, d, 32 + row, k0);
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) e2 = fmaf((float)a1[u], (float)a1[u], fmaf((float)a0[u], (float)a0[u], e2));
                     c00 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, a0, c00, 0, 0, 0);
                     c01 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0, a1, c01, 0, 0, 0);
                     c10 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1, a0, c10, 0, 0, 0);
@@ -138,6 +166,7 @@ __global__ __launch_bounds__(64) void k_compress_qr(Geo g, pkv_page *table, cons
             // C[m][n] sits in lane 32 (m/4 % 2) + n; swapping the upper half of
             // the column-tile-0 accumulator with the lower half of column tile 1
             // gives lane c all of column c (rows 0..31), likewise for rows 32..63.
+            xnorm2 = cq_group_sum<64>(e2);   // |X|_F^2: every element was loaded by one lane
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
                 const auto r0 = __builtin_amdgcn_permlane32_swap(__float_as_uint(c00[i]), __float_as_uint(c01[i]), false, false);
@@ -159,17 +188,24 @@ __global__ __launch_bounds__(64) void k_compress_qr(Geo g, pkv_page *table, cons
             const int tr0 = __builtin_amdgcn_readlane(ref.transposed ? 1 : 0, 0);
             const int tr1 = __builtin_amdgcn_readlane(ref.transposed ? 1 : 0, 32);
             cq_f32x16 cg0 = {}, cg1 = {};
+            float e0 = 0.f, e1 = 0.f;
             for (int s = 0; s < d / 16; ++s) {
                 const int k0 = 16 * s + 8 * kh;
                 if (act0) {
                     const cq_bf16x8 a = cq_load8((const uint16_t *)(uintptr_t)x0, tr0, P, d, row, k0);
                     cg0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, a, cg0, 0, 0, 0);
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) e0 = fmaf((float)a[u], (float)a[u], e0);
                 }
                 if (act1) {
                     const cq_bf16x8 a = cq_load8((const uint16_t *)(uintptr_t)x1, tr1, P, d, row, k0);
                     cg1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, a, cg1, 0, 0, 0);
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) e1 = fmaf((float)a[u], (float)a[u], e1);
                 }
             }
+            const float n0 = cq_group_sum<64>(e0), n1 = cq_group_sum<64>(e1);
+            xnorm2 = grp ? n1 : n0;
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
                 const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(cg0[i]), __float_as_uint(cg1[i]), false, false);
@@ -254,7 +290,11 @@ __global__ __launch_bounds__(64) void k_compress_qr(Geo g, pkv_page *table, cons
     constexpr float kTolFactor = std::is_same<TF, uint16_t>::value ? 10.f : 1.f;
     const float tol = kTolFactor * (float)P * 1.1920929e-7f;
     const float stop_tol = sqrtf(tol);
-    const int r_need = ref.which == 0 ? ref.rk : ref.rv;
+    // requested rank, 0 for a rank chosen from the spectrum (adaptive ranks):
+    // then the r_cap largest columns are converged
+    const int r_req = ref.which == 0 ? ref.rk : ref.rv;
+    const int r_cap = min(g.max_rank, min(P, d));
+    const int r_need = r_req > 0 ? r_req : r_cap;
     // tag = top flag << 8 | column id: the id travels with the column, so
     // equal norms (zero columns) are ranked the same way wherever they sit
     float dsc = 1.f, alpha = 0.f;
@@ -378,6 +418,21 @@ __global__ __launch_bounds__(64) void k_compress_qr(Geo g, pkv_page *table, cons
     const float lam = sqrtf(an2) * gnorm;   // eigenvalue of G (column norm of G Q J)
     const int rho = cq_rank<P>(an2, c, grp);
     const bool tinycol = !(an2 > kCqTiny2);
+    // Adaptive rank: the smallest r with |X - X_r|_F^2 = |X|_F^2 - (sum of the
+    // r largest eigenvalues of G) <= eps^2 |X|_F^2, capped at r_cap (only the
+    // r_cap largest columns are converged, and only they enter the sums used).
+    int r_own = r_req;
+    if (__any(r_req == 0)) {
+        float head = 0.f;   // energy of the columns ranked at or above this one
+        for (int k = 0; k < P; ++k) {
+            const float lk = cq_group_bcast<P>(lam, k, 32 + k, grp);
+            const int rk_ = __float_as_int(cq_group_bcast<P>(__int_as_float(rho), k, 32 + k, grp));
+            head += rk_ <= rho ? lk : 0.f;
+        }
+        const bool ok = xnorm2 - head <= g.rank_err * g.rank_err * xnorm2;
+        const int cand = cq_group_min<P>(ok ? rho + 1 : P + 1);
+        if (r_req == 0) r_own = max(1, min(cand, r_cap));
+    }
     {
         // A column at rounding level starts from the unit vector of its own
         // id k (the row of R it began as; ids travel with the columns): the
@@ -434,9 +489,24 @@ __global__ __launch_bounds__(64) void k_compress_qr(Geo g, pkv_page *table, cons
     // two output dims for every rank: one 4-byte load per page row (a row is
     // one coalesced 256-byte read across the lanes) and 64 fmas against the
     // row's L entries, read as broadcasts.
-    const int which = ref.which, rk = ref.rk, rv = ref.rv;
+    // the page's K and V ranks (each chosen by its own half when adaptive)
+    int rk, rv;
+    if constexpr (P == 64) {
+        __shared__ int s_rank[2];
+        if (lane == 0) s_rank[wave] = r_own;   // wave 0 decomposes K, wave 1 V
+        __syncthreads();
+        rk = s_rank[0];
+        rv = s_rank[1];
+    } else {
+        rk = __builtin_amdgcn_readlane(r_own, 0);    // lanes 0..31 decompose K, 32..63 V
+        rv = __builtin_amdgcn_readlane(r_own, 32);
+    }
+    const int which = ref.which;
     const int r = which == 0 ? rk : rv;
-    constexpr bool kQ4 = is_q4<TF>::value;
+    if (active && c == 0 && r_req == 0) {   // the chosen rank goes into the page's entry
+        uint8_t *ent = (uint8_t *)(table + g.head_index(ref.b, ref.h) * g.max_pages + ref.j);
+        ent[which == 0 ? offsetof(pkv_page, rank_k) : offsetof(pkv_page, rank_v)] = (uint8_t)r;
+    }
     float *sL = cq_smem + 64 + grp * (P * 32);   // this group's P x 32 block
     float *sInvSig = cq_smem + 64 + 64 * 32 + grp * 32;
     {
@@ -455,7 +525,7 @@ __global__ __launch_bounds__(64) void k_compress_qr(Geo g, pkv_page *table, cons
 
     const int64_t slot_off = (g.head_index(ref.b, ref.h) * g.max_pages + ref.j) * g.factor_slot_bytes;
     constexpr int kCols = 2;                      // dims per lane per pass
-    float *sR = cq_smem + 64 + 64 * 32 + 64 + 64;   // INT4 only: 32 x d (one group: P = 64)
+    float *sR = cq_smem + 64 + 64 * 32 + 64 + 64;   // INT4 only: 32 x d (P = 64: one group per wave)
     for (int k0 = 0; k0 < d; k0 += kCols * P) {
         const int k = k0 + kCols * c;
         const bool kin = k < d;
@@ -549,15 +619,12 @@ inline bool compress_qr_supported(const Geo &g) {
 template <typename TF, int P>
 hipError_t launch_compress_qr_t(const LaunchCtx &L, const CompressItems &items, const CompressSrc &src,
                                 int64_t n_decomp) {
-    constexpr int D = 64 / P;
-    // row buffers (64) + L blocks (64 x 32) + inverse sigmas (64) + token tables (64);
-    // INT4 adds R~ (32 x d) and scales
-    size_t smem = (64 + 64 * 32 + 64 + 64) * sizeof(float);
-    if (is_q4<TF>::value) smem += (size_t)(32 * L.geo.d + 64 + L.geo.d) * sizeof(float);
-    const int64_t blocks = ceil_div(n_decomp, D);
+    constexpr int WPB = P == 64 ? 2 : 1;   // one page (K and V) per workgroup
+    const size_t smem = (size_t)WPB * cq_wave_lds(L.geo.d, is_q4<TF>::value) * sizeof(float);
+    const int64_t blocks = ceil_div(n_decomp, 2);
     LayerPtrs p = layer_ptrs(L);
-    hipLaunchKernelGGL((k_compress_qr<TF, P>), dim3((unsigned)blocks), dim3(64), smem, L.stream, L.geo, p.table,
-                       p.dense, p.factor, items, src, n_decomp);
+    hipLaunchKernelGGL((k_compress_qr<TF, P>), dim3((unsigned)blocks), dim3(64 * WPB), smem, L.stream, L.geo,
+                       p.table, p.dense, p.factor, items, src, n_decomp);
     return hipGetLastError();
 }
 

@@ -54,6 +54,10 @@ pkv_status check_geometry(const pkv_cache *c) {
     if (c->sink_tokens < 0 || c->window_tokens < 0)
         return fail(PKV_E_SHAPE, "sink and window must be non-negative");
     if (elem_size(c->dense_dtype) == 0) return fail(PKV_E_UNSUPPORTED, "dense dtype %d", c->dense_dtype);
+    if (!(c->adaptive_rank_error >= 0.f && c->adaptive_rank_error < 1.f))
+        return fail(PKV_E_ARG, "adaptive_rank_error %g outside [0, 1)", (double)c->adaptive_rank_error);
+    if (c->adaptive_rank_error > 0.f && (c->dense_dtype != PKV_BF16 || (c->page_size != 32 && c->page_size != 64)))
+        return fail(PKV_E_UNSUPPORTED, "adaptive ranks need bf16 dense pages with P = 32 or 64");
     if (c->factor_dtype == PKV_INT4) {
         if (c->dense_dtype != PKV_BF16 || c->page_size != 64 || c->head_dim != 128 || c->max_rank > 32)
             return fail(PKV_E_UNSUPPORTED,
@@ -88,6 +92,7 @@ Geo make_geo(const pkv_cache *c) {
     g.P = c->page_size;
     g.max_pages = c->max_pages;
     g.max_rank = c->max_rank;
+    g.rank_err = c->adaptive_rank_error;
     g.S = c->sink_tokens;
     g.W = c->window_tokens;
     g.sink_pages = (int)ceil_div(c->sink_tokens, c->page_size);
@@ -260,9 +265,11 @@ pkv_status pkv_prefill(const pkv_cache *c, int32_t layer, const void *k, const v
     if ((rank_k == nullptr) != (rank_v == nullptr))
         return fail(PKV_E_ARG, "rank_k and rank_v must both be given or both be NULL");
     const int rmax = std::min(c->max_rank, std::min(c->page_size, c->head_dim));
-    if (!rank_k && (default_rank_k < 1 || default_rank_v < 1 || default_rank_k > rmax ||
+    const int rmin = c->adaptive_rank_error > 0.f ? 0 : 1;   // 0: chosen per page
+    if (!rank_k && (default_rank_k < rmin || default_rank_v < rmin || default_rank_k > rmax ||
                     default_rank_v > rmax))
-        return fail(PKV_E_RANK, "default ranks (%d, %d) outside 1..%d", default_rank_k, default_rank_v, rmax);
+        return fail(PKV_E_RANK, "default ranks (%d, %d) outside %d..%d", default_rank_k, default_rank_v, rmin,
+                    rmax);
     SeqArgs seq{};
     seq.n = c->batch;
     int max_np = 0;
@@ -329,13 +336,15 @@ pkv_status pkv_compress_pages(const pkv_cache *c, int32_t layer, int32_t n, cons
     if (n == 0) return PKV_OK;
     if (!b || !kv_head || !page || !rank_k || !rank_v) return fail(PKV_E_ARG, "NULL page list");
     const int rmax = std::min(c->max_rank, std::min(c->page_size, c->head_dim));
+    const int rmin = c->adaptive_rank_error > 0.f ? 0 : 1;   // 0: chosen per page
     std::vector<int64_t> keys((size_t)n);
     for (int i = 0; i < n; ++i) {
         if (b[i] < 0 || b[i] >= c->batch || kv_head[i] < 0 || kv_head[i] >= c->n_kv_heads ||
             page[i] < 0 || page[i] >= c->max_pages)
             return fail(PKV_E_ARG, "page ref %d (b=%d, h=%d, j=%d) out of range", i, b[i], kv_head[i], page[i]);
-        if (rank_k[i] < 1 || rank_v[i] < 1 || rank_k[i] > rmax || rank_v[i] > rmax)
-            return fail(PKV_E_RANK, "page ref %d: ranks (%d, %d) outside 1..%d", i, rank_k[i], rank_v[i], rmax);
+        if (rank_k[i] < rmin || rank_v[i] < rmin || rank_k[i] > rmax || rank_v[i] > rmax)
+            return fail(PKV_E_RANK, "page ref %d: ranks (%d, %d) outside %d..%d", i, rank_k[i], rank_v[i], rmin,
+                        rmax);
         keys[i] = ((int64_t)b[i] * c->n_kv_heads + kv_head[i]) * c->max_pages + page[i];
     }
     std::vector<int64_t> sorted = keys;

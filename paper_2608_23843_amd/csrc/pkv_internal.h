@@ -97,6 +97,7 @@ __host__ __device__ inline int plan_kind(int64_t T, int P, int S, int W, int64_t
 // Flattened geometry, passed to kernels by value.
 struct Geo {
     int B, Hkv, Hq, g, d, P, max_pages, max_rank;
+    float rank_err;                           // adaptive ranks: eps, or 0 (off)
     int S, W, sink_pages, ring_len, dslots;   // dslots = dense slots per head
     int dense_es, factor_es;                  // element sizes in bytes
     int dense_dtype, factor_dtype;

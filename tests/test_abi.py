@@ -135,3 +135,39 @@ def test_call_errors_before_any_launch(pk):
     # import: bad kind
     assert lib.pkv_import_pages(c, 0, 1, P(i32(0)), P(i32(0)), P(i32(0)), P(u8(7)), P(u8(0)), P(u8(0)),
                                 vp(0x2000), P(np.zeros(1, dtype=np.int64)), None, 0, None) == 1
+
+
+@pytest.mark.parametrize("kw,code", [(dict(adaptive_rank_error=1.0), 1), (dict(adaptive_rank_error=-0.1), 1),
+                                     (dict(adaptive_rank_error=float("nan")), 1),
+                                     (dict(adaptive_rank_error=0.2, dense_dtype=0), 6),
+                                     (dict(adaptive_rank_error=0.2, page_size=16, max_rank=16), 6)])
+def test_adaptive_rank_geometry_errors(pk, kw, code):
+    """Adaptive ranks: eps must lie in [0, 1) and needs the bf16 32/64-token decomposition."""
+    lib = pk.load_library()
+    c = _cache(pk, **kw)
+    c.dense_pool = c.factor_pool = c.page_table = 0x1000
+    assert lib.pkv_cache_check(c) == code
+    assert lib.pkv_last_error()
+
+
+def test_rank_zero_requests_need_adaptive_ranks(pk):
+    """A rank of 0 is a request for a rank chosen per page: refused on the host
+    (before any launch) unless the cache enables adaptive ranks; with them the
+    remaining checks (duplicates, range) still apply."""
+    lib = pk.load_library()
+    vp = ctypes.c_void_p
+    i32 = lambda *v: np.array(v, dtype=np.int32)
+    u8 = lambda *v: np.array(v, dtype=np.uint8)
+    P = lambda a: a.ctypes.data_as(vp)
+    b, h, j = i32(0, 1), i32(0, 1), i32(2, 3)
+    c = _cache(pk)
+    c.dense_pool = c.factor_pool = c.page_table = 0x1000
+    assert lib.pkv_compress_pages(c, 0, 2, P(b), P(h), P(j), P(u8(0, 0)), P(u8(0, 0)), None, 0, None) == 3
+    assert lib.pkv_prefill(c, 0, vp(0x2000), vp(0x2000), 128, P(i32(128, 128)), None, None, 0, 0, None, 0,
+                           None) == 3
+    ca = _cache(pk, adaptive_rank_error=0.2)
+    ca.dense_pool = ca.factor_pool = ca.page_table = 0x1000
+    assert lib.pkv_cache_check(ca) == 0
+    assert lib.pkv_compress_pages(ca, 0, 2, P(i32(0, 0)), P(i32(1, 1)), P(i32(3, 3)), P(u8(0, 0)),
+                                  P(u8(0, 0)), None, 0, None) == 1      # duplicate page
+    assert lib.pkv_compress_pages(ca, 0, 2, P(b), P(h), P(j), P(u8(33, 0)), P(u8(0, 0)), None, 0, None) == 3

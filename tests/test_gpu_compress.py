@@ -13,7 +13,7 @@ import pytest
 
 import oracle
 import synth
-from helpers import storage_round
+from helpers import MAX_ABS, MEAN_REL, errors, storage_round
 
 pytestmark = pytest.mark.gpu
 
@@ -306,3 +306,122 @@ def test_rank_deficient_and_zero_pages_bf16():
             assert np.all(Rk == 0) and np.all(Rv == 0)
         if j == 1:   # the five nonzero rows span the page: ranks 6..8 carry nothing
             assert np.abs(Rk[5:]).max() <= 1e-5 * np.abs(Rk).max()
+
+
+def _adaptive_ok(s, r, eps, cap, band=1e-3):
+    """r is an acceptable adaptive rank for singular values s: it meets the
+    bound |X - X_r|_F <= eps |X|_F and r - 1 does not, both up to a relative
+    band of the budget (the GPU decides the integer from fp32 eigenvalues of
+    the Gram matrix, the oracle from fp64 singular values)."""
+    E = float(np.sum(s ** 2))
+    budget = eps * eps * E
+    tail = lambda k: float(np.sum(s[k:] ** 2))
+    if r < 1 or r > cap:
+        return False
+    meets = tail(r) <= budget * (1 + band) + 1e-30
+    minimal = r == 1 or tail(r - 1) > budget * (1 - band) or r == cap and tail(cap) > budget
+    return meets and minimal
+
+
+@pytest.mark.parametrize("P,factor_dtype", [(64, "bf16"), (32, "bf16"), (64, "f32"), (64, "int4")])
+def test_adaptive_ranks_prefill(P, factor_dtype):
+    """Adaptive ranks (eps = 0.2, the paper's 80% reconstruction accuracy) on
+    Qwen3-32B-like key and value pages: every factor page's chosen ranks meet
+    the bound by the oracle's singular values of the stored page while one
+    rank less does not, the page table holds them, fp32 factors reconstruct
+    within the bound, and attention over the cache matches the oracle over the
+    exported pages."""
+    import torch
+    import paper_2608_23843_amd as pk
+    eps, d, S, W = 0.2, 128, P, 2 * P
+    B, Hkv, G = 1, 2, 8
+    T = P * 12 + 9
+    cap = 32
+    wl = synth.Workload("ad", 93, B, Hkv, Hkv * G, d, P, T, S, W, 24, (24,), "bf16", 1e6, 4)
+    K, V = synth.kv_layer(wl, 0, 0, T)
+    npg = -(-T // P)
+    cache = pk.PuzzleKVCache(1, B, Hkv, Hkv * G, d, P, npg, cap, S, W, "bf16", factor_dtype,
+                             adaptive_rank_error=eps)
+    cache.prefill(0, torch.from_numpy(K).to("cuda", torch.bfloat16).contiguous(),
+                  torch.from_numpy(V).to("cuda", torch.bfloat16).contiguous(), [T] * B, default_rank=(0, 0))
+    torch.cuda.synchronize()
+    assert cache.device_status() == 0
+    _, kind, rk, rv = cache.page_table_host(0)
+    plan = oracle.plan_pages(T, P, S, W, npg)
+    chosen = []
+    for h in range(Hkv):
+        assert np.array_equal(kind[0, h], plan)
+        for j in np.flatnonzero(plan == oracle.FACTOR):
+            for X, r in ((K[0, h, j * P:(j + 1) * P], int(rk[0, h, j])), (V[0, h, j * P:(j + 1) * P], int(rv[0, h, j]))):
+                _, s, _, _ = oracle.svd_rows(X.astype(np.float64))
+                assert _adaptive_ok(s, r, eps, cap), (h, j, r, oracle.adaptive_rank(s, eps, cap))
+                chosen.append(r)
+    assert len(set(chosen)) > 1, "the pages should need different ranks"
+    # factors at the chosen ranks
+    refs = [(0, h, int(j)) for h in range(Hkv) for j in np.flatnonzero(plan == oracle.FACTOR)]
+    blocks = _export(cache, refs)
+    R = cache.c.max_rank
+    if factor_dtype == "f32":
+        for (b, h, j), blk in zip(refs, blocks):
+            Lk, Rk, Lv, Rv = _unpack_factor(blk, P, d, R)
+            for L, Rm, X, r in ((Lk, Rk, K[b, h, j * P:(j + 1) * P], int(rk[b, h, j])),
+                                (Lv, Rv, V[b, h, j * P:(j + 1) * P], int(rv[b, h, j]))):
+                X = X.astype(np.float64)
+                assert np.linalg.norm(X - L[:, :r] @ Rm[:r]) <= eps * np.linalg.norm(X) * (1 + 1e-3)
+                _check_factor(L[:, :r], Rm[:r], X, r, 1e-4, 1e-4, 1e-5)
+    # attention over the whole cache against the oracle over the exported pages
+    q = synth.queries(wl, 0, 0)
+    out, _ = cache.attention(0, torch.from_numpy(q).to("cuda", torch.bfloat16).contiguous(), [T] * B)
+    out = out.cpu().numpy().astype(np.float64)
+    for h in range(Hkv):
+        blk = cache.export_pages(0, [0] * npg, [h] * npg, list(range(npg))).cpu().numpy().astype(np.float64)
+        pages = []
+        for j in range(npg):
+            o = blk[j]
+            if plan[j] == oracle.FACTOR:
+                a, c2 = int(rk[0, h, j]), int(rv[0, h, j])
+                pages.append(("factor", o[:P * R].reshape(P, R)[:, :a], o[P * R:P * R + R * d].reshape(R, d)[:a],
+                              o[P * R + R * d:2 * P * R + R * d].reshape(P, R)[:, :c2],
+                              o[2 * P * R + R * d:2 * P * R + 2 * R * d].reshape(R, d)[:c2]))
+            else:
+                pages.append(("dense", o[:P * d].reshape(P, d), o[P * d:2 * P * d].reshape(P, d)))
+        ro, _ = oracle.attention(oracle.HeadCache(T, P, d, pages), q[0, h * G:(h + 1) * G].astype(np.float64))
+        ma, mr = errors(out[0, h * G:(h + 1) * G], ro)
+        assert ma <= MAX_ABS and mr <= MEAN_REL, (h, ma, mr)
+
+
+def test_adaptive_ranks_incremental_compress():
+    """Pages compressed during decoding with a requested rank of 0 get ranks
+    chosen per page, written to the table when the entry becomes FACTOR."""
+    import torch
+    import paper_2608_23843_amd as pk
+    eps, B, Hkv, d, P, S, W = 0.2, 1, 2, 128, 64, 64, 128
+    T0, steps = 64 * 4 + 60, 40
+    wl = synth.Workload("c", 94, B, Hkv, Hkv, d, P, T0, S, W, 24, (24,), "bf16", 5e5, 4, decode_steps=steps)
+    K, V = synth.kv_layer(wl, 0, 0)
+    max_pages = -(-(T0 + steps) // P)
+    cache = pk.PuzzleKVCache(1, B, Hkv, Hkv, d, P, max_pages, 32, S, W, "bf16", "f32", adaptive_rank_error=eps)
+    cache.prefill(0, torch.from_numpy(K[:, :, :T0]).to("cuda", torch.bfloat16).contiguous(),
+                  torch.from_numpy(V[:, :, :T0]).to("cuda", torch.bfloat16).contiguous(), [T0] * B,
+                  default_rank=(24, 0))
+    converted = []
+    for t in range(T0, T0 + steps):
+        cache.append(0, torch.from_numpy(K[:, :, t]).to("cuda", torch.bfloat16).contiguous(),
+                     torch.from_numpy(V[:, :, t]).to("cuda", torch.bfloat16).contiguous(), [t] * B)
+        for j in oracle.eligible_pages(t, t + 1, P, S, W):
+            refs = [(0, h, int(j)) for h in range(Hkv)]
+            bb, hh, jj = zip(*refs)
+            cache.compress_pages(0, bb, hh, jj, [0] * len(refs), [0] * len(refs))
+            converted += refs
+    torch.cuda.synchronize()
+    assert cache.device_status() == 0 and converted
+    _, kind, rk, rv = cache.page_table_host(0)
+    for (b, h, j) in converted:
+        assert kind[b, h, j] == oracle.FACTOR
+        for X, r in ((K[b, h, j * P:(j + 1) * P], int(rk[b, h, j])), (V[b, h, j * P:(j + 1) * P], int(rv[b, h, j]))):
+            _, s, _, _ = oracle.svd_rows(X.astype(np.float64))
+            assert _adaptive_ok(s, r, eps, 32), (h, j, r, oracle.adaptive_rank(s, eps, 32))
+    # prefill kept the fixed key rank and chose the value ranks
+    plan = oracle.plan_pages(T0, P, S, W, max_pages)
+    for j in np.flatnonzero(plan == oracle.FACTOR):
+        assert rk[0, 0, j] == 24
