@@ -135,7 +135,20 @@ def compress_work(kinds, ranks_np, ranks_v_np, B, Hkv, P, d, sweeps_total):
     return {"sweeps": sweeps_total / max(n_dec, 1), "useful": useful, "executed": executed}
 
 
-def cpu_baseline(wl, seed, seq_T, K_dense, V_dense, q, budget_s, layers):
+def chosen_ranks(cache, kinds, max_pages, eps):
+    """The (rank_k, rank_v) the decomposition chose for layer 0, read from its page table."""
+    import numpy as np
+    import paper_2608_23843_amd as pk
+    _, _, rk, rv = cache.page_table_host(0)
+    rk = np.ascontiguousarray(rk[:, :, :max_pages]).astype(np.uint8)
+    rv = np.ascontiguousarray(rv[:, :, :max_pages]).astype(np.uint8)
+    fac = np.flatnonzero(np.asarray(kinds) == pk.PKV_FACTOR)
+    log("ranks chosen for relative error %.2f: mean r_K %.2f, mean r_V %.2f over %d factor pages per head"
+        % (eps, rk[:, :, fac].mean(), rv[:, :, fac].mean(), len(fac)))
+    return rk, rv
+
+
+def cpu_baseline(wl, seed, seq_T, K_dense, V_dense, q, budget_s, layers, ranks, ranks_v):
     """The oracle on a bounded sample: whole (sequence, KV head) heads of one
     layer at the full length, factor pages drawn by the generator, timed until
     the budget is spent; extrapolated to the step (all heads, all layers)."""
@@ -146,8 +159,6 @@ def cpu_baseline(wl, seed, seq_T, K_dense, V_dense, q, budget_s, layers):
     P, d, g = wl.page, wl.head_dim, wl.group
     int4 = wl.factors == "int4"
     kinds = oracle.plan_pages(seq_T, P, wl.sink, wl.window)
-    ranks = synth.page_ranks(wl, seed, 0, len(kinds))
-    ranks_v = synth.page_ranks(wl, seed, 0, len(kinds), "v")
     times, heads = [], []
     for b in range(wl.batch):
         for h in range(wl.kv_heads):
@@ -238,10 +249,15 @@ def main():
     del V
     ranks_np = synth.page_ranks(wl, args.seed, 0, max_pages)
     ranks_v_np = synth.page_ranks(wl, args.seed, 0, max_pages, "v")
+    if wl.rank_error > 0:   # rank 0: the decomposition chooses each page's ranks
+        ranks_np[:] = 0
+        ranks_v_np[:] = 0
+    req_np, req_v_np = ranks_np.copy(), ranks_v_np.copy()   # what prefill and compress_pages ask for
     ranks = torch.from_numpy(ranks_np).cuda().contiguous()
     ranks_v = torch.from_numpy(ranks_v_np).cuda().contiguous()
 
-    cache = pk.PuzzleKVCache(layers, B, Hkv, Hq, d, P, max_pages, max_rank, S, W, wl.dtype, wl.factors)
+    cache = pk.PuzzleKVCache(layers, B, Hkv, Hq, d, P, max_pages, max_rank, S, W, wl.dtype, wl.factors,
+                             adaptive_rank_error=wl.rank_error)
     log("cache: factor pool %.1f GB, dense pool %.2f GB" % (cache.factor_pool.numel() / 1e9,
                                                             cache.dense_pool.numel() / 1e9))
 
@@ -259,6 +275,8 @@ def main():
         comp_ms.append(ev0.elapsed_time(ev1))
     sweeps = cache.compress_sweeps() / 3.0
     status = cache.device_status()
+    if wl.rank_error > 0:
+        ranks_np, ranks_v_np = chosen_ranks(cache, kinds, max_pages, wl.rank_error)
     comp_ms_best = min(comp_ms)
     pages_per_s = n_fact / (comp_ms_best / 1e3)
     comp = compress_work(kinds, ranks_np, ranks_v_np, B, Hkv, P, d, sweeps)
@@ -315,8 +333,8 @@ def main():
             cache.append(layer, toks[s][0], toks[s][1], [pos] * B)
             if len(new_pages):
                 bb, hh, jj = zip(*[(b, h, int(j)) for b in range(B) for h in range(Hkv) for j in new_pages])
-                rr = [int(ranks_np[b, h, j]) for b, h, j in zip(bb, hh, jj)]
-                rv = [int(ranks_v_np[b, h, j]) for b, h, j in zip(bb, hh, jj)]
+                rr = [int(req_np[b, h, j]) for b, h, j in zip(bb, hh, jj)]
+                rv = [int(req_v_np[b, h, j]) for b, h, j in zip(bb, hh, jj)]
                 cache.compress_pages(layer, bb, hh, jj, rr, rv)
                 compress_calls += 1
             if timed:
@@ -346,6 +364,8 @@ def main():
     if not np.isfinite(out.float().cpu().numpy()).all():
         raise RuntimeError("non-finite attention output")
 
+    if wl.rank_error > 0:   # ranks of the pages compressed during the decode steps too
+        ranks_np, ranks_v_np = chosen_ranks(cache, pk.plan_pages(T + n_steps, P, S, W), max_pages, wl.rank_error)
     mid_T = T + args.warmup + args.steps // 2 + 1
     abytes = attention_bytes(cache, ranks_np, ranks_v_np, [mid_T] * B, P, d, B, Hkv, Hq, S, W)
     achieved = abytes / (attn_us * 1e-6) / 1e9
@@ -358,6 +378,8 @@ def main():
         "qwen32b_128k": "mixed-page decode attention time per decode step (64 layers, Qwen3-32B heads, 128K context)",
         "qwen8b_paper_default": "mixed-page decode attention time per decode step (36 layers, Qwen3-8B heads, "
                                 "16K context, pages of 32 tokens, (r_K, r_V) = (16, 14))",
+        "qwen32b_128k_adaptive": "mixed-page decode attention time per decode step (64 layers, Qwen3-32B "
+                                 "heads, 128K context, page ranks chosen for relative error 0.2)",
         "qwen32b_int4": "mixed-page decode attention time per decode step (INT4 factor pages, Qwen3-32B heads, "
                         "128K context, batch 8)",
     }
@@ -376,6 +398,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "batch": B, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d,
                    "page": P, "tokens": T, "sink": S, "window": W, "ranks": list(wl.ranks), "ranks_v": list(wl.ranks_v or wl.ranks),
+                   "rank_error": wl.rank_error,
                    "factor_storage": wl.factors,
                    "layers": layers, "step": "append + planner + compress-when-eligible + attention per layer"},
         "attention_us_per_layer": round(attn_us, 2),
@@ -395,7 +418,7 @@ def main():
         log("CPU baseline (oracle), budget %.0f s" % args.cpu_seconds)
         q0 = synth.queries(wl, args.seed, 0)
         result["cpu_baseline"] = cpu_baseline(wl, args.seed, T, K_dense, V_dense, q0, args.cpu_seconds,
-                                              layers)
+                                              layers, ranks_np, ranks_v_np)
     print(json.dumps(result), flush=True)
 
 

@@ -102,6 +102,25 @@ __device__ __forceinline__ int cq_group_min(int v) {
     return v;
 }
 
+// Adaptive rank from the group's column norms: with key the squared norm of
+// this lane's column and lam its eigenvalue of G, the smallest r whose r
+// largest eigenvalues leave |X|_F^2 - (their sum) <= eps2 |X|_F^2; P + 1 when
+// none does. Ties rank the lower lane first.
+template <int P>
+__device__ __forceinline__ int cq_adaptive_rank(float key, float lam, float xnorm2, float eps2, int c, int grp) {
+    float head = lam;   // energy of the columns ranked at or above this one
+    int above = 0;
+    for (int k = 0; k < P; ++k) {
+        const float kk = cq_group_bcast<P>(key, k, 32 + k, grp);
+        const float lk = cq_group_bcast<P>(lam, k, 32 + k, grp);
+        const bool up = kk > key || (kk == key && k < c);
+        head += up ? lk : 0.f;
+        above += up ? 1 : 0;
+    }
+    const bool ok = xnorm2 - head <= eps2 * xnorm2;
+    return cq_group_min<P>(ok ? above + 1 : P + 1);
+}
+
 // LDS floats per wavefront: R's row buffer (64), L staged as 64 x 32, inverse
 // singular values (64), the position -> token table (64); INT4 adds R~
 // (32 x d) and the scales ((P/32) r8 + d <= 64 + d).
@@ -118,25 +137,31 @@ __device__ __forceinline__ int cq_rank(float key, int c, int grp) {
     return rho;
 }
 
-// One workgroup per page: its K and V decompositions are two wavefronts at
-// P = 64 and the two halves of one wavefront at P = 32, so the pair can agree
-// on its ranks (adaptive ranks decide them here) before either stores.
-template <typename TF, int P>
-__global__ __launch_bounds__(128) void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor,
-                                                     CompressItems items, CompressSrc src, int64_t n_decomp) {
+// One wavefront per workgroup. kAdapt (a cache with adaptive ranks): a rank
+// of 0 asks for the rank chosen from the spectrum. The packed factor slot
+// places V's sections after K's rank, so the V decomposition of a page must
+// know K's rank before it stores: the two halves of the wavefront hold K and
+// V at P = 32, and at P = 64 the wavefront decomposes K, then V. With fixed
+// ranks every P = 64 decomposition is a wavefront of its own.
+template <typename TF, int P, bool kAdapt>
+__global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3)))
+void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor, CompressItems items, CompressSrc src,
+                   int64_t n_decomp) {
     static_assert(P == 32 || P == 64, "P = 32 or 64");
-    constexpr int D = 64 / P;          // decompositions per wave
-    constexpr int WPB = 2 / D;         // waves per workgroup
+    constexpr int D = 64 / P;                          // decompositions per pass
+    constexpr int kPasses = P == 64 && kAdapt ? 2 : 1;
     constexpr bool kQ4 = is_q4<TF>::value;
-    extern __shared__ float cq_lds[];
+    extern __shared__ float cq_smem[];
     const int d = g.d;
-    const int wave = threadIdx.x >> 6;
-    const int lane = threadIdx.x & 63;
-    float *cq_smem = cq_lds + wave * cq_wave_lds(d, kQ4);
+    const int lane = threadIdx.x;
     int *cq_tok = (int *)(cq_smem + 64 + 64 * 32 + 64);   // position -> token, per group
     const int grp = P == 64 ? 0 : lane >> 5;
     const int c = P == 64 ? lane : lane & 31;
-    const int64_t q = ((int64_t)blockIdx.x * WPB + wave) * D + grp;
+    int rk_first = 0;   // two passes: the K rank chosen by the first
+    for (int pass = 0; pass < kPasses; ++pass) {
+    // K and V of a page are decompositions 2i and 2i + 1 of the launch, so
+    // a pass is active exactly when the other one is
+    const int64_t q = ((int64_t)blockIdx.x * kPasses + pass) * D + grp;
 
     const DecompRef ref = decode_decomp<uint16_t>(g, table, dense, items, src, q, n_decomp, c == 0);
     const bool active = ref.active;
@@ -290,11 +315,15 @@ __global__ __launch_bounds__(128) void k_compress_qr(Geo g, pkv_page *table, con
     constexpr float kTolFactor = std::is_same<TF, uint16_t>::value ? 10.f : 1.f;
     const float tol = kTolFactor * (float)P * 1.1920929e-7f;
     const float stop_tol = sqrtf(tol);
-    // requested rank, 0 for a rank chosen from the spectrum (adaptive ranks):
-    // then the r_cap largest columns are converged
+    // requested rank, 0 for a rank chosen from the spectrum (adaptive ranks).
+    // Then each sweep estimates that rank from the current column norms, and
+    // the two columns after it are converged too (at most r_cap): a sweep
+    // that changes the estimate is never the last.
     const int r_req = ref.which == 0 ? ref.rk : ref.rv;
     const int r_cap = min(g.max_rank, min(P, d));
-    const int r_need = r_req > 0 ? r_req : r_cap;
+    const bool adaptive = kAdapt ? __any(r_req == 0) : false;
+    const float eps2 = g.rank_err * g.rank_err;
+    int r_need = r_req > 0 ? r_req : r_cap;
     // tag = top flag << 8 | column id: the id travels with the column, so
     // equal norms (zero columns) are ranked the same way wherever they sit
     float dsc = 1.f, alpha = 0.f;
@@ -396,8 +425,16 @@ __global__ __launch_bounds__(128) void k_compress_qr(Geo g, pkv_page *table, con
             larger = __float_as_int(li);
             for (int m = 16; m < 32; ++m) step(m);
         }
+        bool moved = false;
+        if (adaptive) {
+            const float a2 = fmaxf(alpha, 0.f);
+            const int est = cq_adaptive_rank<P>(a2, sqrtf(a2) * gnorm, xnorm2, eps2, c, grp);
+            const int rn = r_req > 0 ? r_req : min(r_cap, est + 2);
+            moved = rn != r_need;
+            r_need = rn;
+        }
         const int top_new = larger < r_need ? 1 : 0;
-        more = __any(rotated || top_new != (tag >> 8));   // converged only on a settled ranking
+        more = __any(rotated || moved || top_new != (tag >> 8));   // converged only on a settled ranking
         tag = (top_new << 8) | (tag & 255);
     }
     if (active && c == 0) {
@@ -422,15 +459,8 @@ __global__ __launch_bounds__(128) void k_compress_qr(Geo g, pkv_page *table, con
     // r largest eigenvalues of G) <= eps^2 |X|_F^2, capped at r_cap (only the
     // r_cap largest columns are converged, and only they enter the sums used).
     int r_own = r_req;
-    if (__any(r_req == 0)) {
-        float head = 0.f;   // energy of the columns ranked at or above this one
-        for (int k = 0; k < P; ++k) {
-            const float lk = cq_group_bcast<P>(lam, k, 32 + k, grp);
-            const int rk_ = __float_as_int(cq_group_bcast<P>(__int_as_float(rho), k, 32 + k, grp));
-            head += rk_ <= rho ? lk : 0.f;
-        }
-        const bool ok = xnorm2 - head <= g.rank_err * g.rank_err * xnorm2;
-        const int cand = cq_group_min<P>(ok ? rho + 1 : P + 1);
+    if (adaptive) {
+        const int cand = cq_adaptive_rank<P>(an2, lam, xnorm2, eps2, c, grp);
         if (r_req == 0) r_own = max(1, min(cand, r_cap));
     }
     {
@@ -492,11 +522,14 @@ __global__ __launch_bounds__(128) void k_compress_qr(Geo g, pkv_page *table, con
     // the page's K and V ranks (each chosen by its own half when adaptive)
     int rk, rv;
     if constexpr (P == 64) {
-        __shared__ int s_rank[2];
-        if (lane == 0) s_rank[wave] = r_own;   // wave 0 decomposes K, wave 1 V
-        __syncthreads();
-        rk = s_rank[0];
-        rv = s_rank[1];
+        if (kAdapt) {   // pass 0 decomposes K (its sections do not depend on rv), pass 1 V
+            if (pass == 0) rk_first = r_own;
+            rk = rk_first;
+            rv = r_own;
+        } else {
+            rk = ref.rk;
+            rv = ref.rv;
+        }
     } else {
         rk = __builtin_amdgcn_readlane(r_own, 0);    // lanes 0..31 decompose K, 32..63 V
         rv = __builtin_amdgcn_readlane(r_own, 32);
@@ -609,6 +642,7 @@ __global__ __launch_bounds__(128) void k_compress_qr(Geo g, pkv_page *table, con
             for (int a = 0; a < rv; ++a) st(Avt, (int64_t)a * P + t, sL[t * 32 + a]);
         }
     }
+    }   // passes
 }
 
 // Whether the matrix-core decomposition covers this geometry.
@@ -616,16 +650,23 @@ inline bool compress_qr_supported(const Geo &g) {
     return g.dense_dtype == PKV_BF16 && (g.P == 32 || g.P == 64) && g.d % 16 == 0 && g.d <= 256;
 }
 
+template <typename TF, int P, bool kAdapt>
+hipError_t launch_compress_qr_a(const LaunchCtx &L, const CompressItems &items, const CompressSrc &src,
+                                int64_t n_decomp) {
+    constexpr int per_wave = (64 / P) * (P == 64 && kAdapt ? 2 : 1);   // decompositions per wavefront
+    const size_t smem = (size_t)cq_wave_lds(L.geo.d, is_q4<TF>::value) * sizeof(float);
+    const int64_t blocks = ceil_div(n_decomp, (int64_t)per_wave);
+    LayerPtrs p = layer_ptrs(L);
+    hipLaunchKernelGGL((k_compress_qr<TF, P, kAdapt>), dim3((unsigned)blocks), dim3(64), smem, L.stream,
+                       L.geo, p.table, p.dense, p.factor, items, src, n_decomp);
+    return hipGetLastError();
+}
+
 template <typename TF, int P>
 hipError_t launch_compress_qr_t(const LaunchCtx &L, const CompressItems &items, const CompressSrc &src,
                                 int64_t n_decomp) {
-    constexpr int WPB = P == 64 ? 2 : 1;   // one page (K and V) per workgroup
-    const size_t smem = (size_t)WPB * cq_wave_lds(L.geo.d, is_q4<TF>::value) * sizeof(float);
-    const int64_t blocks = ceil_div(n_decomp, 2);
-    LayerPtrs p = layer_ptrs(L);
-    hipLaunchKernelGGL((k_compress_qr<TF, P>), dim3((unsigned)blocks), dim3(64 * WPB), smem, L.stream, L.geo,
-                       p.table, p.dense, p.factor, items, src, n_decomp);
-    return hipGetLastError();
+    return L.geo.rank_err > 0.f ? launch_compress_qr_a<TF, P, true>(L, items, src, n_decomp)
+                                : launch_compress_qr_a<TF, P, false>(L, items, src, n_decomp);
 }
 
 hipError_t launch_compress_qr(const LaunchCtx &L, const CompressItems &items, const CompressSrc &src,

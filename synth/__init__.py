@@ -50,7 +50,8 @@ class Workload:
     layers: int = 1
     decode_steps: int = 0
     factor_dtype: str = ""  # storage of factor pages when it differs from dtype ("int4")
-    ranks_v: tuple = ()     # rank choices of the value factors when they differ from the keys''' 
+    ranks_v: tuple = ()     # rank choices of the value factors when they differ from the keys
+    rank_error: float = 0.0  # > 0: each page's rank chosen for this relative reconstruction error
 
     @property
     def factors(self) -> str:
@@ -80,6 +81,10 @@ WORKLOADS = {
     # (W = P), 16K context, batch 1.
     "qwen8b_paper_default": Workload("qwen8b_paper_default", 6, 1, 8, 32, 128, 32, 16384, 32, 32, 24,
                                      (16,), "bf16", 1.0e6, 4, layers=36, ranks_v=(14,)),
+    # The 128K Qwen3-32B-shaped layer with each page's ranks chosen for 80%
+    # reconstruction accuracy (relative Frobenius error 0.2), at most 32.
+    "qwen32b_128k_adaptive": Workload("qwen32b_128k_adaptive", 7, 4, 8, 64, 128, 64, 131072, 64, 512, 24,
+                                      (32,), "bf16", 1.0e6, 4, layers=64, rank_error=0.2),
     # INT4 factors: Qwen3-32B heads, batch 8, T=128K.
     "qwen32b_int4": Workload("qwen32b_int4", 5, 8, 8, 64, 128, 64, 131072, 64, 512, 24,
                              (16, 24, 32), "bf16", 1.0e6, 4, factor_dtype="int4"),

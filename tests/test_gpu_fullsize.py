@@ -20,7 +20,7 @@ import pytest
 import oracle
 import synth
 from helpers import MAX_ABS, MEAN_REL, errors
-from test_gpu_compress import _check_factor
+from test_gpu_compress import _adaptive_ok, _check_factor
 
 pytestmark = pytest.mark.gpu
 
@@ -35,8 +35,11 @@ def _build(name):
     K, V = synth.kv_layer(wl, 0, 0, T, workers=16)
     ranks = synth.page_ranks(wl, 0, 0, max_pages)
     ranks_v = synth.page_ranks(wl, 0, 0, max_pages, "v")
+    if wl.rank_error > 0:          # rank 0: the decomposition chooses
+        ranks[:] = 0
+        ranks_v[:] = 0
     cache = pk.PuzzleKVCache(1, B, Hkv, Hq, d, P, max_pages, max(wl.ranks + wl.ranks_v), S, W, wl.dtype,
-                             wl.factors)
+                             wl.factors, adaptive_rank_error=wl.rank_error)
     kt = torch.from_numpy(K).to("cuda", torch.bfloat16)
     vt = torch.from_numpy(V).to("cuda", torch.bfloat16)
     rt = torch.from_numpy(ranks).cuda().contiguous()
@@ -64,6 +67,12 @@ def _run(name, heads, n_pages_checked):
     _, kind, rk, rv = cache.page_table_host(0)
     assert np.array_equal(kind[:, :, :n], np.broadcast_to(kinds, (B, Hkv, n)))
     fac = kinds == oracle.FACTOR
+    if wl.rank_error > 0:
+        # chosen ranks: within [1, cap] everywhere, checked against the
+        # oracle's singular values on the sampled heads below
+        for t in (rk, rv):
+            assert t[:, :, :n][:, :, fac].min() >= 1 and t[:, :, :n][:, :, fac].max() <= R
+        ranks, ranks_v = rk.astype(np.uint8), rv.astype(np.uint8)
     assert np.array_equal(rk[:, :, :n][:, :, fac], ranks[:, :, :n][:, :, fac])
     assert np.array_equal(rv[:, :, :n][:, :, fac], ranks_v[:, :, :n][:, :, fac])
     # one attention call over the whole batch, as bench.py makes it
@@ -99,6 +108,11 @@ def _run(name, heads, n_pages_checked):
         print("%s head (%d, %d): max-abs %.3e, normwise mean-relative %.3e" % (name, b, h, ma, mr))
         assert ma <= MAX_ABS and mr <= MEAN_REL, (b, h, ma, mr)
         assert np.abs(lse[b, h * g:(h + 1) * g] - rl).max() <= 1e-3
+        if wl.rank_error > 0:     # every factor page of this head: the chosen ranks
+            for j in np.flatnonzero(fac):
+                for X, rr in ((K[b, h, j * P:(j + 1) * P], rk[b, h, j]), (V[b, h, j * P:(j + 1) * P], rv[b, h, j])):
+                    s = np.linalg.svd(synth.round_bf16(X).astype(np.float64), compute_uv=False)
+                    assert _adaptive_ok(s, int(rr), wl.rank_error, R), (b, h, j, int(rr))
         # sampled decompositions of this head (bf16 factors; the INT4 path's
         # quantizer is checked against the oracle in test_gpu_int4)
         if wl.factors == "bf16":
@@ -115,6 +129,15 @@ def _run(name, heads, n_pages_checked):
 def test_fullsize_qwen32b_128k_bf16():
     """B=4, 64 q / 8 kv heads, d=128, P=64, T=131072, S=64, W=512, r in {16, 24, 32}."""
     checked = _run("qwen32b_128k", [(0, 0), (1, 5), (3, 7)], 4)
+    assert checked == 3 * 4 * 2
+
+
+def test_fullsize_qwen32b_128k_adaptive_ranks():
+    """The 128K layer with every page's ranks chosen by the decomposition for
+    relative Frobenius error 0.2 (cap 32): the chosen ranks of every factor
+    page of three heads against the oracle's singular values, attention and
+    sampled decompositions at those ranks."""
+    checked = _run("qwen32b_128k_adaptive", [(0, 0), (2, 3), (3, 7)], 4)
     assert checked == 3 * 4 * 2
 
 
