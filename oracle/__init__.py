@@ -62,7 +62,9 @@ def _load():
     lib.orc_adaptive_rank.restype = i32
     lib.orc_truncated_factors_batch.argtypes = [i32, i32, i32, p, p, p, p, i32, p, p, i32]
     lib.orc_truncated_factors_batch.restype = None
-    lib.orc_attention.argtypes = [i64, i32, i32, i32, i32, p, p, p, p, p, p, p, p]
+    lib.orc_attention.argtypes = [i64, i32, i32, i32, i32, p, p, p, p, p, p, dbl, p, p]
+    lib.orc_rope_rows.argtypes = [i32, i32, p, dbl, p]
+    lib.orc_rope_rows.restype = i32
     lib.orc_attention.restype = i32
     lib.orc_attention_pagewise.argtypes = [i64, i32, i32, i32, i32, p, p, p, p, p, p, p, i32,
                                            p, p]
@@ -169,16 +171,29 @@ def truncated_factors_batch(X: np.ndarray, ranks, max_sweeps: int = MAX_SWEEPS):
 # --------------------------------------------------------------------------
 # Attention (Eq. (1)) and page-wise state + merge (Eq. (4), Eq. (5))
 # --------------------------------------------------------------------------
+def rope_rows(X: np.ndarray, pos, base: float) -> np.ndarray:
+    """Rotate-half RoPE of the rows of X (n, d) at positions pos (n,), fp64
+    (Section 4.2; Appendix "RoPE Key Analysis")."""
+    Y = np.array(np.atleast_2d(X), dtype=np.float64, order="C")
+    pos = np.ascontiguousarray(np.broadcast_to(np.asarray(pos, dtype=np.int64), (Y.shape[0],)))
+    if _load().orc_rope_rows(Y.shape[0], Y.shape[1], _ptr(pos), float(base), _ptr(Y)) != 0:
+        raise ValueError("orc_rope_rows: d must be even and base > 0")
+    return Y
+
+
 class HeadCache:
     """Logical contents of one KV head: a list of pages.
 
     Each page is ("dense", K, V) with K, V of shape (P, d), or
     ("factor", L_K, R_K, L_V, R_V) with shapes (P, rk), (rk, d), (P, rv), (rv, d).
-    Rows past the sequence length in the last page are ignored."""
+    Rows past the sequence length in the last page are ignored. key_rope_base
+    > 0: the stored keys are pre-RoPE and the attention rotates key t to
+    position t before the scores."""
 
-    def __init__(self, T: int, P: int, d: int, pages):
+    def __init__(self, T: int, P: int, d: int, pages, key_rope_base: float = 0.0):
         self.T, self.P, self.d = int(T), int(P), int(d)
         self.pages = list(pages)
+        self.key_rope_base = float(key_rope_base)
 
     def pack(self):
         kind = np.zeros(len(self.pages), dtype=np.int32)
@@ -218,7 +233,8 @@ def attention(head: HeadCache, q: np.ndarray):
     kind, rk, rv, off, data = head.pack()
     out = np.empty((g, head.d)); lse = np.empty(g)
     rc = _load().orc_attention(head.T, head.P, head.d, g, len(head.pages), _ptr(kind), _ptr(rk),
-                               _ptr(rv), _ptr(off), _ptr(data), _ptr(q), _ptr(out), _ptr(lse))
+                               _ptr(rv), _ptr(off), _ptr(data), _ptr(q), head.key_rope_base, _ptr(out),
+                               _ptr(lse))
     if rc != 0:
         raise ValueError("orc_attention failed (%d)" % rc)
     return out, lse
@@ -227,6 +243,8 @@ def attention(head: HeadCache, q: np.ndarray):
 def attention_pagewise(head: HeadCache, q: np.ndarray, order=None, group: int = 0):
     """Eq. (4) page states merged by Eq. (5), pages visited in `order`, merged in
     groups of `group` visited pages first. Returns (out, lse)."""
+    if head.key_rope_base > 0:
+        raise ValueError("the factor-form evaluation of Eq. (4) needs post-RoPE keys")
     q = np.ascontiguousarray(np.atleast_2d(q), dtype=np.float64)
     g = q.shape[0]
     kind, rk, rv, off, data = head.pack()

@@ -20,7 +20,14 @@
  *       Section 3.3, Eq. (2)).
  *   orc_attention
  *       textbook softmax(q K^T / sqrt(d)) V over the cache rebuilt page by
- *       page from its stored form (Section 3.2, Eq. (1)).
+ *       page from its stored form (Section 3.2, Eq. (1)); for a cache that
+ *       stores keys before RoPE, every rebuilt key row is first rotated to
+ *       its absolute position (orc_rope_rows).
+ *   orc_rope_rows
+ *       rotary position embedding of key rows, rotate-half pairing: the
+ *       paper factorizes post-RoPE keys by default and compares factorizing
+ *       pre-RoPE keys with RoPE applied at cache access (Section 4.2 "Main
+ *       Results"; Appendix "RoPE Key Analysis").
  *   orc_attention_pagewise
  *       the page-local softmax state of Eq. (4) evaluated directly from the
  *       factors, merged by the online-softmax reduction of Eq. (5) in a caller
@@ -270,9 +277,38 @@ static void rebuild_page(int P, int d, int kind, int rk, int rv, const double *s
     }
 }
 
+/* Rotary position embedding in place, rotate-half pairing. Row t of X (an   */
+/* n x d matrix) is the key at position pos[t]. Dimension i < d/2 pairs with */
+/* i + d/2, at frequency theta_i = base^(-2i/d): the pair (x_i, x_{i+d/2})    */
+/* is rotated by the angle pos * theta_i,                                    */
+/*   x_i       <- x_i cos(a) - x_{i+d/2} sin(a)                              */
+/*   x_{i+d/2} <- x_{i+d/2} cos(a) + x_i sin(a).                             */
+/* Angles, sines and cosines in fp64 (libm).                                 */
+int orc_rope_rows(int n, int d, const long long *pos, double base, double *X)
+{
+    if (d % 2 != 0 || !(base > 0.0)) return -1;
+    const int h = d / 2;
+    for (int t = 0; t < n; ++t) {
+        double *x = X + (size_t)t * d;
+        for (int i = 0; i < h; ++i) {
+            const double theta = pow(base, -2.0 * (double)i / (double)d);
+            const double a = (double)pos[t] * theta;
+            const double c = cos(a), s = sin(a);
+            const double x0 = x[i], x1 = x[i + h];
+            x[i] = x0 * c - x1 * s;
+            x[i + h] = x1 * c + x0 * s;
+        }
+    }
+    return 0;
+}
+
+/* key_rope_base > 0: the stored keys are pre-RoPE; each rebuilt key row t   */
+/* is rotated to position t (orc_rope_rows) before the scores. 0: keys are   */
+/* used as stored.                                                           */
 int orc_attention(long long T, int P, int d, int g, int n_pages, const int *kind,
                   const int *rank_k, const int *rank_v, const long long *off,
-                  const double *data, const double *q, double *out, double *lse)
+                  const double *data, const double *q, double key_rope_base,
+                  double *out, double *lse)
 {
     if (T <= 0) return -1;
     double *Kh = (double *)malloc(sizeof(double) * (size_t)T * d);
@@ -291,6 +327,15 @@ int orc_attention(long long T, int P, int d, int g, int n_pages, const int *kind
                      Kh + (size_t)t0 * d, Vh + (size_t)t0 * d);
     }
     if (bad || (long long)n_pages * P < T) { free(Kh); free(Vh); free(s); return -3; }
+    if (key_rope_base > 0.0) {
+        int rbad = 0;
+        #pragma omp parallel for schedule(static) reduction(|:rbad)
+        for (long long t = 0; t < T; ++t) {
+            const long long pos = t;
+            rbad |= orc_rope_rows(1, d, &pos, key_rope_base, Kh + (size_t)t * d) != 0;
+        }
+        if (rbad) { free(Kh); free(Vh); free(s); return -4; }
+    }
 
     const double scale = 1.0 / sqrt((double)d);
     for (int i = 0; i < g; ++i) {

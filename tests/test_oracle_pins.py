@@ -513,3 +513,81 @@ def test_adaptive_rank_meets_the_bound_by_brute_force(eps):
         if r > 1:
             L1, R1, _, _ = oracle.truncated_factors(X, r - 1)
             assert np.linalg.norm(X - L1 @ R1) > eps * np.linalg.norm(X)
+
+
+# --------------------------------------------------------------------------
+# Pre-RoPE keys: rotary position embedding at cache access
+# --------------------------------------------------------------------------
+def test_rope_is_a_complex_multiplication():
+    """RoPE read as in its original formulation: the pair (x_i, x_{i+d/2}) is
+    the complex number x_i + j x_{i+d/2}, multiplied by exp(j pos theta_i)
+    with theta_i = base^(-2i/d). Computed here with numpy's complex
+    exponential, a different route from the oracle's real rotation, so a
+    wrong sign, pairing or frequency fails."""
+    rng = np.random.default_rng(31)
+    d, base = 16, 1.0e4
+    X = rng.standard_normal((7, d))
+    pos = np.array([0, 1, 5, 100, 4097, 65536, 131071])
+    Y = oracle.rope_rows(X, pos, base)
+    h = d // 2
+    theta = np.power(base, -np.arange(h) * 2.0 / d)
+    z = (X[:, :h] + 1j * X[:, h:]) * np.exp(1j * pos[:, None] * theta[None, :])
+    np.testing.assert_allclose(Y[:, :h], z.real, rtol=0, atol=1e-12)
+    np.testing.assert_allclose(Y[:, h:], z.imag, rtol=0, atol=1e-12)
+
+
+def test_rope_closed_forms_and_invariants():
+    """d = 2 has the single frequency 1: the unit key e_0 at position t
+    becomes (cos t, sin t). Position 0 is the identity, every pair keeps its
+    norm, and the score of two rotated vectors depends only on the distance
+    of their positions (the relative-position property of RoPE)."""
+    Y = oracle.rope_rows(np.array([[1.0, 0.0]] * 4), [0, 1, 2, 100], 1.0e6)
+    t = np.array([0.0, 1.0, 2.0, 100.0])
+    np.testing.assert_allclose(Y, np.stack([np.cos(t), np.sin(t)], 1), atol=1e-14)
+    rng = np.random.default_rng(32)
+    d = 128
+    x = rng.standard_normal((3, d))
+    np.testing.assert_array_equal(oracle.rope_rows(x, 0, 5e5), x)
+    y = oracle.rope_rows(x, [3, 777, 120000], 5e5)
+    np.testing.assert_allclose(np.hypot(y[:, :64], y[:, 64:]), np.hypot(x[:, :64], x[:, 64:]), rtol=1e-13)
+    q, k = rng.standard_normal(d), rng.standard_normal(d)
+    s1 = oracle.rope_rows(q, 40, 1e6)[0] @ oracle.rope_rows(k, 1000, 1e6)[0]
+    s2 = oracle.rope_rows(q, 40 + 90000, 1e6)[0] @ oracle.rope_rows(k, 1000 + 90000, 1e6)[0]
+    s3 = q @ oracle.rope_rows(k, 960, 1e6)[0]
+    assert abs(s1 - s2) < 1e-9 and abs(s1 - s3) < 1e-9
+
+
+def test_attention_pre_rope_full_rank_equals_dense_over_rotated_keys():
+    """A cache of pre-RoPE keys (dense pages and full-rank factor pages),
+    attended with RoPE at access, equals plain attention over a dense cache
+    whose keys were rotated beforehand by the complex form above: this pins
+    that key t of page j sits at position j P + t."""
+    rng = np.random.default_rng(33)
+    P, d, g, base = 8, 16, 3, 1.0e4
+    T = 5 * P + 3
+    n = -(-T // P)
+    h = d // 2
+    theta = np.power(base, -np.arange(h) * 2.0 / d)
+    K = rng.standard_normal((n * P, d))
+    V = rng.standard_normal((n * P, d))
+    pos = np.arange(n * P)
+    z = (K[:, :h] + 1j * K[:, h:]) * np.exp(1j * pos[:, None] * theta[None, :])
+    Krot = np.concatenate([z.real, z.imag], 1)
+    pre, post = [], []
+    for j in range(n):
+        Kp, Vp = K[j * P:(j + 1) * P], V[j * P:(j + 1) * P]
+        post.append(("dense", Krot[j * P:(j + 1) * P], Vp))
+        if j in (1, 2, 3):
+            Lk, Rk, _, _ = oracle.truncated_factors(Kp, P)
+            Lv, Rv, _, _ = oracle.truncated_factors(Vp, P)
+            pre.append(("factor", Lk, Rk, Lv, Rv))
+        else:
+            pre.append(("dense", Kp, Vp))
+    q = rng.standard_normal((g, d))
+    o1, l1 = oracle.attention(oracle.HeadCache(T, P, d, pre, key_rope_base=base), q)
+    o2, l2 = oracle.attention(oracle.HeadCache(T, P, d, post), q)
+    np.testing.assert_allclose(o1, o2, rtol=0, atol=1e-11)
+    np.testing.assert_allclose(l1, l2, rtol=0, atol=1e-11)
+    # and the rotation matters: without it the result differs
+    o3, _ = oracle.attention(oracle.HeadCache(T, P, d, pre), q)
+    assert np.abs(o3 - o2).max() > 1e-3
