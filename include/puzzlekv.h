@@ -95,6 +95,9 @@ typedef struct {
  *   B_Vt = R_V^T        d  x r4(rv) row-major (columns >= rv are zero)
  *   A_Vt = L_V^T        rv x P      row-major
  * for e * (P r4(rk) + rk d + rv P + d r4(rv)) bytes (pkv_factor_page_bytes).
+ * A cache of pre-RoPE keys (key_rope_base > 0) stores B_Kt = R_K^T,
+ * d x r4(rk) row-major (columns >= rk zero), in place of B_K, for
+ * e * (P r4(rk) + d r4(rk) + rv P + d r4(rv)) bytes.
  * Every operand is stored with its contraction index contiguous, the order
  * the attention kernel streams it in.
  *
@@ -136,6 +139,19 @@ typedef struct {
      * eps = 0.2). K and V choose independently; the chosen ranks are written
      * to the page table. Needs bf16 dense pages with P = 32 or 64. */
     float adaptive_rank_error;
+    /* Keys stored before RoPE: 0 (off: keys are used as stored, the usual
+     * post-RoPE cache) or the RoPE base. When set, every cached key (k rows
+     * given to pkv_prefill and pkv_append_kv, dense pages, and the pages
+     * pkv_compress_pages factorizes) is the pre-RoPE key, and attention
+     * rotates key t of a sequence to position t before its score, with the
+     * rotate-half pairing: dims i < d/2 and i + d/2 form a pair rotated by
+     * t * base^(-2i/d). Queries are given already rotated. The paper
+     * factorizes post-RoPE keys and compares factorizing pre-RoPE keys with
+     * RoPE applied at cache access (Section 4.2 "Main Results"; Appendix
+     * "RoPE Key Analysis"). Factor slots then hold R_K transposed (B_Kt
+     * above). Needs bf16 dense pages and factors, P = 32 or 64, head_dim =
+     * 64 or 128, max_rank <= 32 and positions below 2^24. */
+    float key_rope_base;
 } pkv_cache;
 
 /* ---- geometry and sizing (host only, no device work) -------------------- */

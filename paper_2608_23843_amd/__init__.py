@@ -74,7 +74,7 @@ class PuzzleKVCache:
 
     def __init__(self, n_layers, batch, n_kv_heads, n_q_heads, head_dim, page_size, max_pages,
                  max_rank, sink_tokens, window_tokens, dense_dtype="bf16", factor_dtype="bf16",
-                 device="cuda", adaptive_rank_error=0.0):
+                 device="cuda", adaptive_rank_error=0.0, key_rope_base=0.0):
         import torch
         self.torch = torch
         self.lib = _lib.load()
@@ -84,6 +84,7 @@ class PuzzleKVCache:
         c.sink_tokens, c.window_tokens = sink_tokens, window_tokens
         c.dense_dtype, c.factor_dtype = _DTYPES[dense_dtype], _DTYPES[factor_dtype]
         c.adaptive_rank_error = float(adaptive_rank_error)   # > 0: rank requests of 0 are chosen per page
+        c.key_rope_base = float(key_rope_base)               # > 0: keys cached before RoPE
         self.c = c
         self.device = torch.device(device)
         lib = self.lib

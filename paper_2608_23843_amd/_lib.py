@@ -40,7 +40,7 @@ class PkvCache(ctypes.Structure):
         ("window_tokens", ctypes.c_int32), ("dense_dtype", ctypes.c_int32),
         ("factor_dtype", ctypes.c_int32), ("dense_pool", ctypes.c_void_p),
         ("factor_pool", ctypes.c_void_p), ("page_table", ctypes.c_void_p),
-        ("adaptive_rank_error", ctypes.c_float),
+        ("adaptive_rank_error", ctypes.c_float), ("key_rope_base", ctypes.c_float),
     ]
 
 

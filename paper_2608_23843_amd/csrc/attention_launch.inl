@@ -39,6 +39,7 @@ hipError_t launch_attention(const LaunchCtx &L, const AttnPlan &plan, const void
     const Geo &g = L.geo;
     const Partials pp = make_partials(ws, (int64_t)g.B * g.Hkv, plan.n_chunks, g.g, g.d);
     if (plan.use_mfma) return launch_attn_mfma(L, plan, (const uint16_t *)q, seq, pp, out, lse);
+    if (g.key_t) return hipErrorInvalidValue;   // pre-RoPE keys: matrix-core kernel only
     const bool db = g.dense_dtype == PKV_BF16, fb = g.factor_dtype == PKV_BF16;
     if (db && fb) launch_generic<uint16_t, uint16_t>(L, p, plan, q, seq, pp, out, lse);
     else if (db) launch_generic<uint16_t, float>(L, p, plan, q, seq, pp, out, lse);

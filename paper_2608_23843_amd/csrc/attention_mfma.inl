@@ -22,6 +22,16 @@
 // transposed. The normalizer is a fifth product, ones x E^T, so it needs no
 // per-token additions.
 //
+// Caches of pre-RoPE keys (ROPE): a factor page's keys are rebuilt on the
+// matrix cores and rotated before the scores, since RoPE does not commute
+// with the factorization. K^T = R_K^T L_K^T (M = dim, K = rank, N = token,
+// R_K^T stored d x r4) comes out with lane (n, q) holding token n and dims
+// 8q..8q+7 of each 32-dim chunk over a pair of dim tiles (the rank-tile map
+// read as a dim map), which is the A operand layout of S^T = K Q^T. The
+// rotate-half pairs (i, i + d/2) sit in the same lane, so the rotation needs
+// no data movement; the rotated keys enter S^T as a bf16 hi/lo pair. Dense
+// keys are rotated the same way from their bf16 operands.
+//
 // Factor operands are read with buffer loads, one resource per section of the
 // slot sized to that section: rank rows past the page's rank fall outside it
 // and read as zero, which also zeroes the matching entries of Z and Y, so the
@@ -129,6 +139,8 @@ struct ValueOps {
 struct PageRes {
     __amdgpu_buffer_rsrc_t ak, bk, bvt, avt;
     int rk, rv, rk4, rv4;
+    int kst;   // ROPE: elements per row of the bk section (d for dense K, r4(rk) for R_K^T)
+    int kcs;   // ROPE: byte step of one 32-dim chunk (64 along a dense K row, 32 rows of R_K^T)
 };
 struct LaneOffs {
     uint32_t bk[2], av[2];   // R_K / L_V^T row rank_row(rt, n), chunk q
@@ -146,10 +158,12 @@ struct Unit {
 template <int P>
 __device__ constexpr int dense_unit_tokens() { return P < 32 ? P : 32; }
 
-template <int D, int P>
+template <int D, int P, bool ROPE = false>
 __device__ inline PageRes unit_res(const char *factor, int64_t fslot_bytes, const char *dense, int64_t dslot_bytes,
                                    const Unit &u) {
     PageRes r;
+    r.kst = D;
+    r.kcs = 64;
     if (u.e.kind == PKV_DENSE) {
         // K rows of the unit feed the R_K registers (the same rank_row lane
         // map serves as the token map of two 16-row tiles), V^T columns of
@@ -170,7 +184,11 @@ __device__ inline PageRes unit_res(const char *factor, int64_t fslot_bytes, cons
     r.rv = is_f ? u.e.rank_v : 0;
     r.rk4 = r4(r.rk);
     r.rv4 = r4(r.rv);
-    const FactorLayout fl = factor_layout(P, D, r.rk, r.rv);
+    if (ROPE) {
+        r.kst = r.rk4;
+        r.kcs = 64 * r.rk4;
+    }
+    const FactorLayout fl = factor_layout(P, D, r.rk, r.rv, ROPE);
     const char *base = factor + (is_f ? u.e.slot : 0) * fslot_bytes;
     r.ak = section_rsrc(base, (uint32_t)(2 * fl.bk));
     r.bk = section_rsrc(base + 2 * fl.bk, (uint32_t)(2 * (fl.bvt - fl.bk)));
@@ -179,12 +197,23 @@ __device__ inline PageRes unit_res(const char *factor, int64_t fslot_bytes, cons
     return r;
 }
 
-template <int D, int P>
+template <int D, int P, bool ROPE = false>
 __device__ inline void issue_key_loads(KeyOps<D, P> &f, const PageRes &r, const LaneOffs &lo, int n, int q) {
+    if constexpr (ROPE) {
+        // dense K: row rank_row(rt, n), columns 32 s + 8q..8q+7 (row length d);
+        // R_K^T: row 32 s + rank_row(rt, n), columns 8q..8q+7 (row length r4(rk))
 #pragma unroll
-    for (int rt = 0; rt < 2; ++rt)
+        for (int rt = 0; rt < 2; ++rt) {
+            const uint32_t vb = 2u * ((uint32_t)rank_row(rt, n) * (uint32_t)r.kst + 8u * q);
 #pragma unroll
-        for (int s = 0; s < D / 32; ++s) f.bk[rt][s] = bld8(r.bk, lo.bk[rt] + 64u * s, 0u);
+            for (int s = 0; s < D / 32; ++s) f.bk[rt][s] = bld8(r.bk, vb, (uint32_t)s * (uint32_t)r.kcs);
+        }
+    } else {
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt)
+#pragma unroll
+            for (int s = 0; s < D / 32; ++s) f.bk[rt][s] = bld8(r.bk, lo.bk[rt] + 64u * s, 0u);
+    }
     const uint32_t v_ak = 2u * (lo.tok0 * r.rk4 + 8 * q);
 #pragma unroll
     for (int tt = 0; tt < P / 16; ++tt) {
@@ -299,6 +328,107 @@ __device__ inline void unit_phase1(WaveState<D> &w, const KeyOps<D, P> &f, const
     page_softmax<D, P, false>(w, st, eh, el, P, q, c2);
 }
 
+// Rotation of frequency i at position t (rotate-half RoPE): the angle
+// t theta_i in revolutions, t w_i with w_i = theta_i / 2 pi held as
+// wh + wl; the product t wh is split exactly (fma) so that its integer part
+// drops out before the hardware sine and cosine, which take revolutions.
+__device__ inline void rope_cs(float t, float wh, float wl, float &c, float &s) {
+    const float p = t * wh;
+    const float e = fmaf(t, wh, -p);
+    const float r = __builtin_amdgcn_fractf(p) + fmaf(t, wl, e);
+    c = __builtin_amdgcn_cosf(r);
+    s = __builtin_amdgcn_sinf(r);
+}
+
+// Rotates the pairs (x[s][u], x[s + D/64][u]) of one lane's key row at
+// position t, x[s][u] being dim 32 s + 8 q + u (rw: wh[D/2] then wl[D/2]).
+template <int D>
+__device__ inline void rope_row(float (&x)[D / 32][8], float t, int q, const float *rw) {
+#pragma unroll
+    for (int s = 0; s < D / 64; ++s)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+            const int i0 = 32 * s + 8 * q + 4 * h;
+            const f32x4 wh = *(const f32x4 *)(rw + i0);
+            const f32x4 wl = *(const f32x4 *)(rw + D / 2 + i0);
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                float c, sn;
+                rope_cs(t, wh[v], wl[v], c, sn);
+                const float a = x[s][4 * h + v], b = x[s + D / 64][4 * h + v];
+                x[s][4 * h + v] = a * c - b * sn;
+                x[s + D / 64][4 * h + v] = fmaf(b, c, a * sn);
+            }
+        }
+}
+
+// Phase 1 of a unit of a pre-RoPE cache. Factor page: per token tile,
+// K^T = R_K^T L_K^T, rotation, S^T = K Q^T; rank entries at or past r4(rk)
+// of the L_K operand are zeroed (the R_K^T operand holds the next row's
+// values there). Dense unit: the K rows are rotated, then S^T = K Q^T.
+// t0: position of the unit's first token.
+template <int D, int P>
+__device__ inline void unit_phase1_rope(WaveState<D> &w, const KeyOps<D, P> &f, const bf16x8 (&qb)[D / 32],
+                                        bool dense, int rows, bf16x8 (&eh)[(P + 31) / 32],
+                                        bf16x8 (&el)[(P + 31) / 32], int n, int q, float c2, int64_t t0, int rk4,
+                                        const float *rw) {
+    if (dense) {
+        f32x4 z[2];
+#pragma unroll
+        for (int rt = 0; rt < 2; ++rt) {
+            float x[D / 32][8];
+#pragma unroll
+            for (int s = 0; s < D / 32; ++s)
+#pragma unroll
+                for (int u = 0; u < 8; ++u) x[s][u] = (float)f.bk[rt][s][u];
+            rope_row<D>(x, (float)(t0 + rank_row(rt, n)), q, rw);
+            z[rt] = zero_f4();
+#pragma unroll
+            for (int s = 0; s < D / 32; ++s) {
+                uint32_t hd[4], ld[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) split2(x[s][2 * u], x[s][2 * u + 1], hd[u], ld[u]);
+                z[rt] = mfma_bf16(__builtin_bit_cast(bf16x8, u32x4{hd[0], hd[1], hd[2], hd[3]}), qb[s], z[rt]);
+                z[rt] = mfma_bf16(__builtin_bit_cast(bf16x8, u32x4{ld[0], ld[1], ld[2], ld[3]}), qb[s], z[rt]);
+            }
+        }
+        bf16x8 eh1[1], el1[1];
+        page_softmax<D, 32, true>(w, z, eh1, el1, rows, q, c2);
+        eh[0] = eh1[0];
+        el[0] = el1[0];
+        return;
+    }
+    const bool m_lo = 8 * q < rk4, m_hi = 8 * q + 4 < rk4;
+    f32x4 st[P / 16];
+#pragma unroll
+    for (int tt = 0; tt < P / 16; ++tt) {
+        u32x4 am = __builtin_bit_cast(u32x4, f.ak[tt]);
+        if (!m_lo) am[0] = am[1] = 0u;
+        if (!m_hi) am[2] = am[3] = 0u;
+        const bf16x8 a = __builtin_bit_cast(bf16x8, am);
+        float x[D / 32][8];
+#pragma unroll
+        for (int s = 0; s < D / 32; ++s)
+#pragma unroll
+            for (int hp = 0; hp < 2; ++hp) {
+                const f32x4 kt = mfma_bf16(f.bk[hp][s], a, zero_f4());
+#pragma unroll
+                for (int v = 0; v < 4; ++v) x[s][4 * hp + v] = kt[v];
+            }
+        rope_row<D>(x, (float)(t0 + token_row<P>(tt, n)), q, rw);
+        st[tt] = zero_f4();
+#pragma unroll
+        for (int s = 0; s < D / 32; ++s) {
+            uint32_t hd[4], ld[4];
+#pragma unroll
+            for (int u = 0; u < 4; ++u) split2(x[s][2 * u], x[s][2 * u + 1], hd[u], ld[u]);
+            st[tt] = mfma_bf16(__builtin_bit_cast(bf16x8, u32x4{hd[0], hd[1], hd[2], hd[3]}), qb[s], st[tt]);
+            st[tt] = mfma_bf16(__builtin_bit_cast(bf16x8, u32x4{ld[0], ld[1], ld[2], ld[3]}), qb[s], st[tt]);
+        }
+    }
+    page_softmax<D, P, false>(w, st, eh, el, P, q, c2);
+}
+
 // Phase 2 of a unit. Factor page: Y^T = L_V^T E^T, O^T += R_V^T Y^T. Dense
 // unit: O^T += V^T E^T with the unit's V^T columns in the R_V^T registers;
 // columns at or past `rows` may hold anything, so they are zeroed.
@@ -362,7 +492,7 @@ __device__ inline pkv_page unpack_entry(uint2 ent) {
 // with page i+1's while phase 2 of page i reads the value operands, refilled
 // in turn with page i+1's. One operand set per wave keeps the register budget
 // at two waves per SIMD.
-template <int D, int P, bool Q4>
+template <int D, int P, bool Q4, bool ROPE = false>
 __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, const pkv_page *__restrict__ table,
                                                                   const char *__restrict__ dense,
                                                                   const char *__restrict__ factor,
@@ -548,6 +678,22 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
     // at once. So all waves arrive at the same number of barriers, whatever
     // mix of factor pages and multi-unit dense pages each one streams.
     __shared__ unsigned int s_blk[4];
+    // pre-RoPE keys: w_i = theta_i / 2 pi = base^(-2i/d) / 2 pi as wh + wl
+    // (fp64 on the way), i < d/2, shared by the workgroup
+    const float *rw = nullptr;
+    if constexpr (ROPE) {
+        __shared__ float s_rw[D];
+        if (threadIdx.x < D / 2) {
+            const int i = (int)threadIdx.x;
+            const double th = exp2(-(2.0 * i / D) * log2((double)g.rope_base));
+            const double wv = th * 0.15915494309189533577;   // 1 / (2 pi)
+            const float wh = (float)wv;
+            s_rw[i] = wh;
+            s_rw[D / 2 + i] = (float)(wv - (double)wh);
+        }
+        __syncthreads();
+        rw = s_rw;
+    }
     int round = 0;
     bool blocks_done = false;
     // Wave 0's block claim is issued at the top of a loop iteration and read
@@ -665,12 +811,18 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
     Unit nxt = next_unit(needs_blk() ? issue_blk() : 0u);
     while (cur.e.kind != PKV_EMPTY || nxt.e.kind != PKV_EMPTY) {
         const unsigned int pre = needs_blk() ? issue_blk() : 0u;
-        const PageRes nres = unit_res<D, P>(factor, g.factor_slot_bytes, dense, g.dense_slot_bytes, nxt);
+        const PageRes nres = unit_res<D, P, ROPE>(factor, g.factor_slot_bytes, dense, g.dense_slot_bytes, nxt);
         bf16x8 eh[KS], el[KS];
         const int rows = unit_rows(cur);
         const bool live = cur.e.kind != PKV_EMPTY, dns = cur.e.kind == PKV_DENSE;
-        if (live) unit_phase1<D, P>(w, ko, qb, dns, rows, eh, el, q4, c2);
-        issue_key_loads<D, P>(ko, nres, lo, n, q4);
+        if (live) {
+            if constexpr (ROPE)
+                unit_phase1_rope<D, P>(w, ko, qb, dns, rows, eh, el, n, q4, c2,
+                                       cur.j * P + (int64_t)UT * cur.half, r4(cur.e.rank_k), rw);
+            else
+                unit_phase1<D, P>(w, ko, qb, dns, rows, eh, el, q4, c2);
+        }
+        issue_key_loads<D, P, ROPE>(ko, nres, lo, n, q4);
         if (live) unit_phase2<D, P>(w, vo, dns, rows, eh, el, q4);
         issue_value_loads<D, P>(vo, nres, lo, n, q4);
         cur = nxt;
@@ -734,7 +886,18 @@ hipError_t launch_attn_mfma(const LaunchCtx &L, const AttnPlan &plan, const uint
 #define PKV_LAUNCH_MFMA(DD, PP)                                                                         \
     hipLaunchKernelGGL((k_attn_mfma<DD, PP, false>), grid, dim3(64 * kMfmaWaves), 0, L.stream, g, p.table,   \
                        p.dense, p.factor, q, seq, plan.pages_per_chunk, plan.n_chunks, pp, out, lse)
-    if (g.factor_dtype == PKV_INT4) {
+#define PKV_LAUNCH_MFMA_ROPE(DD, PP)                                                                    \
+    hipLaunchKernelGGL((k_attn_mfma<DD, PP, false, true>), grid, dim3(64 * kMfmaWaves), 0, L.stream, g,      \
+                       p.table, p.dense, p.factor, q, seq, plan.pages_per_chunk, plan.n_chunks, pp, out, lse)
+    if (g.key_t) {   // pre-RoPE keys (validated on the host: d = 64/128, P = 32/64)
+        if (g.d == 128) {
+            if (g.P == 64) PKV_LAUNCH_MFMA_ROPE(128, 64);
+            else PKV_LAUNCH_MFMA_ROPE(128, 32);
+        } else {
+            if (g.P == 64) PKV_LAUNCH_MFMA_ROPE(64, 64);
+            else PKV_LAUNCH_MFMA_ROPE(64, 32);
+        }
+    } else if (g.factor_dtype == PKV_INT4) {
         hipLaunchKernelGGL((k_attn_mfma<128, 64, true>), grid, dim3(64 * kMfmaWavesQ4), 0, L.stream, g, p.table,
                            p.dense, p.factor, q, seq, plan.pages_per_chunk, plan.n_chunks, pp, out, lse);
     } else if (g.d == 128) {
@@ -747,6 +910,7 @@ hipError_t launch_attn_mfma(const LaunchCtx &L, const AttnPlan &plan, const uint
         else PKV_LAUNCH_MFMA(64, 16);
     }
 #undef PKV_LAUNCH_MFMA
+#undef PKV_LAUNCH_MFMA_ROPE
     return hipGetLastError();
 }
 

@@ -241,14 +241,21 @@ __global__ __launch_bounds__(256) void k_import(Geo g, pkv_page *table, char *de
     const TF *Lv = Rk + (int64_t)rk * d;
     const TF *Rv = Lv + (int64_t)P * rv;
     const int slot = (int)(head * g.max_pages + it.j);
-    const FactorLayout fl = factor_layout(P, d, rk, rv);
+    const FactorLayout fl = factor_layout(P, d, rk, rv, g.key_t != 0);
     TF *Ak = (TF *)(factor + slot * g.factor_slot_bytes);
     TF *Bk = Ak + fl.bk, *Bvt = Ak + fl.bvt, *Avt = Ak + fl.avt;
     for (int i = threadIdx.x; i < P * rk4; i += blockDim.x) {
         int t = i / rk4, a = i % rk4;
         Ak[i] = a < rk ? Lk[t * rk + a] : TF(0);
     }
-    for (int i = threadIdx.x; i < rk * d; i += blockDim.x) Bk[i] = Rk[i];
+    if (g.key_t) {   // R_K^T, d x r4(rk)
+        for (int i = threadIdx.x; i < d * rk4; i += blockDim.x) {
+            int k = i / rk4, a = i % rk4;
+            Bk[i] = a < rk ? Rk[(int64_t)a * d + k] : TF(0);
+        }
+    } else {
+        for (int i = threadIdx.x; i < rk * d; i += blockDim.x) Bk[i] = Rk[i];
+    }
     for (int i = threadIdx.x; i < rv * P; i += blockDim.x) {
         int a = i / P, t = i % P;
         Avt[i] = Lv[t * rv + a];
@@ -307,7 +314,7 @@ __global__ __launch_bounds__(256) void k_export(Geo g, const pkv_page *table, co
         return;
     }
     const int rk = e.rank_k, rv = e.rank_v, rk4 = r4(rk), rv4 = r4(rv);
-    const FactorLayout fl = factor_layout(P, d, rk, rv);
+    const FactorLayout fl = factor_layout(P, d, rk, rv, g.key_t != 0);
     const TF *Ak = (const TF *)(factor + e.slot * g.factor_slot_bytes);
     const TF *Bk = Ak + fl.bk, *Bvt = Ak + fl.bvt, *Avt = Ak + fl.avt;
     float *Lk = o, *Rk = Lk + P * R, *Lv = Rk + R * d, *Rv = Lv + P * R;
@@ -318,7 +325,7 @@ __global__ __launch_bounds__(256) void k_export(Geo g, const pkv_page *table, co
     }
     for (int i = threadIdx.x; i < R * d; i += blockDim.x) {
         int a = i / d, k = i % d;
-        Rk[i] = a < rk ? ld(Bk, i) : 0.f;
+        Rk[i] = a < rk ? ld(Bk, g.key_t ? (int64_t)k * rk4 + a : (int64_t)i) : 0.f;
         Rv[i] = a < rv ? ld(Bvt, (int64_t)k * rv4 + a) : 0.f;
     }
     for (int i = 2 * (P + d) * R + threadIdx.x; i < block; i += blockDim.x) o[i] = 0.f;

@@ -363,6 +363,7 @@ hipError_t launch_compress_any(const LaunchCtx &L, const CompressItems &items, c
                                int64_t n_decomp) {
     if (n_decomp <= 0) return hipSuccess;
     if (compress_qr_supported(L.geo)) return launch_compress_qr(L, items, src, n_decomp);
+    if (L.geo.key_t) return hipErrorInvalidValue;   // R_K^T slots: stored by the matrix-core kernel only
     if (L.geo.factor_dtype == PKV_INT4) {   // validated: bf16 dense pages, P = 64
         if (L.geo.P != 64 || L.geo.dense_dtype != PKV_BF16) return hipErrorInvalidValue;
         return launch_compress_t<uint16_t, q4_t, 64>(L, items, src, n_decomp);

@@ -602,9 +602,17 @@ void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor, Comp
                 for (int a = 0; a < 32; ++a) sR[a * d + k + u] = acc[u][a] * sInvSig[a];
         } else {
             const int rk4 = r4(rk), rv4 = r4(rv);
-            const FactorLayout fl = factor_layout(P, d, rk, rv);
+            const FactorLayout fl = factor_layout(P, d, rk, rv, g.key_t != 0);
             TF *Ak = (TF *)(factor + slot_off);
-            if (which == 0) {
+            if (which == 0 && g.key_t) {
+                TF *Bkt = Ak + fl.bk;                      // R_K^T, d x r4(rk), zero past rk
+#pragma unroll
+                for (int a = 0; a < 32; ++a)
+                    if (a < rk4) {
+                        st(Bkt, (int64_t)k * rk4 + a, acc[0][a]);
+                        st(Bkt, (int64_t)(k + 1) * rk4 + a, acc[1][a]);
+                    }
+            } else if (which == 0) {
                 TF *Bk = Ak + fl.bk;                       // R_K, rk x d
 #pragma unroll
                 for (int a = 0; a < 32; ++a)
@@ -631,7 +639,7 @@ void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor, Comp
         q4_quantize_store(factor + slot_off, f4, P, d, r, which, sL, sR, sScale, lane);
     } else {
         // L: A_K = L_K (P x r4(rk), zero past rk) row by row, A_V^T = L_V^T (rv x P)
-        const FactorLayout fl = factor_layout(P, d, rk, rv);
+        const FactorLayout fl = factor_layout(P, d, rk, rv, g.key_t != 0);
         TF *Ak = (TF *)(factor + slot_off);
         const int t = c;
         if (which == 0) {

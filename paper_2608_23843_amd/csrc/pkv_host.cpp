@@ -58,6 +58,16 @@ pkv_status check_geometry(const pkv_cache *c) {
         return fail(PKV_E_ARG, "adaptive_rank_error %g outside [0, 1)", (double)c->adaptive_rank_error);
     if (c->adaptive_rank_error > 0.f && (c->dense_dtype != PKV_BF16 || (c->page_size != 32 && c->page_size != 64)))
         return fail(PKV_E_UNSUPPORTED, "adaptive ranks need bf16 dense pages with P = 32 or 64");
+    if (!(c->key_rope_base >= 0.f && c->key_rope_base < INFINITY))
+        return fail(PKV_E_ARG, "key_rope_base %g: must be 0 (off) or a positive finite base", (double)c->key_rope_base);
+    if (c->key_rope_base > 0.f) {
+        if (c->dense_dtype != PKV_BF16 || c->factor_dtype != PKV_BF16 || (c->page_size != 32 && c->page_size != 64) ||
+            (c->head_dim != 64 && c->head_dim != 128) || c->max_rank > 32)
+            return fail(PKV_E_UNSUPPORTED, "pre-RoPE keys need bf16 dense pages and factors, P = 32 or 64, "
+                                           "head_dim = 64 or 128 and max_rank <= 32");
+        if ((int64_t)c->max_pages * c->page_size > (1 << 24))
+            return fail(PKV_E_UNSUPPORTED, "pre-RoPE keys: positions must stay below 2^24");
+    }
     if (c->factor_dtype == PKV_INT4) {
         if (c->dense_dtype != PKV_BF16 || c->page_size != 64 || c->head_dim != 128 || c->max_rank > 32)
             return fail(PKV_E_UNSUPPORTED,
@@ -73,13 +83,13 @@ pkv_status check_geometry(const pkv_cache *c) {
 
 // Stored bytes of one factor page pair (codes and scales for INT4); a slot
 // adds the INT4 pad.
-int64_t factor_page_bytes_of(int dtype, int P, int d, int rk, int rv) {
+int64_t factor_page_bytes_of(int dtype, int P, int d, int rk, int rv, bool kt) {
     if (dtype == PKV_INT4) return int4_layout(P, d, rk, rv).pad;
-    return factor_page_elems(P, d, rk, rv) * elem_size(dtype);
+    return factor_page_elems(P, d, rk, rv, kt) * elem_size(dtype);
 }
-int64_t factor_slot_bytes_of(int dtype, int P, int d, int r) {
+int64_t factor_slot_bytes_of(int dtype, int P, int d, int r, bool kt) {
     if (dtype == PKV_INT4) return int4_layout(P, d, r, r).end;
-    return factor_page_bytes_of(dtype, P, d, r, r);
+    return factor_page_bytes_of(dtype, P, d, r, r, kt);
 }
 
 Geo make_geo(const pkv_cache *c) {
@@ -93,6 +103,8 @@ Geo make_geo(const pkv_cache *c) {
     g.max_pages = c->max_pages;
     g.max_rank = c->max_rank;
     g.rank_err = c->adaptive_rank_error;
+    g.rope_base = c->key_rope_base;
+    g.key_t = c->key_rope_base > 0.f ? 1 : 0;
     g.S = c->sink_tokens;
     g.W = c->window_tokens;
     g.sink_pages = (int)ceil_div(c->sink_tokens, c->page_size);
@@ -103,7 +115,7 @@ Geo make_geo(const pkv_cache *c) {
     g.dense_dtype = c->dense_dtype;
     g.factor_dtype = c->factor_dtype;
     g.dense_slot_bytes = 2LL * g.P * g.d * g.dense_es;
-    int64_t fb = factor_slot_bytes_of(c->factor_dtype, g.P, g.d, g.max_rank);
+    int64_t fb = factor_slot_bytes_of(c->factor_dtype, g.P, g.d, g.max_rank, g.key_t != 0);
     g.factor_slot_bytes = (fb + 255) / 256 * 256;
     g.layer_entries = (int64_t)g.B * g.Hkv * g.max_pages;
     g.layer_dense_bytes = (int64_t)g.B * g.Hkv * g.dslots * g.dense_slot_bytes;
@@ -185,7 +197,8 @@ size_t pkv_page_table_bytes(const pkv_cache *c) {
 size_t pkv_factor_page_bytes(const pkv_cache *c, int32_t rank_k, int32_t rank_v) {
     if (check_geometry(c) != PKV_OK) return 0;
     if (rank_k < 1 || rank_v < 1 || rank_k > c->max_rank || rank_v > c->max_rank) return 0;
-    return (size_t)factor_page_bytes_of(c->factor_dtype, c->page_size, c->head_dim, rank_k, rank_v);
+    return (size_t)factor_page_bytes_of(c->factor_dtype, c->page_size, c->head_dim, rank_k, rank_v,
+                                        c->key_rope_base > 0.f);
 }
 int64_t pkv_int4_blob_bytes(const pkv_cache *c, int32_t rank_k, int32_t rank_v) {
     if (check_geometry(c) != PKV_OK || c->factor_dtype != PKV_INT4) return -1;

@@ -16,23 +16,25 @@ constexpr int kCopyItemsPerLaunch = 64;
 __host__ __device__ inline int r4(int r) { return (r + 3) & ~3; }
 __host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-// Elements of a packed factor page pair at ranks (rk, rv).
-__host__ __device__ inline int64_t factor_page_elems(int P, int d, int rk, int rv) {
-    return (int64_t)P * r4(rk) + (int64_t)rk * d + (int64_t)rv * P + (int64_t)d * r4(rv);
+// Elements of a packed factor page pair at ranks (rk, rv). kt: R_K stored
+// transposed, d x r4(rk) (caches of pre-RoPE keys).
+__host__ __device__ inline int64_t factor_page_elems(int P, int d, int rk, int rv, bool kt = false) {
+    return (int64_t)P * r4(rk) + (int64_t)(kt ? r4(rk) : rk) * d + (int64_t)rv * P + (int64_t)d * r4(rv);
 }
 
 // Section starts (in elements) of a factor slot holding ranks (rk, rv):
-// A_K = L_K (P x r4(rk)), B_K = R_K (rk x d), B_Vt = R_V^T (d x r4(rv)),
-// A_Vt = L_V^T (rv x P), packed in that order. A_Vt comes last because its
-// reads past rank rv are the ones that must stop at the page's end.
+// A_K = L_K (P x r4(rk)), B_K = R_K (rk x d) or, with kt, B_Kt = R_K^T
+// (d x r4(rk)), B_Vt = R_V^T (d x r4(rv)), A_Vt = L_V^T (rv x P), packed in
+// that order. A_Vt comes last because its reads past rank rv are the ones
+// that must stop at the page's end.
 struct FactorLayout {
     int64_t ak, bk, bvt, avt, end;
 };
-__host__ __device__ inline FactorLayout factor_layout(int P, int d, int rk, int rv) {
+__host__ __device__ inline FactorLayout factor_layout(int P, int d, int rk, int rv, bool kt = false) {
     FactorLayout f;
     f.ak = 0;
     f.bk = (int64_t)P * r4(rk);
-    f.bvt = f.bk + (int64_t)rk * d;
+    f.bvt = f.bk + (int64_t)(kt ? r4(rk) : rk) * d;
     f.avt = f.bvt + (int64_t)d * r4(rv);
     f.end = f.avt + (int64_t)rv * P;
     return f;
@@ -98,6 +100,8 @@ __host__ __device__ inline int plan_kind(int64_t T, int P, int S, int W, int64_t
 struct Geo {
     int B, Hkv, Hq, g, d, P, max_pages, max_rank;
     float rank_err;                           // adaptive ranks: eps, or 0 (off)
+    float rope_base;                          // keys stored before RoPE: its base, or 0 (off)
+    int key_t;                                // R_K stored transposed (rope_base > 0)
     int S, W, sink_pages, ring_len, dslots;   // dslots = dense slots per head
     int dense_es, factor_es;                  // element sizes in bytes
     int dense_dtype, factor_dtype;

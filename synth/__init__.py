@@ -52,6 +52,7 @@ class Workload:
     factor_dtype: str = ""  # storage of factor pages when it differs from dtype ("int4")
     ranks_v: tuple = ()     # rank choices of the value factors when they differ from the keys
     rank_error: float = 0.0  # > 0: each page's rank chosen for this relative reconstruction error
+    key_rope: bool = False   # keys handed over before RoPE (the cache rotates them at access)
 
     @property
     def factors(self) -> str:
@@ -85,6 +86,10 @@ WORKLOADS = {
     # reconstruction accuracy (relative Frobenius error 0.2), at most 32.
     "qwen32b_128k_adaptive": Workload("qwen32b_128k_adaptive", 7, 4, 8, 64, 128, 64, 131072, 64, 512, 24,
                                       (32,), "bf16", 1.0e6, 4, layers=64, rank_error=0.2),
+    # The 128K Qwen3-32B-shaped layer with keys cached before RoPE: the same
+    # page model without the rotation; attention rotates keys at access.
+    "qwen32b_128k_prerope": Workload("qwen32b_128k_prerope", 8, 4, 8, 64, 128, 64, 131072, 64, 512, 24,
+                                     (16, 24, 32), "bf16", 1.0e6, 4, layers=64, key_rope=True),
     # INT4 factors: Qwen3-32B heads, batch 8, T=128K.
     "qwen32b_int4": Workload("qwen32b_int4", 5, 8, 8, 64, 128, 64, 131072, 64, 512, 24,
                              (16, 24, 32), "bf16", 1.0e6, 4, factor_dtype="int4"),
@@ -173,7 +178,7 @@ def kv_head(wl: Workload, seed: int, layer: int, b: int, h: int, tokens: int | N
     ch = outlier_channels(wl, seed, layer, h)
     if ch.size:
         K[:, ch] *= np.float32(10.0)
-    if wl.rope_base is not None:
+    if wl.rope_base is not None and not wl.key_rope:
         K = _rope(K, wl.rope_base)
     return round_storage(K[:T], wl.dtype), round_storage(V[:T], wl.dtype)
 
@@ -247,7 +252,8 @@ def factor_page(wl: Workload, seed: int, layer: int, b: int, h: int, j: int, r_k
 def decode_kv(wl: Workload, seed: int, layer: int, pos: int):
     """K and V rows (batch, kv_heads, d) for the token at position pos, drawn
     from the same page model as the prefill pages but from their own stream
-    (one stream per decode position), with the key outliers and RoPE at pos."""
+    (one stream per decode position), with the key outliers and RoPE at pos
+    (no RoPE for a workload that hands keys over before it)."""
     P, d = wl.page, wl.head_dim
     K = np.empty((wl.batch, wl.kv_heads, d), dtype=np.float32)
     V = np.empty_like(K)
@@ -260,7 +266,7 @@ def decode_kv(wl: Workload, seed: int, layer: int, pos: int):
             ch = outlier_channels(wl, seed, layer, h)
             if ch.size:
                 K[b, h, ch] *= 10.0
-    if wl.rope_base is not None:
+    if wl.rope_base is not None and not wl.key_rope:
         half = d // 2
         inv = wl.rope_base ** (-np.arange(half, dtype=np.float64) * 2.0 / d)
         c, s = np.cos(pos * inv), np.sin(pos * inv)

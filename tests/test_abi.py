@@ -171,3 +171,37 @@ def test_rank_zero_requests_need_adaptive_ranks(pk):
     assert lib.pkv_compress_pages(ca, 0, 2, P(i32(0, 0)), P(i32(1, 1)), P(i32(3, 3)), P(u8(0, 0)),
                                   P(u8(0, 0)), None, 0, None) == 1      # duplicate page
     assert lib.pkv_compress_pages(ca, 0, 2, P(b), P(h), P(j), P(u8(33, 0)), P(u8(0, 0)), None, 0, None) == 3
+
+
+@pytest.mark.parametrize("kw,code", [(dict(key_rope_base=-1.0), 1), (dict(key_rope_base=float("inf")), 1),
+                                     (dict(key_rope_base=float("nan")), 1),
+                                     (dict(key_rope_base=1e6, dense_dtype=0, factor_dtype=0), 6),
+                                     (dict(key_rope_base=1e6, factor_dtype=2), 6),
+                                     (dict(key_rope_base=1e6, page_size=16, max_rank=16), 6),
+                                     (dict(key_rope_base=1e6, head_dim=256), 6),
+                                     (dict(key_rope_base=1e6, max_pages=(1 << 18) + 1), 6)])
+def test_pre_rope_geometry_errors(pk, kw, code):
+    """Pre-RoPE keys: the base must be 0 or positive and finite, and the
+    geometry one the matrix-core kernels rotate (bf16, P = 32/64, d = 64/128,
+    positions below 2^24)."""
+    lib = pk.load_library()
+    c = _cache(pk, **kw)
+    c.dense_pool = c.factor_pool = c.page_table = 0x1000
+    assert lib.pkv_cache_check(c) == code
+    assert lib.pkv_last_error()
+
+
+def test_pre_rope_slot_holds_r_k_transposed(pk):
+    """With keys cached before RoPE, R_K is stored as d x r4(rk): the page
+    size grows by (r4(rk) - rk) d elements, and the slot is sized for it."""
+    lib = pk.load_library()
+    P, d = 64, 128
+    r4 = lambda r: (r + 3) // 4 * 4
+    c0 = _cache(pk, max_rank=30)
+    c1 = _cache(pk, max_rank=30, key_rope_base=1e6)
+    for rk, rv in [(16, 16), (13, 22), (30, 1)]:
+        b0 = lib.pkv_factor_page_bytes(c0, rk, rv)
+        b1 = lib.pkv_factor_page_bytes(c1, rk, rv)
+        assert b0 == 2 * (P * r4(rk) + rk * d + rv * P + d * r4(rv))
+        assert b1 == 2 * (P * r4(rk) + r4(rk) * d + rv * P + d * r4(rv))
+    assert lib.pkv_factor_slot_bytes(c1) >= 2 * (P * 32 + 32 * d + 30 * P + d * 32)
