@@ -182,7 +182,7 @@ def cpu_baseline(wl, seed, seq_T, K_dense, V_dense, q, budget_s, layers, ranks, 
                 pages[j] = ("factor",) + tuple(
                     q4.dequantize_lines(e[c + "_codes"], e[c + "_scales"], q4.AXIS[c + "_" + w])
                     for e, w in ((ek, "K"), (ev, "V")) for c in ("L", "R"))
-            head = oracle.HeadCache(seq_T, P, d, pages)
+            head = oracle.HeadCache(seq_T, P, d, pages, key_rope_base=wl.rope_base if wl.key_rope else 0.0)
             oracle.attention(head, q[b, h * g:(h + 1) * g].astype(np.float64))
             times.append(time.time() - t)
             heads.append((b, h))
@@ -195,10 +195,10 @@ def cpu_baseline(wl, seed, seq_T, K_dense, V_dense, q, budget_s, layers, ranks, 
     us_step = per_head * n_heads * layers * 1e6
     return {
         "value": us_step, "unit": "us/step", "cores": oracle.num_threads(), "kind": "oracle",
-        "sample": "%d of %d (sequence, KV head) heads of one layer at T=%d (fp64 %srebuild + softmax), "
+        "sample": "%d of %d (sequence, KV head) heads of one layer at T=%d (fp64 %srebuild + %ssoftmax), "
                   "%.2f s per head, extrapolated x%d heads x%d layers"
-                  % (len(times), n_heads, seq_T, "INT4 dequantization + " if int4 else "", per_head, n_heads,
-                     layers),
+                  % (len(times), n_heads, seq_T, "INT4 dequantization + " if int4 else "",
+                     "key RoPE + " if wl.key_rope else "", per_head, n_heads, layers),
     }
 
 
@@ -256,8 +256,9 @@ def main():
     ranks = torch.from_numpy(ranks_np).cuda().contiguous()
     ranks_v = torch.from_numpy(ranks_v_np).cuda().contiguous()
 
+    rope_base = wl.rope_base if wl.key_rope else 0.0   # > 0: keys cached before RoPE
     cache = pk.PuzzleKVCache(layers, B, Hkv, Hq, d, P, max_pages, max_rank, S, W, wl.dtype, wl.factors,
-                             adaptive_rank_error=wl.rank_error)
+                             adaptive_rank_error=wl.rank_error, key_rope_base=rope_base)
     log("cache: factor pool %.1f GB, dense pool %.2f GB" % (cache.factor_pool.numel() / 1e9,
                                                             cache.dense_pool.numel() / 1e9))
 
@@ -380,6 +381,8 @@ def main():
                                 "16K context, pages of 32 tokens, (r_K, r_V) = (16, 14))",
         "qwen32b_128k_adaptive": "mixed-page decode attention time per decode step (64 layers, Qwen3-32B "
                                  "heads, 128K context, page ranks chosen for relative error 0.2)",
+        "qwen32b_128k_prerope": "mixed-page decode attention time per decode step (64 layers, Qwen3-32B "
+                                "heads, 128K context, keys cached before RoPE and rotated at access)",
         "qwen32b_int4": "mixed-page decode attention time per decode step (INT4 factor pages, Qwen3-32B heads, "
                         "128K context, batch 8)",
     }
@@ -398,7 +401,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": wl.name, "batch": B, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d,
                    "page": P, "tokens": T, "sink": S, "window": W, "ranks": list(wl.ranks), "ranks_v": list(wl.ranks_v or wl.ranks),
-                   "rank_error": wl.rank_error,
+                   "rank_error": wl.rank_error, "keys_before_rope": wl.key_rope,
                    "factor_storage": wl.factors,
                    "layers": layers, "step": "append + planner + compress-when-eligible + attention per layer"},
         "attention_us_per_layer": round(attn_us, 2),

@@ -39,7 +39,8 @@ def _build(name):
         ranks[:] = 0
         ranks_v[:] = 0
     cache = pk.PuzzleKVCache(1, B, Hkv, Hq, d, P, max_pages, max(wl.ranks + wl.ranks_v), S, W, wl.dtype,
-                             wl.factors, adaptive_rank_error=wl.rank_error)
+                             wl.factors, adaptive_rank_error=wl.rank_error,
+                             key_rope_base=wl.rope_base if wl.key_rope else 0.0)
     kt = torch.from_numpy(K).to("cuda", torch.bfloat16)
     vt = torch.from_numpy(V).to("cuda", torch.bfloat16)
     rt = torch.from_numpy(ranks).cuda().contiguous()
@@ -102,7 +103,7 @@ def _run(name, heads, n_pages_checked):
                 pages.append(("factor", Lk, Rk, Lv, Rv))
             else:
                 pages.append(("dense", o[:P * d].reshape(P, d), o[P * d:2 * P * d].reshape(P, d)))
-        head = oracle.HeadCache(T, P, d, pages)
+        head = oracle.HeadCache(T, P, d, pages, key_rope_base=wl.rope_base if wl.key_rope else 0.0)
         ro, rl = oracle.attention(head, q[b, h * g:(h + 1) * g].astype(np.float64))
         ma, mr = errors(out[b, h * g:(h + 1) * g], ro)
         print("%s head (%d, %d): max-abs %.3e, normwise mean-relative %.3e" % (name, b, h, ma, mr))
@@ -138,6 +139,14 @@ def test_fullsize_qwen32b_128k_adaptive_ranks():
     page of three heads against the oracle's singular values, attention and
     sampled decompositions at those ranks."""
     checked = _run("qwen32b_128k_adaptive", [(0, 0), (2, 3), (3, 7)], 4)
+    assert checked == 3 * 4 * 2
+
+
+def test_fullsize_qwen32b_128k_pre_rope():
+    """The 128K layer with keys cached before RoPE (rotated at access, base
+    1e6): attention of three heads against the oracle's fp64 rotation, and
+    sampled decompositions of the pre-RoPE pages."""
+    checked = _run("qwen32b_128k_prerope", [(0, 0), (1, 6), (3, 2)], 4)
     assert checked == 3 * 4 * 2
 
 
