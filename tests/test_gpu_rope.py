@@ -47,6 +47,8 @@ def _check(cache, q, seq, plan_of, rk, rv, P, d, R, G, label):
     lse = lse.cpu().numpy().astype(np.float64)
     worst = 0.0
     for b, T in enumerate(seq):
+        if T == 0:   # empty sequences are checked by the caller
+            continue
         n = -(-T // P)
         for h in range(cache.c.n_kv_heads):
             pages = _pages_from_export(cache, b, h, n, plan_of(T, n), rk, rv, P, d, R)
@@ -179,3 +181,40 @@ def test_pre_rope_decode_steps_with_compression():
     _, _, rk, rv = cache.page_table_host(0)
     q = synth.queries(wl, 0, 3)
     _check(cache, q, [T] * B, lambda Tb, n: oracle.plan_pages(Tb, P, S, W, n), rk, rv, P, d, 32, G, "decode")
+
+
+def test_pre_rope_with_adaptive_ranks():
+    """Both variants at once: pre-RoPE keys whose ranks the decomposition
+    chooses for relative error 0.2 (R_K^T stored at the chosen rank, padded to
+    a multiple of 4), then attention with the rotation at access; also an
+    empty sequence in the batch (output 0, lse -inf)."""
+    import torch
+    import paper_2608_23843_amd as pk
+    from test_gpu_compress import _adaptive_ok
+    d, P, G, B, Hkv, S, W = 128, 64, 8, 2, 2, 64, 128
+    T = [P * 9 + 33, 0]
+    npg = -(-T[0] // P)
+    wl = synth.Workload("rope_ad", 98, B, Hkv, Hkv * G, d, P, T[0], S, W, 24, (24,), "bf16", BASE, 4,
+                        key_rope=True)
+    K, V = synth.kv_layer(wl, 0, 0, npg * P)
+    R, eps = 32, 0.2
+    cache = pk.PuzzleKVCache(1, B, Hkv, Hkv * G, d, P, npg, R, S, W, "bf16", "bf16", adaptive_rank_error=eps,
+                             key_rope_base=BASE)
+    cache.prefill(0, torch.from_numpy(K).to("cuda", torch.bfloat16).contiguous(),
+                  torch.from_numpy(V).to("cuda", torch.bfloat16).contiguous(), T, default_rank=(0, 0))
+    torch.cuda.synchronize()
+    assert cache.device_status() == 0
+    _, kind, rk, rv = cache.page_table_host(0)
+    plan = oracle.plan_pages(T[0], P, S, W, npg)
+    for h in range(Hkv):
+        for j in np.flatnonzero(plan == oracle.FACTOR):
+            for X, r in ((K[0, h, j * P:(j + 1) * P], rk[0, h, j]), (V[0, h, j * P:(j + 1) * P], rv[0, h, j])):
+                _, s, _, _ = oracle.svd_rows(X.astype(np.float64))
+                assert _adaptive_ok(s, int(r), eps, R), (h, j, int(r))
+    q = synth.queries(wl, 0, 0)
+    out, lse = cache.attention(0, torch.from_numpy(q).to("cuda", torch.bfloat16).contiguous(), T)
+    torch.cuda.synchronize()
+    o1 = out[1].cpu().numpy()
+    assert np.all(o1 == 0) and np.all(np.isneginf(lse[1].cpu().numpy()))
+    _check(cache, q, T, lambda Tb, n: oracle.plan_pages(Tb, P, S, W, n), rk, rv, P, d, R, G,
+           "pre-RoPE + adaptive")
