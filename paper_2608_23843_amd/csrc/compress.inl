@@ -156,9 +156,8 @@ __global__ __launch_bounds__(64) void k_compress(Geo g, pkv_page *table, const c
     for (int k = 0; k < P; ++k) gcol[k] *= ginv;
     // Rotation threshold P 2^-23 on the cosine of two columns; for factors
     // stored in bf16 ten times that (two sweeps fewer of ~12, the rank-r
-    // reconstruction moving by ~1e-4 |X|, far below bf16 rounding). fp32 and
-    // INT4 factors keep the tight threshold, so an INT4 page quantizes
-    // exactly the factors an fp32 page of the same input stores.
+    // reconstruction moving by ~1e-4 |X|, far below bf16 rounding). fp32
+    // factors keep the tight threshold.
     constexpr float kTolFactor = std::is_same<TF, uint16_t>::value ? 10.f : 1.f;
     const float tol = kTolFactor * (float)P * 1.1920929e-7f;
     const float tiny2 = fro2 > 0.f ? tol * tol : 0.f;  // relative to |G|_F^2 = 1
@@ -260,36 +259,6 @@ __global__ __launch_bounds__(64) void k_compress(Geo g, pkv_page *table, const c
 
     if (!active) return;
 
-    if constexpr (is_q4<TF>::value) {
-        // ---- INT4 outputs (Section 4.3): balance by Sigma^(1/2), quantize --------
-        // sigma = sqrt(lambda); L~ column = L column * sigma^(1/2), R~ row =
-        // R row / sigma^(1/2) (zero where sigma is zero), staged in LDS after X.
-        float *sL = (float *)(sX_all + (int64_t)P * ld_x);   // P x 32
-        float *sR = sL + P * 32;                              // 32 x d
-        float *sScale = sR + 32 * d;                          // (P/32) r8 + d <= 64 + d
-        const int r = which == 0 ? rk : rv;
-        const float root = sqrtf(sqrtf(fmaxf(lam, 0.f)));
-        const float inv = root > 0.f ? 1.f / root : 0.f;
-        if (rho < r)
-            for (int t = 0; t < P; ++t) sL[t * 32 + rho] = jcol[t] * root;
-        for (int k0 = 0; k0 < d; k0 += 16) {
-            float acc[16];
-#pragma unroll
-            for (int u = 0; u < 16; ++u) acc[u] = 0.f;
-            for (int t = 0; t < P; ++t) {
-                const float lt = jcol[t];
-#pragma unroll
-                for (int u = 0; u < 16; ++u) acc[u] = fmaf(lt, to_f32(sX[t * ld_x + k0 + u]), acc[u]);
-            }
-            if (rho < r)
-#pragma unroll
-                for (int u = 0; u < 16; ++u) sR[rho * d + k0 + u] = acc[u] * inv;
-        }
-        __syncthreads();
-        const Int4Layout f4 = int4_layout(P, d, rk, rv);
-        char *slot4 = factor + (g.head_index(b, h) * g.max_pages + j) * g.factor_slot_bytes;
-        q4_quantize_store(slot4, f4, P, d, r, which, sL, sR, sScale, lane);
-    } else {
     // ---- outputs ------------------------------------------------------------
     const int rk4 = r4(rk), rv4 = r4(rv);
     const FactorLayout fl = factor_layout(P, d, rk, rv);
@@ -325,7 +294,6 @@ __global__ __launch_bounds__(64) void k_compress(Geo g, pkv_page *table, const c
         }
     }
     (void)r; (void)rr4;
-    }
 }
 
 template <typename TX, typename TF, int P>
@@ -334,7 +302,6 @@ hipError_t launch_compress_t(const LaunchCtx &L, const CompressItems &items, con
     constexpr int D = 64 / P;
     const int pad = sizeof(TX) == 2 ? 2 : 1;
     size_t smem = (size_t)D * P * (L.geo.d + pad) * sizeof(TX);
-    if (is_q4<TF>::value) smem += (size_t)(P * 32 + 32 * L.geo.d + 64 + L.geo.d) * sizeof(float);
     const int64_t blocks = ceil_div(n_decomp, D);
     LayerPtrs p = layer_ptrs(L);
     hipLaunchKernelGGL((k_compress<TX, TF, P>), dim3((unsigned)blocks), dim3(64), smem, L.stream, L.geo,
@@ -364,10 +331,9 @@ hipError_t launch_compress_any(const LaunchCtx &L, const CompressItems &items, c
     if (n_decomp <= 0) return hipSuccess;
     if (compress_qr_supported(L.geo)) return launch_compress_qr(L, items, src, n_decomp);
     if (L.geo.key_t) return hipErrorInvalidValue;   // R_K^T slots: stored by the matrix-core kernel only
-    if (L.geo.factor_dtype == PKV_INT4) {   // validated: bf16 dense pages, P = 64
-        if (L.geo.P != 64 || L.geo.dense_dtype != PKV_BF16) return hipErrorInvalidValue;
-        return launch_compress_t<uint16_t, q4_t, 64>(L, items, src, n_decomp);
-    }
+    // INT4 caches are validated to bf16 pages of 64 tokens with d = 128: the
+    // matrix-core kernel above always takes them
+    if (L.geo.factor_dtype == PKV_INT4) return hipErrorInvalidValue;
     const bool db = L.geo.dense_dtype == PKV_BF16, fb = L.geo.factor_dtype == PKV_BF16;
     if (db && fb) return launch_compress_p<uint16_t, uint16_t>(L, items, src, n_decomp);
     if (db) return launch_compress_p<uint16_t, float>(L, items, src, n_decomp);

@@ -122,9 +122,9 @@ __device__ __forceinline__ int cq_adaptive_rank(float key, float lam, float xnor
 }
 
 // LDS floats per wavefront: R's row buffer (64), L staged as 64 x 32, inverse
-// singular values (64), the position -> token table (64); INT4 adds R~
-// (32 x d) and the scales ((P/32) r8 + d <= 64 + d).
-__host__ __device__ inline int cq_wave_lds(int d, bool q4) { return 64 + 64 * 32 + 64 + 64 + (q4 ? 32 * d + 64 + d : 0); }
+// singular values (64), the position -> token table (64); INT4 adds R~'s
+// codes (32 x d bytes) and L~'s scales ((P/32) r8 or P <= 64).
+__host__ __device__ inline int cq_wave_lds(int d, bool q4) { return 64 + 64 * 32 + 64 + 64 + (q4 ? 8 * d + 64 : 0); }
 
 // Rank of `key` among the P lanes of the group: descending, ties to the lower lane.
 template <int P>
@@ -558,7 +558,9 @@ void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor, Comp
 
     const int64_t slot_off = (g.head_index(ref.b, ref.h) * g.max_pages + ref.j) * g.factor_slot_bytes;
     constexpr int kCols = 2;                      // dims per lane per pass
-    float *sR = cq_smem + 64 + 64 * 32 + 64 + 64;   // INT4 only: 32 x d (P = 64: one group per wave)
+    int8_t *sRc = (int8_t *)(cq_smem + 64 + 64 * 32 + 64 + 64);   // INT4 only: R~ codes (P = 64: one group per wave)
+    Int4Layout f4{};
+    if constexpr (kQ4) f4 = int4_layout(P, d, rk, rv);
     for (int k0 = 0; k0 < d; k0 += kCols * P) {
         const int k = k0 + kCols * c;
         const bool kin = k < d;
@@ -595,11 +597,28 @@ void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor, Comp
         }
         if (!kin) continue;
         if constexpr (kQ4) {
-            // R~ = Sigma^(-1/2) R: the accumulation used L~ = L Sigma^(1/2), so divide by sigma
+            // R~ = Sigma^(-1/2) R: the accumulation used L~ = L Sigma^(1/2), so
+            // divide by sigma. R~'s scales run down a column (one dim, all
+            // ranks), which this lane holds: its scale goes to the slot and
+            // its codes to LDS (K: [rank][dim], V: [dim][rank]) for packing.
 #pragma unroll
-            for (int u = 0; u < kCols; ++u)
+            for (int u = 0; u < kCols; ++u) {
+                float amax = 0.f;
 #pragma unroll
-                for (int a = 0; a < 32; ++a) sR[a * d + k + u] = acc[u][a] * sInvSig[a];
+                for (int a = 0; a < 32; ++a) {
+                    acc[u][a] *= sInvSig[a];
+                    if (a < r) amax = fmaxf(amax, fabsf(acc[u][a]));
+                }
+                const uint16_t hs = f16_rne((double)amax / (double)kQ4Max);
+                *(uint16_t *)(factor + slot_off + (which == 0 ? q4_rk_scale(f4, k + u) : q4_rv_scale(f4, k + u))) = hs;
+                const float sc = half_bits_to_f32(hs);
+#pragma unroll
+                for (int a = 0; a < 32; ++a) {
+                    const int8_t code = (int8_t)(a < r ? q4_code(acc[u][a], sc) : 0);
+                    if (which == 0) sRc[a * d + k + u] = code;
+                    else sRc[(k + u) * 32 + a] = code;
+                }
+            }
         } else {
             const int rk4 = r4(rk), rv4 = r4(rv);
             const FactorLayout fl = factor_layout(P, d, rk, rv, g.key_t != 0);
@@ -634,9 +653,8 @@ void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor, Comp
     if constexpr (kQ4) {
         __builtin_amdgcn_s_waitcnt(0xc07f);
         __builtin_amdgcn_wave_barrier();
-        float *sScale = sR + 32 * d;
-        const Int4Layout f4 = int4_layout(P, d, rk, rv);
-        q4_quantize_store(factor + slot_off, f4, P, d, r, which, sL, sR, sScale, lane);
+        float *sScale = (float *)(sRc + 32 * d);
+        q4_store_codes(factor + slot_off, f4, P, d, r, which, sL, sRc, sScale, lane);
     } else {
         // L: A_K = L_K (P x r4(rk), zero past rk) row by row, A_V^T = L_V^T (rv x P)
         const FactorLayout fl = factor_layout(P, d, rk, rv, g.key_t != 0);

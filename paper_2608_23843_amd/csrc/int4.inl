@@ -91,32 +91,29 @@ constexpr uint32_t kQ4ZeroWord = 0x88888888u;   // eight zero codes
 
 // ---- quantizer (page compression) -------------------------------------------
 //
-// Called by one wave after the balanced factors of one page half are in LDS:
-// sL[t * 32 + a] = L~[t][a] (a < r) and sR[a * d + c] = R~[a][c]; `which` = 0
-// for K, 1 for V. Scales first (one run per lane at a time), then every
-// 32-bit word of codes is assembled by one lane from its eight elements.
-__device__ void q4_quantize_store(char *slot, const Int4Layout &f, int P, int d, int r, int which, const float *sL,
-                                  const float *sR, float *sScale, int lane) {
-    // scales: K -> L~_K runs (run, a) then R~_K columns; V -> L~_V rows then R~_V columns
+// Called by one wave after the balanced factors of one page half are staged:
+// sL[t * 32 + a] = L~[t][a] (a < r) in LDS, R~ already quantized by the
+// caller (its scales, one per column of ranks, stored in the slot; its codes
+// in sRc: K as sRc[a * d + c], V as sRc[c * 32 + a], zero past rank r);
+// `which` = 0 for K, 1 for V. L~'s scales first (one run per lane at a time),
+// then every 32-bit word of codes is assembled by one lane from its eight
+// elements.
+__device__ void q4_store_codes(char *slot, const Int4Layout &f, int P, int d, int r, int which, const float *sL,
+                               const int8_t *sRc, float *sScale, int lane) {
+    // scales: K -> L~_K runs (run, a); V -> L~_V rows
     const int n_lruns = which == 0 ? (P / kQ4Run) * r8(r) : P;
-    for (int idx = lane; idx < n_lruns + d; idx += 64) {
+    for (int idx = lane; idx < n_lruns; idx += 64) {
         float amax = 0.f;
         int64_t pos;
-        if (idx < n_lruns) {
-            if (which == 0) {
-                const int u = idx / r8(r), a = idx % r8(r);
-                if (a < r)
-                    for (int t = u * kQ4Run; t < (u + 1) * kQ4Run; ++t) amax = fmaxf(amax, fabsf(sL[t * 32 + a]));
-                pos = q4_lk_scale(f, u, a);
-            } else {
-                const int t = idx;
-                for (int a = 0; a < r; ++a) amax = fmaxf(amax, fabsf(sL[t * 32 + a]));
-                pos = q4_lv_scale(f, t);
-            }
+        if (which == 0) {
+            const int u = idx / r8(r), a = idx % r8(r);
+            if (a < r)
+                for (int t = u * kQ4Run; t < (u + 1) * kQ4Run; ++t) amax = fmaxf(amax, fabsf(sL[t * 32 + a]));
+            pos = q4_lk_scale(f, u, a);
         } else {
-            const int c = idx - n_lruns;
-            for (int a = 0; a < r; ++a) amax = fmaxf(amax, fabsf(sR[a * d + c]));
-            pos = which == 0 ? q4_rk_scale(f, c) : q4_rv_scale(f, c);
+            const int t = idx;
+            for (int a = 0; a < r; ++a) amax = fmaxf(amax, fabsf(sL[t * 32 + a]));
+            pos = q4_lv_scale(f, t);
         }
         const uint16_t h = f16_rne((double)amax / (double)kQ4Max);
         *(uint16_t *)(slot + pos) = h;
@@ -124,8 +121,14 @@ __device__ void q4_quantize_store(char *slot, const Int4Layout &f, int P, int d,
     }
     __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): scale stores to LDS done
     __builtin_amdgcn_wave_barrier();
-    // codes, one 32-bit word per lane per step; each word's eight elements are
-    // recovered from its position
+    // eight codes of R~ held contiguously in sRc -> one word
+    auto pack8 = [](const int8_t *p8) -> uint32_t {
+        const uint64_t v = *(const uint64_t *)p8;
+        uint32_t word = 0;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) word |= q4_nib((int)(int8_t)(v >> (8 * e))) << int4_nib(e);
+        return word;
+    };
     if (which == 0) {
         // L~_K words: [kq][i][tt], 16 * 4 words per kq
         const int n_lk = (r8(r) / 8) * 64;
@@ -140,29 +143,17 @@ __device__ void q4_quantize_store(char *slot, const Int4Layout &f, int P, int d,
             }
             *(uint32_t *)(slot + f.akc + 4LL * w) = word;
         }
-        // R~_K words: [a][kq][s], d / 8 words per row
+        // R~_K words: [a][kq][s], d / 8 words per row, dims 32 s + 8 kq + e
         for (int w = lane; w < r * (d / 8); w += 64) {
             const int a = w / (d / 8), kq = (w % (d / 8)) / 4, s = w % 4;
-            uint32_t word = 0;
-            for (int e = 0; e < 8; ++e) {
-                const int c = 32 * s + 8 * kq + e;
-                word |= q4_nib(q4_code(sR[a * d + c], sScale[n_lruns + c])) << int4_nib(e);
-            }
-            *(uint32_t *)(slot + f.bkc + 4LL * w) = word;
+            *(uint32_t *)(slot + f.bkc + 4LL * w) = pack8(sRc + a * d + 32 * s + 8 * kq);
         }
     } else {
-        // R~_V^T words: [kq][i][dt], 16 * 8 words per kq
+        // R~_V^T words: [kq][i][dt], 16 * 8 words per kq, ranks 8 kq + e of dim 16 dt + i
         const int n_rv = (r8(r) / 8) * 128;
         for (int w = lane; w < n_rv; w += 64) {
             const int kq = w / 128, i = (w / 8) % 16, dt = w % 8;
-            const int c = 16 * dt + i;
-            uint32_t word = 0;
-            for (int e = 0; e < 8; ++e) {
-                const int a = 8 * kq + e;
-                const int code = a < r ? q4_code(sR[a * d + c], sScale[n_lruns + c]) : 0;
-                word |= q4_nib(code) << int4_nib(e);
-            }
-            *(uint32_t *)(slot + f.bvc + 4LL * w) = word;
+            *(uint32_t *)(slot + f.bvc + 4LL * w) = pack8(sRc + (16 * dt + i) * 32 + 8 * kq);
         }
         // L~_V^T words: [i][kq][rt][ks], 16 words per i, i < r8 / 2
         const int n_lv = (r8(r) / 2) * 16;
