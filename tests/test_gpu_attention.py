@@ -174,3 +174,34 @@ def test_repeated_calls_share_workspace():
                 assert float((out - first).abs().max()) <= 1e-5 * scale
                 assert float((lse - lse0).abs().max()) <= 1e-5
         assert np.all(ws[-16:].cpu().numpy() == 0)
+
+
+@pytest.mark.parametrize("g", [1, 16])
+def test_query_group_extremes_bf16(g):
+    """One query head per KV head (g = 1, 15 of the 16 MFMA columns unused)
+    and the largest supported group (g = 16), d = 128, P = 64."""
+    out, ref, lse, rl = run_case(2, 2, g, 128, 64, [64 * 11 + 20, 64 * 6], 64, 128,
+                                 lambda b, h, j: (24 - (j % 3) * 4, 20), r0=24, wid=91)
+    _assert_close(out, ref, lse, rl)
+
+
+def test_ragged_lengths_around_unit_boundaries():
+    """P = 64 dense pages are streamed as two 32-token units: lengths just
+    below, at and above 32, 64 and the window edge, in one batch, with heads
+    too short to fill one round of page claims."""
+    lens = [1, 31, 32, 33, 63, 64, 65, 127, 129, 64 * 9 + 31, 64 * 9 + 32, 64 * 9 + 33]
+    out, ref, lse, rl = run_case(len(lens), 1, 4, 128, 64, lens, 64, 128,
+                                 lambda b, h, j: (16 + 4 * (j % 4), 32 - 4 * (j % 3)), r0=24, wid=92)
+    _assert_close(out, ref, lse, rl)
+
+
+def test_largest_batch():
+    """255 sequences (the batch limit) of lengths 0 .. 260 in one call."""
+    rng = np.random.default_rng(8)
+    lens = [int(x) for x in rng.integers(0, 261, 255)]
+    lens[0], lens[1] = 0, 260
+    out, ref, lse, rl = run_case(255, 1, 2, 64, 32, lens, 32, 32, 8, r0=8, wid=93)
+    for b, T in enumerate(lens):
+        if T == 0:
+            assert np.all(out[b] == 0) and np.all(np.isneginf(lse[b]))
+    _assert_close(out, ref, lse, rl)
