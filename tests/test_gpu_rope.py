@@ -93,6 +93,7 @@ def test_pre_rope_imported_oracle_factors():
     """Factor pages from the oracle's own decomposition of the pre-RoPE keys
     and dense pages, imported through the C ABI: no GPU decomposition
     involved, so this pins the attention side alone."""
+    import torch
     import paper_2608_23843_amd as pk
     d, P, G, B, Hkv, S, W = 128, 64, 8, 1, 2, 64, 128
     T = P * 10 + 41
@@ -105,8 +106,6 @@ def test_pre_rope_imported_oracle_factors():
     cache.reset()
     ranks = [(r, 23 - (j % 5)) for j, r in enumerate([24, 7, 18, 21, 24, 11, 24, 15, 24, 24, 24])][:n]
     q = synth.queries(wl, 0, 0)
-    import torch
-    out, _ = None, None
     refs = []
     for h in range(Hkv):
         pages = build_head_pages(K[0, h], V[0, h], T, P, S, W, ranks, "bf16")
