@@ -205,3 +205,34 @@ def test_largest_batch():
         if T == 0:
             assert np.all(out[b] == 0) and np.all(np.isneginf(lse[b]))
     _assert_close(out, ref, lse, rl)
+
+
+@pytest.mark.parametrize("case", range(12))
+def test_random_geometries(case):
+    """Seeded draws over the bf16 matrix-core kernel's geometry: (d, P)
+    cycling over {64, 128} x {16, 32, 64}, query group 1..16, sink and window of 0..3
+    pages (in tokens, not always page multiples), ranks 1..min(P, 32) drawn
+    per page for K and V separately, 1..4 sequences of ragged lengths (one
+    possibly empty)."""
+    rng = np.random.default_rng(1000 + case)
+    d = (64, 128)[(case // 3) % 2]
+    P = (16, 32, 64)[case % 3]
+    g = int(rng.integers(1, 17))
+    Hkv = int(rng.integers(1, 4))
+    B = int(rng.integers(1, 5))
+    S = int(rng.integers(0, 3 * P + 1))
+    W = int(rng.integers(0, 3 * P + 1))
+    rmax = min(P, 32)
+    lens = [int(rng.integers(1, 40 * P)) for _ in range(B)]
+    if B > 1 and rng.random() < 0.3:
+        lens[int(rng.integers(0, B))] = 0
+    rk = rng.integers(1, rmax + 1, (B, Hkv, 64))
+    rv = rng.integers(1, rmax + 1, (B, Hkv, 64))
+    out, ref, lse, rl = run_case(B, Hkv, g, d, P, lens, S, W,
+                                 lambda b, h, j: (int(rk[b, h, j % 64]), int(rv[b, h, j % 64])),
+                                 r0=int(rng.integers(2, rmax + 1)), wid=100 + case)
+    print("case %d: B=%d Hkv=%d g=%d d=%d P=%d S=%d W=%d lens=%s" % (case, B, Hkv, g, d, P, S, W, lens))
+    for b, T in enumerate(lens):
+        if T == 0:
+            assert np.all(out[b] == 0) and np.all(np.isneginf(lse[b]))
+    _assert_close(out, ref, lse, rl)
