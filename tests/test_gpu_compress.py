@@ -425,3 +425,39 @@ def test_adaptive_ranks_incremental_compress():
     plan = oracle.plan_pages(T0, P, S, W, max_pages)
     for j in np.flatnonzero(plan == oracle.FACTOR):
         assert rk[0, 0, j] == 24
+
+
+@pytest.mark.parametrize("case", range(8))
+def test_random_geometries_matrix_core(case):
+    """Seeded draws over the matrix-core decomposition: P in {32, 64}, d a
+    multiple of 32 up to 256 (d < P gives Gram matrices of rank d), per-page
+    ranks 1..min(P, d, 32), fp32 or bf16 factors, a planted page rank r0 and
+    RoPE'd keys with outlier channels; every factor page of every head is
+    checked against the oracle's SVD (sign-invariant)."""
+    rng = np.random.default_rng(2000 + case)
+    P = (32, 64)[case % 2]
+    d = int(rng.choice([32, 64, 96, 128, 192, 256]))
+    ft = ("f32", "bf16")[(case // 2) % 2]
+    tols = (1e-4, 1e-4, 1e-5) if ft == "f32" else (6e-3, 1e-2, 4e-3)
+    B, Hkv = int(rng.integers(1, 3)), int(rng.integers(1, 3))
+    S, W = P * int(rng.integers(0, 2)), P * int(rng.integers(1, 3))
+    T = P * int(rng.integers(4, 10)) + int(rng.integers(0, P))
+    rmax = min(P, d, 32)
+    npg = -(-T // P)
+    table = rng.integers(1, rmax + 1, (B, Hkv, npg))
+    r0 = int(rng.integers(2, rmax + 1))
+    cache, K, V, npg = _prefill_case(B, Hkv, d, P, T, S, W, 0, "bf16", ft, r0, rank_table=table,
+                                     rope=1e6, outliers=2, seed=case)
+    assert cache.device_status() == 0
+    kind = oracle.plan_pages(T, P, S, W, npg)
+    refs = [(b, h, j) for b in range(B) for h in range(Hkv) for j in range(npg) if kind[j] == oracle.FACTOR]
+    print("case %d: P=%d d=%d %s B=%d Hkv=%d T=%d S=%d W=%d r0=%d, %d factor pages"
+          % (case, P, d, ft, B, Hkv, T, S, W, r0, len(refs)))
+    blocks = _export(cache, refs)
+    R = cache.c.max_rank
+    for (b, h, j), blk in zip(refs, blocks):
+        r = int(table[b, h, j])
+        Lk, Rk, Lv, Rv = _unpack_factor(blk, P, d, R)
+        for L, Rm, X in ((Lk, Rk, K[b, h, j * P:(j + 1) * P]), (Lv, Rv, V[b, h, j * P:(j + 1) * P])):
+            _check_factor(L[:, :r], Rm[:r], X.astype(np.float64), r, *tols)
+            assert np.all(L[:, r:] == 0) and np.all(Rm[r:] == 0)
