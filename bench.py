@@ -276,6 +276,10 @@ def main():
         comp_ms.append(ev0.elapsed_time(ev1))
     sweeps = cache.compress_sweeps() / 3.0
     status = cache.device_status()
+    fp = cache.footprint([T] * B, layer=0)   # live KV footprint of the prefilled layer
+    fp_ratio = (fp["dense_bytes"] + fp["factor_bytes"]) / fp["raw_bytes"]
+    fp_slots = (fp["dense_bytes"] + fp["factor_slot_bytes"]) / fp["raw_bytes"]
+    log("live KV footprint at T=%d: %.5f of raw (slots with padding: %.5f)" % (T, fp_ratio, fp_slots))
     if wl.rank_error > 0:
         ranks_np, ranks_v_np = chosen_ranks(cache, kinds, max_pages, wl.rank_error)
     comp_ms_best = min(comp_ms)
@@ -414,6 +418,8 @@ def main():
         "compress_useful_tflops": round(comp["useful"] / comp_ms_best / 1e9, 3),
         "compress_executed_tflops": round(comp["executed"] / comp_ms_best / 1e9, 3),
         "compress_calls_in_run": compress_calls,
+        "footprint_ratio": round(fp_ratio, 5),
+        "footprint_ratio_slots": round(fp_slots, 5),
         "device_status": status,
         "roofline": roofline,
     }

@@ -290,6 +290,37 @@ int64_t pkv_int4_blob_bytes(const pkv_cache *c, int32_t rank_k, int32_t rank_v);
 pkv_status pkv_export_int4_pages(const pkv_cache *c, int32_t layer, int32_t n, const int32_t *b,
                                  const int32_t *kv_head, const int32_t *page, void *dst, pkv_stream s);
 
+/* ---- accounting ----------------------------------------------------------- */
+
+/* Live KV footprint of one layer (layer >= 0) or of every layer (layer < 0),
+ * read from the page table: the logical live cache against the raw,
+ * uncompressed one (Section 4.5, "Memory Footprint"; Eq. (3) for a factor
+ * page). seq_len: host [batch], the tokens each sequence holds. Sums over
+ * the selected layers and every (sequence, KV head):
+ *   raw_bytes          K and V of every live token in dense_dtype (2 T d e)
+ *   dense_bytes        K and V of the tokens held on dense pages
+ *   factor_bytes       factor pages at their ranks, logical: (r_K + r_V)(P + d)
+ *                      elements of factor_dtype (Eq. (3)); INT4: half a byte
+ *                      per code plus 2 bytes per fp16 scale, one scale per run
+ *                      of up to 32 elements along the paper's directions
+ *   factor_slot_bytes  what those pages' slots hold, padding included (the
+ *                      sum of pkv_factor_page_bytes)
+ *   dense_pages, factor_pages
+ * (dense_bytes + factor_bytes) / raw_bytes is the footprint ratio the paper
+ * reports. The page table is copied to the host on stream s, which is
+ * synchronized; no kernel runs. A page inside a sequence that is neither
+ * dense nor factorized gives PKV_E_STATE. */
+typedef struct {
+    int64_t raw_bytes;
+    int64_t dense_bytes;
+    int64_t factor_bytes;
+    int64_t factor_slot_bytes;
+    int64_t dense_pages;
+    int64_t factor_pages;
+} pkv_footprint;
+pkv_status pkv_cache_bytes(const pkv_cache *c, int32_t layer, const int32_t *seq_len, pkv_footprint *out,
+                           pkv_stream s);
+
 /* ---- diagnostics --------------------------------------------------------- */
 
 /* Synchronizes the stream, then returns (and clears) the current device's

@@ -243,6 +243,15 @@ class PuzzleKVCache:
               "pkv_compress_sweeps")
         return int(n.value)
 
+    def footprint(self, seq_len, layer: int = -1, stream=None) -> dict:
+        """Live KV footprint (pkv_cache_bytes) of `layer` (-1: every layer) for the
+        sequences' lengths seq_len, as a dict of byte and page counts."""
+        seq = _i32(seq_len, self.c.batch)
+        f = _lib.PkvFootprint()
+        check(self.lib.pkv_cache_bytes(ctypes.byref(self.c), layer, seq.ctypes.data, ctypes.byref(f),
+                                       _stream_handle(self.torch, stream)), "pkv_cache_bytes")
+        return {name: int(getattr(f, name)) for name, _ in f._fields_}
+
     def device_status(self, stream=None) -> int:
         bits = ctypes.c_uint32(0)
         check(self.lib.pkv_device_status(_stream_handle(self.torch, stream), ctypes.byref(bits)),

@@ -23,8 +23,13 @@ EXPORTS = [
     "pkv_workspace_bytes", "pkv_plan_pages", "pkv_eligible_pages", "pkv_cache_reset", "pkv_prefill",
     "pkv_append_kv", "pkv_compress_pages", "pkv_mixed_decode_attention", "pkv_import_pages",
     "pkv_export_block_elems", "pkv_export_pages", "pkv_int4_blob_bytes", "pkv_export_int4_pages",
-    "pkv_device_status", "pkv_compress_sweeps", "pkv_last_error", "pkv_version",
+    "pkv_device_status", "pkv_compress_sweeps", "pkv_cache_bytes", "pkv_last_error", "pkv_version",
 ]
+
+
+class PkvFootprint(ctypes.Structure):
+    _fields_ = [(name, ctypes.c_int64) for name in ("raw_bytes", "dense_bytes", "factor_bytes",
+                                                    "factor_slot_bytes", "dense_pages", "factor_pages")]
 
 
 class PkvPage(ctypes.Structure):
@@ -82,6 +87,7 @@ def load():
         "pkv_export_int4_pages": ([cp, i32, i32, vp, vp, vp, vp, vp], i32),
         "pkv_device_status": ([vp, ctypes.POINTER(u32)], i32),
         "pkv_compress_sweeps": ([vp, ctypes.POINTER(ctypes.c_uint64)], i32),
+        "pkv_cache_bytes": ([cp, i32, vp, ctypes.POINTER(PkvFootprint), vp], i32),
         "pkv_last_error": ([], ctypes.c_char_p),
         "pkv_version": ([], ctypes.c_char_p),
     }

@@ -524,6 +524,63 @@ pkv_status pkv_compress_sweeps(pkv_stream s, uint64_t *sweeps) {
     return PKV_OK;
 }
 
+pkv_status pkv_cache_bytes(const pkv_cache *c, int32_t layer, const int32_t *seq_len, pkv_footprint *out,
+                           pkv_stream s) {
+    pkv_status st = check_cache(c, true);
+    if (st != PKV_OK) return st;
+    if (!seq_len || !out) return fail(PKV_E_ARG, "seq_len and out must not be NULL");
+    if (layer >= c->n_layers) return fail(PKV_E_ARG, "layer %d outside 0..%d", layer, c->n_layers - 1);
+    const Geo g = make_geo(c);
+    for (int b = 0; b < g.B; ++b)
+        if (seq_len[b] < 0 || (int64_t)seq_len[b] > (int64_t)g.max_pages * g.P)
+            return fail(PKV_E_SHAPE, "seq_len[%d] = %d outside 0..max_pages * P", b, seq_len[b]);
+    const int64_t P = g.P, d = g.d, ed = g.dense_es;
+    const bool kt = g.key_t != 0;
+    // logical bytes of a factor page pair at ranks (rk, rv)
+    auto logical = [&](int64_t rk, int64_t rv) -> int64_t {
+        if (g.factor_dtype == PKV_INT4) {
+            auto runs = [](int64_t n) { return (n + 31) / 32; };
+            const int64_t scales = rk * runs(P) + d * runs(rk) + P * runs(rv) + d * runs(rv);
+            return (rk + rv) * (P + d) / 2 + 2 * scales;
+        }
+        return (rk + rv) * (P + d) * g.factor_es;
+    };
+    pkv_footprint f{};
+    std::vector<pkv_page> tab((size_t)g.layer_entries);
+    const int l0 = layer < 0 ? 0 : layer, l1 = layer < 0 ? c->n_layers : layer + 1;
+    for (int l = l0; l < l1; ++l) {
+        hipError_t e = hipMemcpyAsync(tab.data(), c->page_table + (int64_t)l * g.layer_entries,
+                                      sizeof(pkv_page) * (size_t)g.layer_entries, hipMemcpyDeviceToHost,
+                                      (hipStream_t)s);
+        if (e == hipSuccess) e = hipStreamSynchronize((hipStream_t)s);
+        if (e != hipSuccess) return hip_fail(e, "pkv_cache_bytes (page table copy)");
+        for (int b = 0; b < g.B; ++b) {
+            const int64_t T = seq_len[b];
+            for (int h = 0; h < g.Hkv; ++h) {
+                f.raw_bytes += 2 * T * d * ed;
+                const pkv_page *row = tab.data() + g.head_index(b, h) * g.max_pages;
+                for (int64_t j = 0; j * P < T; ++j) {
+                    const pkv_page ent = row[j];
+                    if (ent.kind == PKV_DENSE) {
+                        ++f.dense_pages;
+                        f.dense_bytes += 2 * std::min<int64_t>(P, T - j * P) * d * ed;
+                    } else if (ent.kind == PKV_FACTOR) {
+                        ++f.factor_pages;
+                        f.factor_bytes += logical(ent.rank_k, ent.rank_v);
+                        f.factor_slot_bytes +=
+                            factor_page_bytes_of(g.factor_dtype, (int)P, (int)d, ent.rank_k, ent.rank_v, kt);
+                    } else {
+                        return fail(PKV_E_STATE, "layer %d, sequence %d, KV head %d: page %lld holds tokens but is "
+                                    "empty", l, b, h, (long long)j);
+                    }
+                }
+            }
+        }
+    }
+    *out = f;
+    return PKV_OK;
+}
+
 pkv_status pkv_device_status(pkv_stream s, uint32_t *bits) {
     if (!bits) return fail(PKV_E_ARG, "bits is NULL");
     hipError_t e = hipStreamSynchronize((hipStream_t)s);

@@ -205,3 +205,19 @@ def test_pre_rope_slot_holds_r_k_transposed(pk):
         assert b0 == 2 * (P * r4(rk) + rk * d + rv * P + d * r4(rv))
         assert b1 == 2 * (P * r4(rk) + r4(rk) * d + rv * P + d * r4(rv))
     assert lib.pkv_factor_slot_bytes(c1) >= 2 * (P * 32 + 32 * d + 30 * P + d * 32)
+
+
+def test_cache_bytes_argument_errors(pk):
+    """pkv_cache_bytes checks its arguments before touching the page table."""
+    from paper_2608_23843_amd import _lib
+    lib = pk.load_library()
+    c = _cache(pk)
+    c.dense_pool = c.factor_pool = c.page_table = 0x1000
+    f = _lib.PkvFootprint()
+    seq = np.array([64, 64], dtype=np.int32)
+    assert lib.pkv_cache_bytes(c, 0, None, ctypes.byref(f), None) == 1
+    assert lib.pkv_cache_bytes(c, 0, seq.ctypes.data, None, None) == 1
+    assert lib.pkv_cache_bytes(c, 2, seq.ctypes.data, ctypes.byref(f), None) == 1
+    big = np.array([64, 8 * 64 + 1], dtype=np.int32)
+    assert lib.pkv_cache_bytes(c, 0, big.ctypes.data, ctypes.byref(f), None) == 2
+    assert lib.pkv_last_error()
