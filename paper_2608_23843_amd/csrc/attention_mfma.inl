@@ -362,6 +362,26 @@ __device__ inline void rope_row(float (&x)[D / 32][8], float t, int q, const flo
         }
 }
 
+// Rotates the pairs (x0[u], x1[u]) of one lane's key row at position t:
+// x0[u] is dim 32 s + 8 q + u, x1[u] its partner d/2 above.
+template <int D>
+__device__ inline void rope_pair(float (&x0)[8], float (&x1)[8], float t, int s, int q, const float *rw) {
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int i0 = 32 * s + 8 * q + 4 * h;
+        const f32x4 wh = *(const f32x4 *)(rw + i0);
+        const f32x4 wl = *(const f32x4 *)(rw + D / 2 + i0);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            float c, sn;
+            rope_cs(t, wh[v], wl[v], c, sn);
+            const float a = x0[4 * h + v], b = x1[4 * h + v];
+            x0[4 * h + v] = a * c - b * sn;
+            x1[4 * h + v] = fmaf(b, c, a * sn);
+        }
+    }
+}
+
 // Phase 1 of a unit of a pre-RoPE cache. Factor page: per token tile,
 // K^T = R_K^T L_K^T, rotation, S^T = K Q^T; rank entries at or past r4(rk)
 // of the L_K operand are zeroed (the R_K^T operand holds the next row's
@@ -406,24 +426,30 @@ __device__ inline void unit_phase1_rope(WaveState<D> &w, const KeyOps<D, P> &f, 
         if (!m_lo) am[0] = am[1] = 0u;
         if (!m_hi) am[2] = am[3] = 0u;
         const bf16x8 a = __builtin_bit_cast(bf16x8, am);
-        float x[D / 32][8];
-#pragma unroll
-        for (int s = 0; s < D / 32; ++s)
-#pragma unroll
-            for (int hp = 0; hp < 2; ++hp) {
-                const f32x4 kt = mfma_bf16(f.bk[hp][s], a, zero_f4());
-#pragma unroll
-                for (int v = 0; v < 4; ++v) x[s][4 * hp + v] = kt[v];
-            }
-        rope_row<D>(x, (float)(t0 + token_row<P>(tt, n)), q, rw);
+        const float tpos = (float)(t0 + token_row<P>(tt, n));
         st[tt] = zero_f4();
+        // one rotate-half pair of 32-dim chunks (s, s + d/64) at a time
 #pragma unroll
-        for (int s = 0; s < D / 32; ++s) {
-            uint32_t hd[4], ld[4];
+        for (int s0 = 0; s0 < D / 64; ++s0) {
+            float x[2][8];
 #pragma unroll
-            for (int u = 0; u < 4; ++u) split2(x[s][2 * u], x[s][2 * u + 1], hd[u], ld[u]);
-            st[tt] = mfma_bf16(__builtin_bit_cast(bf16x8, u32x4{hd[0], hd[1], hd[2], hd[3]}), qb[s], st[tt]);
-            st[tt] = mfma_bf16(__builtin_bit_cast(bf16x8, u32x4{ld[0], ld[1], ld[2], ld[3]}), qb[s], st[tt]);
+            for (int k = 0; k < 2; ++k)
+#pragma unroll
+                for (int hp = 0; hp < 2; ++hp) {
+                    const f32x4 kt = mfma_bf16(f.bk[hp][s0 + k * (D / 64)], a, zero_f4());
+#pragma unroll
+                    for (int v = 0; v < 4; ++v) x[k][4 * hp + v] = kt[v];
+                }
+            rope_pair<D>(x[0], x[1], tpos, s0, q, rw);
+#pragma unroll
+            for (int k = 0; k < 2; ++k) {
+                uint32_t hd[4], ld[4];
+#pragma unroll
+                for (int u = 0; u < 4; ++u) split2(x[k][2 * u], x[k][2 * u + 1], hd[u], ld[u]);
+                const bf16x8 qv = qb[s0 + k * (D / 64)];
+                st[tt] = mfma_bf16(__builtin_bit_cast(bf16x8, u32x4{hd[0], hd[1], hd[2], hd[3]}), qv, st[tt]);
+                st[tt] = mfma_bf16(__builtin_bit_cast(bf16x8, u32x4{ld[0], ld[1], ld[2], ld[3]}), qv, st[tt]);
+            }
         }
     }
     page_softmax<D, P, false>(w, st, eh, el, P, q, c2);
