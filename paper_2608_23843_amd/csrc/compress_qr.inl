@@ -312,7 +312,11 @@ void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor, Comp
     // the r largest columns did not change and no pair touching them needed a
     // rotation by more than sqrt(tol) in cosine: Jacobi converges
     // quadratically, so what such a sweep leaves is below tol.
-    constexpr float kTolFactor = std::is_same<TF, uint16_t>::value ? 10.f : 1.f;
+    // Threshold on the cosine of two columns: P 2^-23, a hundred times that
+    // for bf16 factors (7.6e-4 at P = 64), below the 2^-9 rounding of every
+    // stored entry of L. fp32 factors, and INT4 factors (quantized from
+    // exactly what an fp32 cache stores), keep the tight one.
+    constexpr float kTolFactor = std::is_same<TF, uint16_t>::value ? 100.f : 1.f;
     const float tol = kTolFactor * (float)P * 1.1920929e-7f;
     const float stop_tol = sqrtf(tol);
     // requested rank, 0 for a rank chosen from the spectrum (adaptive ranks).
