@@ -158,10 +158,10 @@ void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor, Comp
     const int grp = P == 64 ? 0 : lane >> 5;
     const int c = P == 64 ? lane : lane & 31;
     int rk_first = 0;   // two passes: the K rank chosen by the first
-    for (int pass = 0; pass < kPasses; ++pass) {
+    for (int kv = 0; kv < kPasses; ++kv) {
     // K and V of a page are decompositions 2i and 2i + 1 of the launch, so
     // a pass is active exactly when the other one is
-    const int64_t q = ((int64_t)blockIdx.x * kPasses + pass) * D + grp;
+    const int64_t q = ((int64_t)blockIdx.x * kPasses + kv) * D + grp;
 
     const DecompRef ref = decode_decomp<uint16_t>(g, table, dense, items, src, q, n_decomp, c == 0);
     const bool active = ref.active;
@@ -526,8 +526,8 @@ void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor, Comp
     // the page's K and V ranks (each chosen by its own half when adaptive)
     int rk, rv;
     if constexpr (P == 64) {
-        if (kAdapt) {   // pass 0 decomposes K (its sections do not depend on rv), pass 1 V
-            if (pass == 0) rk_first = r_own;
+        if (kAdapt) {   // kv = 0 decomposes K (its sections do not depend on rv), kv = 1 V
+            if (kv == 0) rk_first = r_own;
             rk = rk_first;
             rv = r_own;
         } else {
