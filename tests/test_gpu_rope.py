@@ -217,3 +217,10 @@ def test_pre_rope_with_adaptive_ranks():
     assert np.all(o1 == 0) and np.all(np.isneginf(lse[1].cpu().numpy()))
     _check(cache, q, T, lambda Tb, n: oracle.plan_pages(Tb, P, S, W, n), rk, rv, P, d, R, G,
            "pre-RoPE + adaptive")
+    # the footprint counts the transposed, padded R_K of these slots
+    f = cache.footprint(T)
+    fac_pages = [(h, j) for h in range(Hkv) for j in np.flatnonzero(plan == oracle.FACTOR)]
+    assert f["factor_pages"] == len(fac_pages)
+    assert f["factor_slot_bytes"] == sum(cache.factor_page_bytes(int(rk[0, h, j]), int(rv[0, h, j]))
+                                         for h, j in fac_pages)
+    assert f["factor_bytes"] == sum((int(rk[0, h, j]) + int(rv[0, h, j])) * (P + d) * 2 for h, j in fac_pages)
