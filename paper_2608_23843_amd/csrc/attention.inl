@@ -14,11 +14,12 @@ namespace pkv {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
-// Partial states of one call, for each (sequence, KV head) `head`, query qi
-// of the group and chunk c: O[head][qi][k][c] with the chunk index fastest
-// (padded to nc4, a multiple of 4, so one output's chunks share cache lines),
-// and the max M[head][qi][c] (log2 units) and normalizer L[head][qi][c]; then
-// one merge counter per head.
+// Partial states of one call, for each (sequence, KV head) `head`, chunk c
+// and query qi of the group: O[head][c][qi][k], the max M[head][c][qi] (log2
+// units) and the normalizer L[head][c][qi], so that each workgroup's partial
+// is one contiguous block (whole cache lines written, no line shared between
+// workgroups) and the merge reads one chunk per load across consecutive
+// lanes; then one merge counter per head.
 struct Partials {
     float *o, *m, *l;
     unsigned int *counters;  // chunks published, per head
@@ -26,9 +27,9 @@ struct Partials {
     __host__ __device__ unsigned int *claim(int64_t head) const { return claims + head * 64; }
     int nc, nc4, g, d;
     __host__ __device__ int64_t oi(int64_t head, int qi, int k, int c) const {
-        return ((head * g + qi) * d + k) * nc4 + c;
+        return ((head * nc4 + c) * g + qi) * d + k;
     }
-    __host__ __device__ int64_t mi(int64_t head, int qi, int c) const { return (head * g + qi) * nc4 + c; }
+    __host__ __device__ int64_t mi(int64_t head, int qi, int c) const { return (head * nc4 + c) * g + qi; }
 };
 
 __host__ __device__ inline int64_t round256(int64_t b) { return (b + 255) / 256 * 256; }
@@ -98,15 +99,16 @@ __device__ void publish_and_merge(const Geo &g, int64_t head, const Partials &pp
         const int qi = idx / d, k = idx % d;
         const float *mp = pp.m + pp.mi(head, qi, 0), *lp = pp.l + pp.mi(head, qi, 0);
         const float *op = pp.o + pp.oi(head, qi, k, 0);
+        const int64_t cm = G, co = (int64_t)G * d;   // chunk strides
         float M = -INFINITY, L = 0.f, A = 0.f;
         for (int c0 = 0; c0 < nc; c0 += 8) {
             float mv[8], lv[8], ov[8];
 #pragma unroll
             for (int u = 0; u < 8; ++u) {
                 const bool ok = c0 + u < nc;
-                mv[u] = ok ? ld_dev(mp + c0 + u) : -INFINITY;
-                lv[u] = ok ? ld_dev(lp + c0 + u) : 0.f;
-                ov[u] = ok ? ld_dev(op + c0 + u) : 0.f;
+                mv[u] = ok ? ld_dev(mp + (c0 + u) * cm) : -INFINITY;
+                lv[u] = ok ? ld_dev(lp + (c0 + u) * cm) : 0.f;
+                ov[u] = ok ? ld_dev(op + (c0 + u) * co) : 0.f;
             }
             float Mg = M;
 #pragma unroll
