@@ -55,10 +55,14 @@ typedef enum { PKV_EMPTY = 0, PKV_DENSE = 1, PKV_FACTOR = 2 } pkv_kind;
 
 /* Device status bits (pkv_device_status). */
 #define PKV_DEV_NOT_DENSE     0x1u /* compress_pages found a page that is not dense   */
-#define PKV_DEV_BAD_PAGE      0x2u /* attention met an empty page below the length    */
-#define PKV_DEV_RING_OVERRUN  0x4u /* append would overwrite a page still dense       */
+#define PKV_DEV_BAD_PAGE      0x2u /* attention met an empty page below the length,   */
+                                   /* or more dense pages per head than dense slots  */
+#define PKV_DEV_RING_OVERRUN  0x4u /* append or import would overwrite a page still  */
+                                   /* dense (two dense pages on one ring slot)       */
 #define PKV_DEV_NO_CONVERGE   0x8u /* a decomposition hit the sweep cap (result kept)  */
 #define PKV_DEV_BAD_RANK      0x10u /* prefill met a rank outside 1..max_rank (clamped) */
+#define PKV_DEV_NOT_ELIGIBLE  0x20u /* compress_pages found a dense page that is       */
+                                    /* incomplete or still inside the window           */
 
 /*
  * Page-table entry, 8 bytes. slot is relative to the layer:
@@ -72,7 +76,7 @@ typedef struct {
     uint8_t kind;   /* pkv_kind */
     uint8_t rank_k; /* factor pages: r_K, else 0 */
     uint8_t rank_v; /* factor pages: r_V, else 0 */
-    uint8_t flags;  /* reserved, 0 */
+    uint8_t rows;   /* dense pages: tokens written (1..P; P for imported pages), else 0 */
 } pkv_page;
 
 /*
@@ -168,7 +172,8 @@ size_t pkv_page_table_bytes(const pkv_cache *c);
 size_t pkv_factor_page_bytes(const pkv_cache *c, int32_t rank_k, int32_t rank_v);
 
 /* Workspace sizes. op PKV_OP_ATTENTION: n = longest sequence length passed to
- * pkv_mixed_decode_attention; PKV_OP_COMPRESS: n = pages per call;
+ * pkv_mixed_decode_attention (a workspace sized for n serves every call with
+ * sequences up to n tokens); PKV_OP_COMPRESS: n = pages per call;
  * PKV_OP_PREFILL: n = longest prompt length. */
 enum { PKV_OP_ATTENTION = 0, PKV_OP_COMPRESS = 1, PKV_OP_PREFILL = 2, PKV_OP_IMPORT = 3 };
 size_t pkv_workspace_bytes(const pkv_cache *c, int32_t op, int64_t n);
@@ -224,10 +229,16 @@ pkv_status pkv_append_kv(const pkv_cache *c, int32_t layer, const void *k_new, c
  * factors of Eq. (2)); K and V of a page are decomposed independently.
  * b, kv_head, page: host [n]; rank_k, rank_v: host [n], 1 <= r <= min(P, d,
  * max_rank), or 0 for a rank chosen per page when adaptive ranks are enabled
- * (adaptive_rank_error > 0). Each page must be complete and DENSE; the entry becomes FACTOR
- * with its ranks and its dense slot is free for reuse. A page found not dense
- * is left untouched and PKV_DEV_NOT_DENSE is raised. Duplicate pages in one
- * call are rejected (PKV_E_ARG). Workspace: pkv_workspace_bytes(PKV_OP_COMPRESS, n). */
+ * (adaptive_rank_error > 0). A page is factorized once, when it has left the
+ * window (Section 3.3, "Incremental Cache Update"): it must be DENSE and
+ * complete (P rows written), outside the sink, and the cache must hold at
+ * least window_tokens tokens after it. The entry then becomes FACTOR with its
+ * ranks and its dense slot is free for reuse. A sink page is refused on the
+ * host (PKV_E_STATE, nothing enqueued). Other refusals are seen on the device:
+ * the page is left untouched and PKV_DEV_NOT_DENSE (already factorized or
+ * empty) or PKV_DEV_NOT_ELIGIBLE (incomplete, or still inside the window) is
+ * raised. Duplicate pages in one call are rejected (PKV_E_ARG).
+ * Workspace: pkv_workspace_bytes(PKV_OP_COMPRESS, n). */
 pkv_status pkv_compress_pages(const pkv_cache *c, int32_t layer, int32_t n, const int32_t *b,
                               const int32_t *kv_head, const int32_t *page, const uint8_t *rank_k,
                               const uint8_t *rank_v, void *ws, size_t ws_bytes, pkv_stream s);
@@ -240,11 +251,13 @@ pkv_status pkv_compress_pages(const pkv_cache *c, int32_t layer, int32_t n, cons
  * out = 0 and lse = -inf). out: device fp32 [batch][n_q_heads][d], normalized.
  * lse: device fp32 [batch][n_q_heads] log-sum-exp of the scaled scores, or NULL.
  * Softmax scale 1/sqrt(d); query head i uses KV head i / (n_q_heads / n_kv_heads).
- * Workspace: pkv_workspace_bytes(PKV_OP_ATTENTION, max seq_len) bytes holding
- * per-chunk partial states and two counters per (sequence, KV head); it must
- * be zero-filled before its first use, and every call leaves it ready for the
- * next (the counters return to zero). Calls that share a workspace must not
- * overlap. One kernel launch per call. With bf16 storage the pages of a head
+ * Workspace: pkv_workspace_bytes(PKV_OP_ATTENTION, max seq_len) bytes. It
+ * begins with two counters per (sequence, KV head): 4 * batch * n_kv_heads
+ * bytes rounded up to a multiple of 256, then 256 * batch * n_kv_heads bytes;
+ * per-chunk partial states follow. The counters must be zero before the first
+ * use; every call returns them to zero and writes every partial it reads, so
+ * a workspace sized for the longest sequence serves calls of any shorter
+ * length. Calls that share a workspace must not overlap. One kernel launch per call. With bf16 storage the pages of a head
  * are handed to the GPU's waves dynamically, so the order of the fp32 sums,
  * and with it the last bits of out and lse, can differ from call to call. */
 pkv_status pkv_mixed_decode_attention(const pkv_cache *c, int32_t layer, const void *q,
@@ -260,7 +273,11 @@ pkv_status pkv_mixed_decode_attention(const pkv_cache *c, int32_t layer, const v
  * dtype (dense_dtype for dense pages, factor_dtype for factor pages) and page
  * i's block starts src_offset[i] elements into it (for INT4 factor pages the
  * block is the canonical INT4 blob and src_offset[i] counts bytes). The
- * page-table entry is set. Workspace: pkv_workspace_bytes(PKV_OP_IMPORT, n). */
+ * page-table entry is set; a dense page counts as complete (rows = P). A
+ * dense page goes to its ring slot: two dense pages of one head on the same
+ * slot in one call are rejected (PKV_E_ARG), and a dense page whose slot
+ * already holds another dense page of the head is not written and raises
+ * PKV_DEV_RING_OVERRUN. Workspace: pkv_workspace_bytes(PKV_OP_IMPORT, n). */
 pkv_status pkv_import_pages(const pkv_cache *c, int32_t layer, int32_t n, const int32_t *b,
                             const int32_t *kv_head, const int32_t *page, const uint8_t *kind,
                             const uint8_t *rank_k, const uint8_t *rank_v, const void *src,

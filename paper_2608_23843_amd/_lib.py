@@ -15,6 +15,7 @@ PKV_EMPTY, PKV_DENSE, PKV_FACTOR = 0, 1, 2
 PKV_OP_ATTENTION, PKV_OP_COMPRESS, PKV_OP_PREFILL, PKV_OP_IMPORT = 0, 1, 2, 3
 PKV_DEV_NOT_DENSE, PKV_DEV_BAD_PAGE, PKV_DEV_RING_OVERRUN, PKV_DEV_NO_CONVERGE, PKV_DEV_BAD_RANK = (
     0x1, 0x2, 0x4, 0x8, 0x10)
+PKV_DEV_NOT_ELIGIBLE = 0x20
 
 # Every symbol include/puzzlekv.h declares.
 EXPORTS = [
@@ -34,7 +35,7 @@ class PkvFootprint(ctypes.Structure):
 
 class PkvPage(ctypes.Structure):
     _fields_ = [("slot", ctypes.c_int32), ("kind", ctypes.c_uint8), ("rank_k", ctypes.c_uint8),
-                ("rank_v", ctypes.c_uint8), ("flags", ctypes.c_uint8)]
+                ("rank_v", ctypes.c_uint8), ("rows", ctypes.c_uint8)]
 
 
 class PkvCache(ctypes.Structure):

@@ -14,12 +14,17 @@ namespace pkv {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
-// Partial states of one call, for each (sequence, KV head) `head`, chunk c
-// and query qi of the group: O[head][c][qi][k], the max M[head][c][qi] (log2
-// units) and the normalizer L[head][c][qi], so that each workgroup's partial
-// is one contiguous block (whole cache lines written, no line shared between
+// Workspace of one call. It starts with the per-head words that must be zero
+// when a call begins and that every call returns to zero: one merge counter
+// per (sequence, KV head) `head`, then one page-claim word per head on its
+// own 256-byte line. Their offsets depend only on the number of heads, so a
+// workspace sized for the longest sequence can be shared by calls of any
+// length. The partial states follow, for each head, chunk c and query qi of
+// the group: O[head][c][qi][k], the max M[head][c][qi] (log2 units) and the
+// normalizer L[head][c][qi], so that each workgroup's partial is one
+// contiguous block (whole cache lines written, no line shared between
 // workgroups) and the merge reads one chunk per load across consecutive
-// lanes; then one merge counter per head.
+// lanes. The partials are fully written by every call before they are read.
 struct Partials {
     float *o, *m, *l;
     unsigned int *counters;  // chunks published, per head
@@ -34,28 +39,39 @@ struct Partials {
 
 __host__ __device__ inline int64_t round256(int64_t b) { return (b + 255) / 256 * 256; }
 
-__host__ __device__ inline int64_t partials_bytes(int64_t heads, int n_chunks, int g, int d) {
+// Bytes of the zero-on-entry words for `heads` heads.
+__host__ __device__ inline int64_t counter_bytes(int64_t heads) { return round256(heads * 4) + heads * 256; }
+// Bytes of the partial states.
+__host__ __device__ inline int64_t partial_state_bytes(int64_t heads, int n_chunks, int g, int d) {
     const int64_t nc4 = (n_chunks + 3) / 4 * 4;
-    return round256(heads * g * d * nc4 * 4) + 2 * round256(heads * g * nc4 * 4) + round256(heads * 4) + heads * 256;
+    return round256(heads * g * d * nc4 * 4) + 2 * round256(heads * g * nc4 * 4);
+}
+__host__ __device__ inline int64_t partials_bytes(int64_t heads, int n_chunks, int g, int d) {
+    return counter_bytes(heads) + partial_state_bytes(heads, n_chunks, g, d);
 }
 
-__host__ __device__ inline Partials make_partials(void *ws, int64_t heads, int n_chunks, int g, int d) {
+// counters: a region of counter_bytes(heads_cap) bytes (heads_cap >= heads)
+// laid out as the counters of heads_cap heads; states: the partial states.
+__host__ __device__ inline Partials make_partials(void *counters, int64_t heads_cap, void *states, int64_t heads,
+                                                  int n_chunks, int g, int d) {
     Partials p;
     p.nc = n_chunks;
     p.nc4 = (n_chunks + 3) / 4 * 4;
     p.g = g;
     p.d = d;
-    char *c = (char *)ws;
+    p.counters = (unsigned int *)counters;
+    p.claims = (unsigned int *)((char *)counters + round256(heads_cap * 4));
+    char *c = (char *)states;
     p.o = (float *)c;
     c += round256(heads * g * d * p.nc4 * 4);
     p.m = (float *)c;
     c += round256(heads * g * p.nc4 * 4);
     p.l = (float *)c;
-    c += round256(heads * g * p.nc4 * 4);
-    p.counters = (unsigned int *)c;
-    c += round256(heads * 4);
-    p.claims = (unsigned int *)c;
     return p;
+}
+// A caller's workspace: the counters of `heads` heads, then the states.
+__host__ __device__ inline Partials make_partials(void *ws, int64_t heads, int n_chunks, int g, int d) {
+    return make_partials(ws, heads, (char *)ws + counter_bytes(heads), heads, n_chunks, g, d);
 }
 
 // ---- combine: Eq. (5) across the chunks of one head, then normalize -----------

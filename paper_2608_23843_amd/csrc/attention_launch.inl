@@ -33,11 +33,10 @@ static void launch_generic(const LaunchCtx &L, const LayerPtrs &p, const AttnPla
                        p.factor, (const TD *)q, seq, plan.pages_per_chunk, plan.n_chunks, pp, out, lse);
 }
 
-hipError_t launch_attention(const LaunchCtx &L, const AttnPlan &plan, const void *q, const SeqArgs &seq,
-                            float *out, float *lse, void *ws) {
+static hipError_t launch_attention_pp(const LaunchCtx &L, const AttnPlan &plan, const void *q, const SeqArgs &seq,
+                                      float *out, float *lse, const Partials &pp) {
     LayerPtrs p = layer_ptrs(L);
     const Geo &g = L.geo;
-    const Partials pp = make_partials(ws, (int64_t)g.B * g.Hkv, plan.n_chunks, g.g, g.d);
     if (plan.use_mfma) return launch_attn_mfma(L, plan, (const uint16_t *)q, seq, pp, out, lse);
     if (g.key_t) return hipErrorInvalidValue;   // pre-RoPE keys: matrix-core kernel only
     const bool db = g.dense_dtype == PKV_BF16, fb = g.factor_dtype == PKV_BF16;
@@ -46,6 +45,13 @@ hipError_t launch_attention(const LaunchCtx &L, const AttnPlan &plan, const void
     else if (fb) launch_generic<float, uint16_t>(L, p, plan, q, seq, pp, out, lse);
     else launch_generic<float, float>(L, p, plan, q, seq, pp, out, lse);
     return hipGetLastError();
+}
+
+hipError_t launch_attention(const LaunchCtx &L, const AttnPlan &plan, const void *q, const SeqArgs &seq,
+                            float *out, float *lse, void *ws) {
+    const Geo &g = L.geo;
+    return launch_attention_pp(L, plan, q, seq, out, lse,
+                               make_partials(ws, (int64_t)g.B * g.Hkv, plan.n_chunks, g.g, g.d));
 }
 
 }  // namespace pkv

@@ -507,7 +507,7 @@ __device__ inline pkv_page unpack_entry(uint2 ent) {
     e.kind = (uint8_t)(meta & 0xffu);
     e.rank_k = (uint8_t)((meta >> 8) & 0xffu);
     e.rank_v = (uint8_t)((meta >> 16) & 0xffu);
-    e.flags = 0;
+    e.rows = 0;
     return e;
 }
 
@@ -589,7 +589,9 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
         // wait for every load issued before it
         asm volatile("" : "+v"(k));
         Claim c;
-        c.j = (int64_t)__builtin_amdgcn_readfirstlane(k);
+        // the claim word is unsigned: widened as such, a stale or wrapped
+        // value can only fail the range check, never index below the table
+        c.j = (int64_t)(uint32_t)__builtin_amdgcn_readfirstlane((int)k);
         c.raw = c.j < n_pages ? tab[c.j] : make_uint2(0u, 0u);
         return c;
     };
@@ -636,6 +638,7 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
                     if (e.kind == PKV_DENSE) {
                         const unsigned int di = atomicAdd(&s_nd, 1u);
                         if (di < (unsigned int)kQ4DenseStage) s_dense[di] = (int)j;
+                        else raise_status(PKV_DEV_BAD_PAGE);   // more dense pages than a head can hold
                     } else {
                         raise_status(PKV_DEV_BAD_PAGE);
                     }

@@ -41,14 +41,49 @@ inline LayerPtrs layer_ptrs(const LaunchCtx &L) {
     return p;
 }
 
-__device__ inline void write_entry(pkv_page *e, int slot, int kind, int rk, int rv) {
+// rows: tokens a DENSE page holds (1..P); 0 for other kinds.
+__device__ inline void write_entry(pkv_page *e, int slot, int kind, int rk, int rv, int rows = 0) {
     pkv_page v;
     v.slot = slot;
     v.kind = (uint8_t)kind;
     v.rank_k = (uint8_t)rk;
     v.rank_v = (uint8_t)rv;
-    v.flags = 0;
+    v.rows = (uint8_t)rows;
     *e = v;
+}
+
+// Whether logical page j of (sequence, KV head) `head` may be factorized now
+// (Section 3.3, "Incremental Cache Update": a page is converted once, when it
+// is complete and has left the local window; sink pages stay dense). It must
+// be DENSE and hold P rows, lie outside the sink, and the cache must already
+// hold token (j + 1) P + W - 1, i.e. at least W tokens past the page. Returns
+// 0, or the status bit that refuses it.
+__device__ inline unsigned int compress_refusal(const Geo &g, const pkv_page *table, int64_t head, int j) {
+    const pkv_page e = table[head * g.max_pages + j];
+    if (e.kind != PKV_DENSE) return PKV_DEV_NOT_DENSE;
+    if (j < g.sink_pages || e.rows < g.P) return PKV_DEV_NOT_ELIGIBLE;
+    const int64_t m = (int64_t)(j + 1) * g.P + g.W - 1;
+    const int64_t jm = m / g.P;
+    if (jm >= g.max_pages) return PKV_DEV_NOT_ELIGIBLE;
+    const pkv_page em = table[head * g.max_pages + jm];
+    const bool held = em.kind == PKV_FACTOR || (em.kind == PKV_DENSE && (int64_t)em.rows > m % g.P);
+    return held ? 0u : PKV_DEV_NOT_ELIGIBLE;
+}
+
+// Whether the dense slot of page j is held by another DENSE page of the head
+// (a page that maps to the same ring position). Every thread of the
+// workgroup scans a share of those pages; the result is the workgroup's.
+__device__ inline bool dense_slot_taken(const Geo &g, const pkv_page *table, int64_t head, int j) {
+    __shared__ int s_taken;
+    if (threadIdx.x == 0) s_taken = 0;
+    __syncthreads();
+    if (j >= g.sink_pages) {
+        const int first = g.sink_pages + (j - g.sink_pages) % g.ring_len;
+        for (int jj = first + (int)threadIdx.x * g.ring_len; jj < g.max_pages; jj += (int)blockDim.x * g.ring_len)
+            if (jj != j && table[head * g.max_pages + jj].kind == PKV_DENSE) s_taken = 1;
+    }
+    __syncthreads();
+    return s_taken != 0;
 }
 
 // ---- reset ------------------------------------------------------------------
@@ -125,7 +160,7 @@ __global__ __launch_bounds__(256) void k_prefill_pages(Geo g, pkv_page *table, c
     const TE *sK = k + (head * src_tokens + t0) * g.d;
     const TE *sV = v + (head * src_tokens + t0) * g.d;
     copy_dense_page<TE>(g, sK, sV, g.d, rows, (TE *)(dense + slot * g.dense_slot_bytes));
-    if (threadIdx.x == 0) write_entry(e, slot, PKV_DENSE, 0, 0);
+    if (threadIdx.x == 0) write_entry(e, slot, PKV_DENSE, 0, 0, rows);
 }
 
 hipError_t launch_prefill_pages(const LaunchCtx &L, const void *k, const void *v, int64_t src_tokens,
@@ -183,7 +218,10 @@ __global__ void k_append(Geo g, pkv_page *table, char *dense, const T *k_new, co
         K[(int64_t)row * g.d + i] = kn[i];
         Vt[(int64_t)i * g.P + row] = vn[i];
     }
-    if (row == 0 && threadIdx.x == 0) write_entry(e, slot, PKV_DENSE, 0, 0);
+    if (threadIdx.x == 0) {
+        if (row == 0) write_entry(e, slot, PKV_DENSE, 0, 0, 1);
+        else e->rows = (uint8_t)(row + 1);
+    }
 }
 
 hipError_t launch_append(const LaunchCtx &L, const void *k_new, const void *v_new, const SeqArgs &pos) {
@@ -206,7 +244,8 @@ __global__ void k_compress_commit(Geo g, pkv_page *table, CompressItems items) {
     if (i >= items.n) return;
     const CompressItem it = items.it[i];
     const int64_t idx = g.head_index(it.b, it.h) * g.max_pages + it.j;
-    if (table[idx].kind == PKV_DENSE) {
+    // the same test the decompositions made: a refused page stays as it is
+    if (compress_refusal(g, table, g.head_index(it.b, it.h), it.j) == 0u) {
         // a requested rank of 0 was chosen by the decomposition and stored in the entry
         const pkv_page cur = table[idx];
         write_entry(table + idx, (int)idx, PKV_FACTOR, it.rk ? it.rk : cur.rank_k, it.rv ? it.rv : cur.rank_v);
@@ -229,10 +268,14 @@ __global__ __launch_bounds__(256) void k_import(Geo g, pkv_page *table, char *de
     pkv_page *e = table + head * g.max_pages + it.j;
     const int P = g.P, d = g.d;
     if (it.kind == PKV_DENSE) {
+        if (dense_slot_taken(g, table, head, it.j)) {
+            if (threadIdx.x == 0) raise_status(PKV_DEV_RING_OVERRUN);
+            return;
+        }
         const TD *s = (const TD *)src + it.src_off;
         const int slot = (int)(head * g.dslots + g.dense_ring_slot(it.j));
         copy_dense_page<TD>(g, s, s + (int64_t)P * d, d, P, (TD *)(dense + slot * g.dense_slot_bytes));
-        if (threadIdx.x == 0) write_entry(e, slot, PKV_DENSE, 0, 0);
+        if (threadIdx.x == 0) write_entry(e, slot, PKV_DENSE, 0, 0, P);
         return;
     }
     const int rk = it.rk, rv = it.rv, rk4 = r4(rk), rv4 = r4(rv);

@@ -34,9 +34,10 @@ template <typename TF> struct is_q4 { static constexpr bool value = false; };
 template <> struct is_q4<q4_t> { static constexpr bool value = true; };
 
 // One decomposition of a compress or prefill launch: which page, which half
-// (K or V), its ranks and where its P x d values are. A page that is not
-// dense (compress mode) raises PKV_DEV_NOT_DENSE when `report` is set and
-// leaves the decomposition inactive.
+// (K or V), its ranks and where its P x d values are. A page that may not be
+// factorized now (compress mode: not dense, incomplete, in the sink or still
+// inside the window) raises its status bit when `report` is set and leaves
+// the decomposition inactive.
 struct DecompRef {
     bool active;
     int b, h, j, rk, rv, which;
@@ -57,9 +58,11 @@ __device__ inline DecompRef decode_decomp(const Geo &g, const pkv_page *table, c
     if (src.mode == SRC_CACHE) {
         const CompressItem it = items.it[item];
         r.b = it.b; r.h = it.h; r.j = it.j; r.rk = it.rk; r.rv = it.rv;
-        const pkv_page e = table[g.head_index(r.b, r.h) * g.max_pages + r.j];
-        if (e.kind != PKV_DENSE) {
-            if (report) raise_status(PKV_DEV_NOT_DENSE);
+        const int64_t head = g.head_index(r.b, r.h);
+        const pkv_page e = table[head * g.max_pages + r.j];
+        const unsigned int refusal = compress_refusal(g, table, head, r.j);
+        if (refusal) {
+            if (report) raise_status(refusal);
             r.active = false;
         } else {
             const TX *slot = (const TX *)(dense + e.slot * g.dense_slot_bytes);

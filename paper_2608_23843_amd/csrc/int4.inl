@@ -289,11 +289,15 @@ __global__ __launch_bounds__(256) void k_import_q4(Geo g, pkv_page *table, char 
     const int64_t head = g.head_index(it.b, it.h);
     pkv_page *e = table + head * g.max_pages + it.j;
     if (it.kind == PKV_DENSE) {
+        if (dense_slot_taken(g, table, head, it.j)) {
+            if (threadIdx.x == 0) raise_status(PKV_DEV_RING_OVERRUN);
+            return;
+        }
         const uint16_t *s = (const uint16_t *)src + it.src_off;
         const int slot = (int)(head * g.dslots + g.dense_ring_slot(it.j));
         copy_dense_page<uint16_t>(g, s, s + (int64_t)g.P * g.d, g.d, g.P,
                                   (uint16_t *)(dense + slot * g.dense_slot_bytes));
-        if (threadIdx.x == 0) write_entry(e, slot, PKV_DENSE, 0, 0);
+        if (threadIdx.x == 0) write_entry(e, slot, PKV_DENSE, 0, 0, g.P);
         return;
     }
     const int slot = (int)(head * g.max_pages + it.j);

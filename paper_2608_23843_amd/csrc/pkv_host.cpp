@@ -358,6 +358,8 @@ pkv_status pkv_compress_pages(const pkv_cache *c, int32_t layer, int32_t n, cons
         if (rank_k[i] < rmin || rank_v[i] < rmin || rank_k[i] > rmax || rank_v[i] > rmax)
             return fail(PKV_E_RANK, "page ref %d: ranks (%d, %d) outside %d..%d", i, rank_k[i], rank_v[i], rmin,
                         rmax);
+        if (page[i] < ceil_div(c->sink_tokens, c->page_size))
+            return fail(PKV_E_STATE, "page ref %d: page %d is a sink page, which stays dense", i, page[i]);
         keys[i] = ((int64_t)b[i] * c->n_kv_heads + kv_head[i]) * c->max_pages + page[i];
     }
     std::vector<int64_t> sorted = keys;
@@ -422,6 +424,20 @@ pkv_status pkv_import_pages(const pkv_cache *c, int32_t layer, int32_t n, const 
         return fail(PKV_E_ARG, "NULL argument");
     const int rmax = std::min(c->max_rank, std::min(c->page_size, c->head_dim));
     LaunchCtx L = ctx(c, layer, s);
+    // two dense pages of one head on one ring slot in this call: the kernels
+    // of one launch cannot see each other's entries, so this is checked here
+    {
+        std::vector<int64_t> slots;
+        for (int x = 0; x < n; ++x) {
+            if (kind[x] != PKV_DENSE || b[x] < 0 || b[x] >= c->batch || kv_head[x] < 0 ||
+                kv_head[x] >= c->n_kv_heads || page[x] < 0 || page[x] >= c->max_pages)
+                continue;   // reported below
+            slots.push_back(L.geo.head_index(b[x], kv_head[x]) * L.geo.dslots + L.geo.dense_ring_slot(page[x]));
+        }
+        std::sort(slots.begin(), slots.end());
+        if (std::adjacent_find(slots.begin(), slots.end()) != slots.end())
+            return fail(PKV_E_ARG, "two dense pages of one head map to the same dense slot in one import");
+    }
     for (int base = 0; base < n; base += kCopyItemsPerLaunch) {
         CopyItems items{};
         items.n = std::min(kCopyItemsPerLaunch, n - base);

@@ -126,15 +126,22 @@ def test_call_errors_before_any_launch(pk):
                                   P(u8(4, 4)), None, 0, None) == 1
     assert lib.pkv_compress_pages(c, 0, 2, P(b), P(h), P(i32(2, 8)), P(u8(4, 4)), P(u8(4, 4)), None, 0,
                                   None) == 1
+    # compress a sink page: refused on the host, the sink stays dense
+    assert lib.pkv_compress_pages(c, 0, 2, P(b), P(h), P(i32(0, 3)), P(u8(4, 4)), P(u8(4, 4)), None, 0,
+                                  None) == 4
     # append beyond the table; prefill with a length beyond the source
     assert lib.pkv_append_kv(c, 0, vp(0x2000), vp(0x2000), P(i32(8 * 64, 0)), None) == 2
     assert lib.pkv_prefill(c, 0, vp(0x2000), vp(0x2000), 100, P(i32(101, 5)), None, None, 4, 4, None, 0,
                            None) == 2
     assert lib.pkv_prefill(c, 0, vp(0x2000), vp(0x2000), 100, P(i32(50, 5)), None, None, 0, 4, None, 0,
                            None) == 3
-    # import: bad kind
+    # import: bad kind; two dense pages of one head on one ring slot (P = 64,
+    # one sink page, a ring of 256 / 64 + 2 = 6 slots: pages 1 and 7)
     assert lib.pkv_import_pages(c, 0, 1, P(i32(0)), P(i32(0)), P(i32(0)), P(u8(7)), P(u8(0)), P(u8(0)),
                                 vp(0x2000), P(np.zeros(1, dtype=np.int64)), None, 0, None) == 1
+    assert lib.pkv_import_pages(c, 0, 2, P(i32(1, 1)), P(i32(0, 0)), P(i32(1, 7)), P(u8(1, 1)), P(u8(0, 0)),
+                                P(u8(0, 0)), vp(0x2000), P(np.zeros(2, dtype=np.int64)), None, 0, None) == 1
+    assert "same dense slot" in lib.pkv_last_error().decode()
 
 
 @pytest.mark.parametrize("kw,code", [(dict(adaptive_rank_error=1.0), 1), (dict(adaptive_rank_error=-0.1), 1),

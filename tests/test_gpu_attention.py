@@ -236,3 +236,48 @@ def test_random_geometries(case):
         if T == 0:
             assert np.all(out[b] == 0) and np.all(np.isneginf(lse[b]))
     _assert_close(out, ref, lse, rl)
+
+
+def test_workspace_reuse_across_chunk_counts():
+    """One workspace serves calls whose lengths give different chunk counts
+    (at B = 1, 8 KV heads, P = 32 a head of 1,000 tokens splits into 32
+    chunks, one of 1,100 tokens into 18): the counters sit at a fixed offset,
+    so every call matches a call on a fresh workspace and the oracle, and the
+    counters read zero afterwards."""
+    import torch
+    import paper_2608_23843_amd as pk
+    B, Hkv, g, d, P, S, W, r = 1, 8, 4, 128, 32, 32, 32, 16
+    lens = (1000, 1100)
+    wl = _workload(B, Hkv, g, d, P, max(lens), S, W, 8, "bf16", wid=93)
+    caches, refs = [], []
+    q = synth.queries(wl, 0)
+    qt = torch.from_numpy(q).to(device="cuda", dtype=torch.bfloat16).contiguous()
+    for T in lens:
+        max_pages = -(-max(lens) // P)
+        cache = pk.PuzzleKVCache(1, B, Hkv, Hkv * g, d, P, max_pages, r, S, W, "bf16", "bf16")
+        ref = np.zeros((B, Hkv * g, d))
+        for h in range(Hkv):
+            K, V = synth.kv_head(wl, 0, 0, 0, h, max_pages * P)
+            pages = build_head_pages(K.astype(np.float64), V.astype(np.float64), T, P, S, W, r, "bf16")
+            import_head(cache, 0, 0, h, pages)
+            ref[0, h * g:(h + 1) * g], _ = oracle.attention(oracle_head(T, P, d, pages),
+                                                            q[0, h * g:(h + 1) * g].astype(np.float64))
+        caches.append(cache)
+        refs.append(ref)
+    sizes = [caches[0].workspace_bytes(pk.PKV_OP_ATTENTION, T) for T in lens]
+    assert sizes[0] != sizes[1], "the two lengths must give different partial layouts"
+    ws = caches[0].workspace(pk.PKV_OP_ATTENTION, 4096)
+    for rep in range(2):
+        for cache, T, ref in zip(caches, lens, refs):
+            out, lse = cache.attention(0, qt, [T], workspace=ws)
+            fresh, lse_f = cache.attention(0, qt, [T], workspace=cache.workspace(pk.PKV_OP_ATTENTION, T))
+            torch.cuda.synchronize()
+            assert cache.device_status() == 0
+            o = out.cpu().numpy().astype(np.float64)
+            assert float((out - fresh).abs().max()) <= 1e-5 * float(fresh.abs().max())
+            assert float((lse - lse_f).abs().max()) <= 1e-5
+            ma, mr = errors(o, ref)
+            assert ma <= MAX_ABS and mr <= MEAN_REL, (T, rep, ma, mr)
+    heads = B * Hkv
+    counters = (4 * heads + 255) // 256 * 256 + 256 * heads
+    assert int(ws[:counters].count_nonzero()) == 0

@@ -461,3 +461,85 @@ def test_random_geometries_matrix_core(case):
         for L, Rm, X in ((Lk, Rk, K[b, h, j * P:(j + 1) * P]), (Lv, Rv, V[b, h, j * P:(j + 1) * P])):
             _check_factor(L[:, :r], Rm[:r], X.astype(np.float64), r, *tols)
             assert np.all(L[:, r:] == 0) and np.all(Rm[r:] == 0)
+
+
+def test_compress_refuses_pages_not_yet_eligible():
+    """A page is factorized once, when it is complete and has left the window
+    (Section 3.3, "Incremental Cache Update"). The page table records the rows
+    each dense page holds (bit-exact against the plan at every step); a sink
+    page is refused on the host (PKV_E_STATE), the current partial page and a
+    complete page still inside the window raise PKV_DEV_NOT_ELIGIBLE and stay
+    exactly as they were, and the same page is accepted once it has left."""
+    import torch
+    import paper_2608_23843_amd as pk
+    B, Hkv, d, P, S, W, r = 1, 2, 128, 64, 64, 128, 16
+    T0, steps = 64 * 4 + 10, 70
+    wl = synth.Workload("c", 97, B, Hkv, Hkv, d, P, T0, S, W, 24, (r,), "bf16", 5e5, 4, decode_steps=steps)
+    K, V = synth.kv_layer(wl, 0, 0)
+    max_pages = -(-(T0 + steps) // P) + 1
+    cache = pk.PuzzleKVCache(1, B, Hkv, Hkv, d, P, max_pages, 32, S, W, "bf16", "bf16")
+    kt = torch.from_numpy(K[:, :, :T0]).to("cuda", torch.bfloat16).contiguous()
+    vt = torch.from_numpy(V[:, :, :T0]).to("cuda", torch.bfloat16).contiguous()
+    cache.prefill(0, kt, vt, [T0] * B, default_rank=(r, r))
+
+    def rows_ok(T):
+        t = cache.page_table(0).cpu().numpy()
+        plan = oracle.plan_pages(T, P, S, W, max_pages)
+        want = np.array([min(P, T - j * P) if plan[j] == oracle.DENSE else 0 for j in range(max_pages)])
+        return np.array_equal(t[..., 4], np.broadcast_to(plan, t[..., 4].shape)) and \
+            np.array_equal(t[..., 7], np.broadcast_to(want, t[..., 7].shape))
+
+    assert rows_ok(T0)
+    with pytest.raises(pk.PuzzleKVError, match="PKV_E_STATE"):
+        cache.compress_pages(0, [0], [0], [0], [r], [r])
+    done = set()
+    for t in range(T0, T0 + steps):
+        kn = torch.from_numpy(K[:, :, t]).to("cuda", torch.bfloat16).contiguous()
+        vn = torch.from_numpy(V[:, :, t]).to("cuda", torch.bfloat16).contiguous()
+        cache.append(0, kn, vn, [t] * B)
+        T = t + 1
+        plan = oracle.plan_pages(T, P, S, W, max_pages)
+        cur = (T - 1) // P                       # the page holding the newest token
+        probes = [cur]                           # incomplete unless T is a multiple of P
+        probes += [j for j in range(1, cur) if plan[j] == oracle.DENSE and j not in done]
+        for j in sorted(set(probes)):
+            if plan[j] == oracle.FACTOR:
+                continue
+            before = cache.page_table(0).clone()
+            cache.compress_pages(0, [0], [1], [j], [r], [r])
+            assert cache.device_status() == pk._lib.PKV_DEV_NOT_ELIGIBLE, (T, j)
+            assert torch.equal(before, cache.page_table(0)), (T, j)
+        for j in oracle.eligible_pages(t, T, P, S, W):
+            cache.compress_pages(0, [0, 0], [0, 1], [int(j)] * 2, [r, r], [r, r])
+            assert cache.device_status() == 0, (T, j)
+            done.add(int(j))
+        assert rows_ok(T), T
+    assert done, "the run must cross a window boundary"
+
+
+def test_import_refuses_two_dense_pages_on_one_slot():
+    """Dense pages of one head live in a ring of ceil(W/P) + 2 slots: importing
+    pages j and j + ring length together is refused on the host; importing the
+    second while the first is still dense raises PKV_DEV_RING_OVERRUN and
+    leaves the slot and the entry untouched."""
+    import torch
+    import paper_2608_23843_amd as pk
+    P, d, S, W = 16, 64, 16, 32
+    cache = pk.PuzzleKVCache(1, 1, 1, 1, d, P, 16, 4, S, W, "f32", "f32")
+    ring = -(-W // P) + 2
+    a = torch.full((2 * P * d,), 1.0, device="cuda")
+    bsrc = torch.full((2 * P * d,), 2.0, device="cuda")
+    with pytest.raises(pk.PuzzleKVError, match="PKV_E_ARG"):
+        cache.import_pages(0, [0, 0], [0, 0], [1, 1 + ring], [oracle.DENSE] * 2, [0, 0], [0, 0],
+                           torch.cat([a, bsrc]), [0, 2 * P * d])
+    cache.import_pages(0, [0], [0], [1], [oracle.DENSE], [0], [0], a, [0])
+    assert cache.device_status() == 0
+    before = cache.page_table(0).clone()
+    pool = cache.dense_pool.clone()
+    cache.import_pages(0, [0], [0], [1 + ring], [oracle.DENSE], [0], [0], bsrc, [0])
+    assert cache.device_status() == pk._lib.PKV_DEV_RING_OVERRUN
+    assert torch.equal(before, cache.page_table(0))
+    assert torch.equal(pool, cache.dense_pool)
+    # the same page imported again replaces itself
+    cache.import_pages(0, [0], [0], [1], [oracle.DENSE], [0], [0], bsrc, [0])
+    assert cache.device_status() == 0

@@ -267,3 +267,49 @@ def test_int4_compress_then_attention():
     out, ref = _attend(c4, wl, seq, heads, g)
     ma, mr = errors(out, ref)
     assert ma <= MAX_ABS and mr <= MEAN_REL, (ma, mr)
+
+
+def test_int4_workspace_reuse_across_chunk_counts():
+    """INT4 kernel: one workspace serves calls whose lengths give different
+    chunk counts (B = 1, 8 KV heads: 2,000 tokens split into 32 chunks, 2,100
+    into 17); every call matches a call on a fresh workspace and the oracle,
+    and the claim and merge counters read zero afterwards."""
+    import torch
+    import paper_2608_23843_amd as pk
+    B, Hkv, g, S, W = 1, 8, 8, 64, 128
+    lens = (2000, 2100)
+    wl = _wl(B, Hkv, g, max(lens), S, W, seed_wid=96)
+    max_pages = -(-max(lens) // P)
+    caches, heads_of = [], []
+    for T in lens:
+        cache = pk.PuzzleKVCache(1, B, Hkv, Hkv * g, D, P, max_pages, 32, S, W, "bf16", "int4")
+        heads = {}
+        for h in range(Hkv):
+            K, V = synth.kv_head(wl, 0, 0, 0, h, max_pages * P)
+            pages, blobs = _encode_head(_bf16(K), _bf16(V), T, S, W, lambda j: (24, 16))
+            _import(cache, 0, h, pages, blobs)
+            heads[(0, h)] = oracle.HeadCache(T, P, D, pages)
+        caches.append(cache)
+        heads_of.append(heads)
+    sizes = [caches[0].workspace_bytes(pk.PKV_OP_ATTENTION, T) for T in lens]
+    assert sizes[0] != sizes[1], "the two lengths must give different partial layouts"
+    q = synth.queries(wl, 0)
+    qt = torch.from_numpy(q).to(device="cuda", dtype=torch.bfloat16).contiguous()
+    ws = caches[0].workspace(pk.PKV_OP_ATTENTION, 4096)
+    for rep in range(2):
+        for cache, T, heads in zip(caches, lens, heads_of):
+            out, lse = cache.attention(0, qt, [T], workspace=ws)
+            fresh, lse_f = cache.attention(0, qt, [T], workspace=cache.workspace(pk.PKV_OP_ATTENTION, T))
+            torch.cuda.synchronize()
+            assert cache.device_status() == 0
+            assert float((out - fresh).abs().max()) <= 1e-5 * float(fresh.abs().max())
+            assert float((lse - lse_f).abs().max()) <= 1e-5
+            o = out.cpu().numpy().astype(np.float64)
+            ref = np.zeros_like(o)
+            for (b, h), head in heads.items():
+                ref[b, h * g:(h + 1) * g], _ = oracle.attention(head, q[b, h * g:(h + 1) * g].astype(np.float64))
+            ma, mr = errors(o, ref)
+            assert ma <= MAX_ABS and mr <= MEAN_REL, (T, rep, ma, mr)
+    heads = B * Hkv
+    counters = (4 * heads + 255) // 256 * 256 + 256 * heads
+    assert int(ws[:counters].count_nonzero()) == 0
