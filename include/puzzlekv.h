@@ -264,6 +264,26 @@ pkv_status pkv_mixed_decode_attention(const pkv_cache *c, int32_t layer, const v
                                       const int32_t *seq_len, float *out, float *lse, void *ws,
                                       size_t ws_bytes, pkv_stream s);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same
+ * attention as pkv_mixed_decode_attention, same arguments and results, with
+ * no workspace argument. Its counters and partial states live in a static
+ * device array of PKV_NOALLOC_SCRATCH_BYTES bytes that the library holds on
+ * each GPU it runs on until the process ends; it calls no allocator. The
+ * array keeps the last call's contents: its counter region (laid out for
+ * PKV_NOALLOC_MAX_HEADS (sequence, KV head) pairs) is cleared by a kernel on
+ * the caller's stream at the first call on a device, and every call returns
+ * it to zero. All calls on one GPU share the array, so calls that overlap on
+ * one GPU (different streams, or different threads without ordering) race
+ * and must not be made. Returns PKV_E_WORKSPACE, before anything is
+ * enqueued, when batch * n_kv_heads exceeds PKV_NOALLOC_MAX_HEADS or the
+ * call's partial states do not fit beside the counters (then use
+ * pkv_mixed_decode_attention with a workspace). */
+#define PKV_NOALLOC_SCRATCH_BYTES (16ll << 20)
+#define PKV_NOALLOC_MAX_HEADS 2048
+pkv_status pkv_mixed_decode_attention_noalloc(const pkv_cache *c, int32_t layer, const void *q,
+                                              const int32_t *seq_len, float *out, float *lse, pkv_stream s);
+
 /* ---- import / export of pages in the logical layout ---------------------
  * Logical page block, row-major:
  *   DENSE : K (P x d), V (P x d)

@@ -191,6 +191,20 @@ class PuzzleKVCache:
               "pkv_mixed_decode_attention")
         return out, lse
 
+    def attention_noalloc(self, layer, q, seq_len, out, lse=None, stream=None):
+        """pkv_mixed_decode_attention_noalloc: the same attention into caller
+        buffers out (batch, n_q_heads, d) fp32 and lse (batch, n_q_heads) fp32
+        or None, with the library's static scratch instead of a workspace."""
+        c = self.c
+        assert q.is_contiguous() and q.dtype == self.qdtype and tuple(q.shape) == (c.batch, c.n_q_heads, c.head_dim)
+        assert out.is_contiguous() and out.dtype == self.torch.float32 and out.numel() == c.batch * c.n_q_heads * c.head_dim
+        seq = _i32(seq_len, c.batch)
+        check(self.lib.pkv_mixed_decode_attention_noalloc(ctypes.byref(c), layer, q.data_ptr(), _np_ptr(seq),
+                                                          out.data_ptr(), None if lse is None else lse.data_ptr(),
+                                                          _stream_handle(self.torch, stream)),
+              "pkv_mixed_decode_attention_noalloc")
+        return out, lse
+
     def import_pages(self, layer, b, h, page, kind, rank_k, rank_v, src, src_offset, stream=None):
         """src: device 1-D tensor (dense dtype for dense pages, factor dtype for factors)."""
         b, h, page = _i32(b), _i32(h), _i32(page)

@@ -22,7 +22,8 @@ EXPORTS = [
     "pkv_cache_check", "pkv_dense_slots_per_head", "pkv_dense_slot_bytes", "pkv_factor_slot_bytes",
     "pkv_dense_pool_bytes", "pkv_factor_pool_bytes", "pkv_page_table_bytes", "pkv_factor_page_bytes",
     "pkv_workspace_bytes", "pkv_plan_pages", "pkv_eligible_pages", "pkv_cache_reset", "pkv_prefill",
-    "pkv_append_kv", "pkv_compress_pages", "pkv_mixed_decode_attention", "pkv_import_pages",
+    "pkv_append_kv", "pkv_compress_pages", "pkv_mixed_decode_attention", "pkv_mixed_decode_attention_noalloc",
+    "pkv_import_pages",
     "pkv_export_block_elems", "pkv_export_pages", "pkv_int4_blob_bytes", "pkv_export_int4_pages",
     "pkv_device_status", "pkv_compress_sweeps", "pkv_cache_bytes", "pkv_last_error", "pkv_version",
 ]
@@ -81,6 +82,7 @@ def load():
         "pkv_append_kv": ([cp, i32, vp, vp, vp, vp], i32),
         "pkv_compress_pages": ([cp, i32, i32, vp, vp, vp, vp, vp, vp, sz, vp], i32),
         "pkv_mixed_decode_attention": ([cp, i32, vp, vp, vp, vp, vp, sz, vp], i32),
+        "pkv_mixed_decode_attention_noalloc": ([cp, i32, vp, vp, vp, vp, vp], i32),
         "pkv_import_pages": ([cp, i32, i32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp], i32),
         "pkv_export_block_elems": ([cp], i64),
         "pkv_export_pages": ([cp, i32, i32, vp, vp, vp, vp, vp, sz, vp], i32),

@@ -24,6 +24,11 @@ int64_t attention_workspace_bytes(const Geo &g, int64_t max_T) {
     return partials_bytes((int64_t)g.B * g.Hkv, p.n_chunks, g.g, g.d);
 }
 
+int64_t attention_state_bytes(const Geo &g, int64_t max_T) {
+    const AttnPlan p = attention_plan(g, max_T);
+    return partial_state_bytes((int64_t)g.B * g.Hkv, p.n_chunks, g.g, g.d);
+}
+
 template <typename TD, typename TF>
 static void launch_generic(const LaunchCtx &L, const LayerPtrs &p, const AttnPlan &plan, const void *q,
                            const SeqArgs &seq, const Partials &pp, float *out, float *lse) {
@@ -52,6 +57,67 @@ hipError_t launch_attention(const LaunchCtx &L, const AttnPlan &plan, const void
     const Geo &g = L.geo;
     return launch_attention_pp(L, plan, q, seq, out, lse,
                                make_partials(ws, (int64_t)g.B * g.Hkv, plan.n_chunks, g.g, g.d));
+}
+
+// ---- attention without a caller workspace -----------------------------------
+//
+// For callers that cannot allocate (graph capture, serving loops): the
+// counters and partial states live in one static device array per GPU. Its
+// counter region is laid out for kScratchHeads heads whatever the call's
+// geometry, so calls of different batch sizes, head counts and lengths find
+// their counters at the same addresses; it is cleared once per device (first
+// call on the device, by a kernel on the caller's stream) and every call
+// returns the counters it used to zero. The partial states that follow are
+// written by each call before they are read. Calls that overlap on one GPU
+// race on this memory.
+constexpr int64_t kScratchBytes = PKV_NOALLOC_SCRATCH_BYTES;
+constexpr int64_t kScratchHeads = PKV_NOALLOC_MAX_HEADS;
+constexpr int kScratchDevices = 64;
+static_assert(kScratchBytes % 256 == 0, "scratch size");
+
+static __device__ __align__(256) char scratch[kScratchBytes];
+
+static std::mutex g_scratch_mu;
+static void *g_scratch_ptr[kScratchDevices];   // device address of `scratch`, per device
+
+__global__ void k_zero_words(unsigned int *p, int64_t n) {
+    for (int64_t i = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; i < n; i += (int64_t)gridDim.x * blockDim.x)
+        p[i] = 0u;
+}
+
+int64_t scratch_state_bytes() { return kScratchBytes - counter_bytes(kScratchHeads); }
+
+// The device address of this GPU's scratch array (set up on first use).
+static hipError_t scratch_on_device(hipStream_t stream, char **out) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kScratchDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        const int64_t words = counter_bytes(kScratchHeads) / 4;
+        hipLaunchKernelGGL(k_zero_words, dim3((unsigned)ceil_div(words, 256)), dim3(256), 0, stream,
+                           (unsigned int *)p, words);
+        e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = (char *)g_scratch_ptr[dev];
+    return hipSuccess;
+}
+
+hipError_t launch_attention_noalloc(const LaunchCtx &L, const AttnPlan &plan, const void *q, const SeqArgs &seq,
+                                    float *out, float *lse) {
+    const Geo &g = L.geo;
+    char *base = nullptr;
+    hipError_t e = scratch_on_device(L.stream, &base);
+    if (e != hipSuccess) return e;
+    const Partials pp = make_partials(base, kScratchHeads, base + counter_bytes(kScratchHeads), (int64_t)g.B * g.Hkv,
+                                      plan.n_chunks, g.g, g.d);
+    return launch_attention_pp(L, plan, q, seq, out, lse, pp);
 }
 
 }  // namespace pkv

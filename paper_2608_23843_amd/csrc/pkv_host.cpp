@@ -408,6 +408,34 @@ pkv_status pkv_mixed_decode_attention(const pkv_cache *c, int32_t layer, const v
     return check_launch(launch_attention(L, plan, q, seq, out, lse, ws), "pkv_mixed_decode_attention");
 }
 
+pkv_status pkv_mixed_decode_attention_noalloc(const pkv_cache *c, int32_t layer, const void *q,
+                                              const int32_t *seq_len, float *out, float *lse, pkv_stream s) {
+    pkv_status st = check_cache(c, true);
+    if (st != PKV_OK) return st;
+    if ((st = check_layer(c, layer)) != PKV_OK) return st;
+    if (!q || !seq_len || !out) return fail(PKV_E_ARG, "q, seq_len or out is NULL");
+    SeqArgs seq{};
+    seq.n = c->batch;
+    int64_t max_T = 0;
+    for (int b = 0; b < c->batch; ++b) {
+        if (seq_len[b] < 0 || (int64_t)seq_len[b] > (int64_t)c->max_pages * c->page_size)
+            return fail(PKV_E_SHAPE, "seq_len[%d] = %d outside 0..max_pages * P", b, seq_len[b]);
+        seq.len[b] = seq_len[b];
+        max_T = std::max<int64_t>(max_T, seq_len[b]);
+    }
+    LaunchCtx L = ctx(c, layer, s);
+    const int64_t heads = (int64_t)c->batch * c->n_kv_heads;
+    if (heads > PKV_NOALLOC_MAX_HEADS)
+        return fail(PKV_E_WORKSPACE, "batch * n_kv_heads = %lld above the static scratch's %d heads; use "
+                    "pkv_mixed_decode_attention with a workspace", (long long)heads, PKV_NOALLOC_MAX_HEADS);
+    const int64_t need = attention_state_bytes(L.geo, max_T);
+    if (need > scratch_state_bytes())
+        return fail(PKV_E_WORKSPACE, "partial states of %lld bytes above the static scratch's %lld; use "
+                    "pkv_mixed_decode_attention with a workspace", (long long)need, (long long)scratch_state_bytes());
+    AttnPlan plan = attention_plan(L.geo, max_T);
+    return check_launch(launch_attention_noalloc(L, plan, q, seq, out, lse), "pkv_mixed_decode_attention_noalloc");
+}
+
 // ---- import / export ---------------------------------------------------------
 
 pkv_status pkv_import_pages(const pkv_cache *c, int32_t layer, int32_t n, const int32_t *b,

@@ -210,6 +210,12 @@ struct AttnPlan {
 };
 AttnPlan attention_plan(const Geo &g, int64_t max_T);
 int64_t attention_workspace_bytes(const Geo &g, int64_t max_T);
+// Partial-state bytes the calls without a workspace can use, and the bytes
+// such a call needs for its geometry and longest sequence.
+int64_t scratch_state_bytes();
+int64_t attention_state_bytes(const Geo &g, int64_t max_T);
+hipError_t launch_attention_noalloc(const LaunchCtx &L, const AttnPlan &plan, const void *q, const SeqArgs &seq,
+                                    float *out, float *lse);
 hipError_t launch_attention(const LaunchCtx &L, const AttnPlan &plan, const void *q, const SeqArgs &seq,
                             float *out, float *lse, void *ws);
 

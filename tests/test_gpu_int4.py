@@ -272,8 +272,9 @@ def test_int4_compress_then_attention():
 def test_int4_workspace_reuse_across_chunk_counts():
     """INT4 kernel: one workspace serves calls whose lengths give different
     chunk counts (B = 1, 8 KV heads: 2,000 tokens split into 32 chunks, 2,100
-    into 17); every call matches a call on a fresh workspace and the oracle,
-    and the claim and merge counters read zero afterwards."""
+    into 17); every call agrees with a call on a fresh workspace to the
+    kernel's precision and with the oracle to the parity bar, and the claim
+    and merge counters read zero afterwards."""
     import torch
     import paper_2608_23843_amd as pk
     B, Hkv, g, S, W = 1, 8, 8, 64, 128
@@ -302,9 +303,14 @@ def test_int4_workspace_reuse_across_chunk_counts():
             fresh, lse_f = cache.attention(0, qt, [T], workspace=cache.workspace(pk.PKV_OP_ATTENTION, T))
             torch.cuda.synchronize()
             assert cache.device_status() == 0
-            assert float((out - fresh).abs().max()) <= 1e-5 * float(fresh.abs().max())
-            assert float((lse - lse_f).abs().max()) <= 1e-5
+            # pages reach the waves in a dynamic order, which moves the lazy
+            # max's rescale points and with them the fp16 roundings of the
+            # weights, so two calls agree only to the kernel's own precision
+            # (stale counters would give garbage or nothing at all)
             o = out.cpu().numpy().astype(np.float64)
+            ma, mr = errors(o, fresh.cpu().numpy().astype(np.float64))
+            assert ma <= 1e-3 and mr <= 1e-4, (T, rep, ma, mr)
+            assert float((lse - lse_f).abs().max()) <= 1e-4
             ref = np.zeros_like(o)
             for (b, h), head in heads.items():
                 ref[b, h * g:(h + 1) * g], _ = oracle.attention(head, q[b, h * g:(h + 1) * g].astype(np.float64))
