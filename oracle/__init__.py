@@ -168,6 +168,24 @@ def truncated_factors_batch(X: np.ndarray, ranks, max_sweeps: int = MAX_SWEEPS):
     return Lout, Rout, sig, sweeps
 
 
+def global_factors(X: np.ndarray, r: int, max_sweeps: int = MAX_SWEEPS):
+    """Global SVD, the paper's controlled baseline (Section 4.1 "Baselines";
+    Appendix "Baseline Configurations"): one basis shared by every token of the
+    compressible region X (N x d) of one KV head, the rank-r truncated SVD
+    X ~ U_r Sigma_r W_r^T stored as A = U_r Sigma_r (N x r), one coefficient
+    row per token, and B = W_r^T (r x d), the shared basis.
+
+    Computed with the same one-sided Jacobi as the page factors, applied to
+    the d rows of X^T: X^T = J Y with J (d x d) = W and the rows of Y the
+    sigma_k u_k^T, so B = J[:, :r]^T and A = Y[:r]^T. r is capped at
+    min(N, d). Returns (A, B, sig, sweeps); sig holds all d singular values."""
+    X = np.ascontiguousarray(X, dtype=np.float64)
+    N, d = X.shape
+    r = int(min(r, N, d))
+    J, sig, Y, sw = svd_rows(np.ascontiguousarray(X.T), max_sweeps)
+    return np.ascontiguousarray(Y[:r].T), np.ascontiguousarray(J[:, :r].T), sig, sw
+
+
 # --------------------------------------------------------------------------
 # Attention (Eq. (1)) and page-wise state + merge (Eq. (4), Eq. (5))
 # --------------------------------------------------------------------------
@@ -222,6 +240,31 @@ class HeadCache:
                 pos += a.size
         data = np.concatenate(chunks) if chunks else np.zeros(1)
         return kind, rk, rv, off, data
+
+
+def global_head(T: int, P: int, d: int, kinds, K: np.ndarray, V: np.ndarray, A_K: np.ndarray,
+                B_K: np.ndarray, A_V: np.ndarray, B_V: np.ndarray) -> HeadCache:
+    """The logical contents of one KV head stored by Global SVD: pages the plan
+    `kinds` keeps dense hold K, V (rows of the whole sequence, T x d) as they
+    are; the tokens of the factorized pages, in order, are the rows of A_K,
+    A_V, rebuilt with the shared bases B_K, B_V. Each such page is written as a
+    factor page (L = its rows of A, R = B), so attention over it is the same
+    textbook softmax over the rebuilt keys and values."""
+    pages, row = [], 0
+    for j, kd in enumerate(kinds):
+        if kd == FACTOR:
+            pages.append(("factor", A_K[row:row + P], B_K, A_V[row:row + P], B_V))
+            row += P
+        else:
+            Kp = np.zeros((P, d)); Vp = np.zeros((P, d))
+            n = min(P, T - j * P)
+            Kp[:n] = K[j * P:j * P + n]
+            Vp[:n] = V[j * P:j * P + n]
+            pages.append(("dense", Kp, Vp))
+    if row != A_K.shape[0] or row != A_V.shape[0]:
+        raise ValueError("coefficient rows (%d, %d) do not match the %d factorized tokens"
+                         % (A_K.shape[0], A_V.shape[0], row))
+    return HeadCache(T, P, d, pages)
 
 
 def attention(head: HeadCache, q: np.ndarray):

@@ -7,7 +7,11 @@ Plain restatements of the paper's storage formulas:
   * whole-cache ratio when some pages stay dense (Section 4.5, "Memory
     Footprint": dense pages count at ratio 1),
   * INT4 factor storage, 4-bit codes plus one fp16 scale per run of at most 32
-    elements along the direction Section 4.3 names for each factor.
+    elements along the direction Section 4.3 names for each factor,
+  * Global SVD storage (Section 4.2, "Main Results": rho_global = r (S + d) /
+    (S d) for an input of S tokens), with the rank matched to a budget
+    counting the dense sink and window tokens as well (Appendix "Baseline
+    Configurations").
 """
 from __future__ import annotations
 
@@ -58,3 +62,23 @@ def int4_cache_ratio(n_pages: int, n_dense: int, P: int, r_k: int, r_v: int, d: 
                      group: int = 32) -> float:
     rho = int4_page_ratio(P, r_k, r_v, d, group)
     return (rho * (n_pages - n_dense) + n_dense) / n_pages
+
+
+def global_storage_elems(n_dense_tokens: int, n_factor_tokens: int, d: int, r: int) -> int:
+    """Elements Global SVD stores for one KV head: K and V of the dense tokens,
+    and for each of K and V the coefficients (one r-vector per factorized
+    token) plus the shared r x d basis."""
+    return 2 * n_dense_tokens * d + 2 * r * (n_factor_tokens + d)
+
+
+def global_rank(n_dense_tokens: int, n_factor_tokens: int, d: int, rho: float) -> int:
+    """Largest rank r (same for K and V, at most min(N, d)) whose whole-head
+    storage, dense tokens included, stays within rho times the raw cache
+    (2 T d elements, T = dense + factorized tokens); 0 if even rank 1 does not fit."""
+    T = n_dense_tokens + n_factor_tokens
+    budget = rho * 2.0 * T * d
+    best = 0
+    for r in range(1, min(n_factor_tokens, d) + 1):
+        if global_storage_elems(n_dense_tokens, n_factor_tokens, d, r) <= budget:
+            best = r
+    return best

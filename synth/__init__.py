@@ -17,7 +17,11 @@ SeedSequence([seed, workload_id, tag, ...])):
     5e5 (Llama-3-8B shape) or 1e6 (Qwen3-32B shape);
   * queries: per (batch, query head) i.i.d. N(0, 1/d);
   * ranks: fixed, or uniform over a set per (layer, batch, kv head, page);
-  * storage rounding: bf16 round-to-nearest-even, or none for fp32.
+  * storage rounding: bf16 round-to-nearest-even, or none for fp32;
+  * non-stationary sequences (workloads with segment_pages != 1): the planted
+    basis W is shared by runs of segment_pages consecutive pages and drawn
+    afresh for the next run (0: one basis for the whole sequence), so the
+    subspace the keys and values live in changes every segment.
 """
 from __future__ import annotations
 
@@ -53,6 +57,8 @@ class Workload:
     ranks_v: tuple = ()     # rank choices of the value factors when they differ from the keys
     rank_error: float = 0.0  # > 0: each page's rank chosen for this relative reconstruction error
     key_rope: bool = False   # keys handed over before RoPE (the cache rotates them at access)
+    segment_pages: int = 1   # pages sharing one planted basis (0: the whole sequence)
+    global_rho: float = 0.0  # > 0: a Global SVD cache with its rank matched to this storage ratio
 
     @property
     def factors(self) -> str:
@@ -152,9 +158,14 @@ def _rope(x: np.ndarray, base: float) -> np.ndarray:
     return out
 
 
-def _low_rank_pages(g: np.random.Generator, n_pages: int, P: int, d: int, r0: int):
+def _low_rank_pages(g: np.random.Generator, n_pages: int, P: int, d: int, r0: int, seg: int = 1):
     G = g.standard_normal((n_pages, P, r0), dtype=np.float32)
-    W = g.standard_normal((n_pages, r0, d), dtype=np.float32)
+    if seg == 1:
+        W = g.standard_normal((n_pages, r0, d), dtype=np.float32)
+    else:
+        run = n_pages if seg <= 0 else seg
+        Ws = g.standard_normal((-(-n_pages // run), r0, d), dtype=np.float32)
+        W = np.repeat(Ws, run, axis=0)[:n_pages]
     N = g.standard_normal((n_pages, P, d), dtype=np.float32)
     N *= np.float32(0.05)
     N += np.matmul(G, W)
@@ -173,8 +184,8 @@ def kv_head(wl: Workload, seed: int, layer: int, b: int, h: int, tokens: int | N
     T = wl.tokens + wl.decode_steps if tokens is None else int(tokens)
     P, d = wl.page, wl.head_dim
     n_pages = -(-T // P)
-    K = _low_rank_pages(rng(seed, wl.wid, TAG_KEY, layer, b, h), n_pages, P, d, wl.r0)
-    V = _low_rank_pages(rng(seed, wl.wid, TAG_VALUE, layer, b, h), n_pages, P, d, wl.r0)
+    K = _low_rank_pages(rng(seed, wl.wid, TAG_KEY, layer, b, h), n_pages, P, d, wl.r0, wl.segment_pages)
+    V = _low_rank_pages(rng(seed, wl.wid, TAG_VALUE, layer, b, h), n_pages, P, d, wl.r0, wl.segment_pages)
     ch = outlier_channels(wl, seed, layer, h)
     if ch.size:
         K[:, ch] *= np.float32(10.0)
