@@ -50,8 +50,9 @@ typedef enum {
 /* Element types. PKV_INT4 is a factor storage type only (see below). */
 typedef enum { PKV_F32 = 0, PKV_BF16 = 1, PKV_INT4 = 2 } pkv_dtype;
 
-/* Kind of a logical page. */
-typedef enum { PKV_EMPTY = 0, PKV_DENSE = 1, PKV_FACTOR = 2 } pkv_kind;
+/* Kind of a logical page. PKV_GLOBAL: the page's tokens are rows of the
+ * head's Global SVD coefficients (pkv_global_prefill). */
+typedef enum { PKV_EMPTY = 0, PKV_DENSE = 1, PKV_FACTOR = 2, PKV_GLOBAL = 3 } pkv_kind;
 
 /* Device status bits (pkv_device_status). */
 #define PKV_DEV_NOT_DENSE     0x1u /* compress_pages found a page that is not dense   */
@@ -174,8 +175,11 @@ size_t pkv_factor_page_bytes(const pkv_cache *c, int32_t rank_k, int32_t rank_v)
 /* Workspace sizes. op PKV_OP_ATTENTION: n = longest sequence length passed to
  * pkv_mixed_decode_attention (a workspace sized for n serves every call with
  * sequences up to n tokens); PKV_OP_COMPRESS: n = pages per call;
- * PKV_OP_PREFILL: n = longest prompt length. */
-enum { PKV_OP_ATTENTION = 0, PKV_OP_COMPRESS = 1, PKV_OP_PREFILL = 2, PKV_OP_IMPORT = 3 };
+ * PKV_OP_PREFILL: n = longest prompt length; PKV_OP_GLOBAL_PREFILL and
+ * PKV_OP_GLOBAL_ATTENTION: n = longest sequence of pkv_global_prefill and
+ * pkv_global_attention. */
+enum { PKV_OP_ATTENTION = 0, PKV_OP_COMPRESS = 1, PKV_OP_PREFILL = 2, PKV_OP_IMPORT = 3,
+       PKV_OP_GLOBAL_PREFILL = 4, PKV_OP_GLOBAL_ATTENTION = 5 };
 size_t pkv_workspace_bytes(const pkv_cache *c, int32_t op, int64_t n);
 
 /* ---- page plan (host, integer; Section 3.3 and Section 4.1) ---------------
@@ -326,6 +330,76 @@ int64_t pkv_int4_blob_bytes(const pkv_cache *c, int32_t rank_k, int32_t rank_v);
  * factor page gives zeros. */
 pkv_status pkv_export_int4_pages(const pkv_cache *c, int32_t layer, int32_t n, const int32_t *b,
                                  const int32_t *kv_head, const int32_t *page, void *dst, pkv_stream s);
+
+/* ---- Global SVD baseline ----------------------------------------------------
+ * The paper's controlled baseline for compression granularity (Section 4.1
+ * "Baselines"; Section 4.2 "Main Results"; Appendix "Baseline
+ * Configurations"): for each (layer, sequence, KV head) and each of K and V,
+ * one rank-r basis shared by every token of the compressible region, which
+ * is the run of pages the plan factorizes; the sink and window pages stay
+ * dense exactly as in PuzzleKV. The region X (N x d) is stored as X ~ A B with
+ * B = W_r^T (r x d), the top-r right singular vectors of X (eigenvectors of
+ * its Gram matrix X^T X), and A = X B^T (N x r), one coefficient row per
+ * token (A = U_r Sigma_r). The dense pages and the page table live in a
+ * pkv_cache (bf16 dense pages, head_dim 128, P = 32 or 64); the factorized
+ * pages' entries get kind PKV_GLOBAL (slot = the coefficient row of the
+ * page's first token, rank_k = rank_v = r). The baseline is built from a
+ * prompt and attended at that length (append and compress_pages do not apply
+ * to it), and pkv_cache_bytes refuses its layers (PKV_E_STATE).
+ *
+ * Layout, bf16, r8 = r rounded up to a multiple of 8, per (layer, sequence,
+ * KV head) in [n_layers][batch][n_kv_heads] order:
+ *   basis: B_K (r8 x d), B_V (r8 x d), B_V^T (d x r8), row-major, entries
+ *          past rank r zero
+ *   coef:  A_K (max_tokens x r8) token-major, then A_V^T (r8 x max_tokens)
+ *          rank-major; row t of A_K (column t of A_V^T) is token t0 + t of
+ *          the region, t0 = ceil(S / P) P; entries past rank r zero
+ */
+typedef struct {
+    int32_t rank;        /* r: 1 .. 128 */
+    int32_t max_tokens;  /* coefficient rows per (layer, sequence, KV head): a positive multiple of 32 */
+    void *basis;         /* device, pkv_global_basis_bytes */
+    void *coef;          /* device, pkv_global_coef_bytes */
+} pkv_global;
+size_t pkv_global_basis_bytes(const pkv_cache *c, const pkv_global *gl);
+size_t pkv_global_coef_bytes(const pkv_cache *c, const pkv_global *gl);
+/* The rank matched to a storage budget (host, integer): the largest r in
+ * 1..min(N, d) with 2 n d + 2 r (N + d) <= rho 2 T d, where a head of T tokens
+ * keeps n of them dense (sink and window pages of the plan for T, P, S, W) and
+ * N = T - n in the region: the dense tokens count against the budget as the
+ * paper's appendix describes; with n = 0 it is the paper's
+ * rho_global = r (S + d) / (S d) <= rho. Returns 0 if no rank fits, -1 for an
+ * invalid argument. */
+int32_t pkv_global_rank(int64_t T, int32_t P, int32_t S, int32_t W, int32_t d, double rho);
+/* Builds one layer from the dense prompt cache, as pkv_prefill does for
+ * PuzzleKV: dense pages copied, and for each (sequence, KV head) and each of
+ * K and V the Gram matrix of the region on the matrix cores, its eigenvectors
+ * by one-sided Jacobi (fp32), the basis rounded to bf16 and the coefficients
+ * A = X B^T projected with that rounded basis. k, v: device
+ * [batch][n_kv_heads][src_tokens][d] bf16; seq_len: host [batch], each at
+ * most src_tokens and max_pages * P, with its region at most max_tokens rows.
+ * Workspace: pkv_workspace_bytes(PKV_OP_GLOBAL_PREFILL, max seq_len) (fp32
+ * Gram partials of 4,096-token chunks). PKV_DEV_NO_CONVERGE if an
+ * eigen-solve reaches its sweep cap (result kept). */
+pkv_status pkv_global_prefill(const pkv_cache *c, const pkv_global *gl, int32_t layer, const void *k, const void *v,
+                              int64_t src_tokens, const int32_t *seq_len, void *ws, size_t ws_bytes, pkv_stream s);
+/* Single-query GQA decode attention over a layer built by pkv_global_prefill,
+ * at the prefill lengths: per (sequence, KV head) Z = B_K q once, scores from
+ * A_K Z, Y = sum_t p_t A_V[t] in the rank space and O = Y B_V, plus the dense
+ * pages, merged by Eq. (5); coefficients are never rebuilt into K or V.
+ * Arguments, outputs and workspace conventions as pkv_mixed_decode_attention,
+ * with pkv_workspace_bytes(PKV_OP_GLOBAL_ATTENTION, max seq_len). A page the
+ * plan keeps dense that is not DENSE, or a region whose last page is not
+ * PKV_GLOBAL, raises PKV_DEV_BAD_PAGE. */
+pkv_status pkv_global_attention(const pkv_cache *c, const pkv_global *gl, int32_t layer, const void *q,
+                                const int32_t *seq_len, float *out, float *lse, void *ws, size_t ws_bytes,
+                                pkv_stream s);
+/* Reads one (sequence b, KV head h)'s factors as fp32 (device outputs):
+ * basis_k, basis_v (r x d) and coef_k, coef_v (n_rows x r, rows 0..n_rows-1
+ * of the region), n_rows <= max_tokens. */
+pkv_status pkv_global_export(const pkv_cache *c, const pkv_global *gl, int32_t layer, int32_t b, int32_t h,
+                             int64_t n_rows, float *basis_k, float *basis_v, float *coef_k, float *coef_v,
+                             pkv_stream s);
 
 /* ---- accounting ----------------------------------------------------------- */
 

@@ -13,11 +13,12 @@ import ctypes
 import numpy as np
 
 from . import _lib
-from ._lib import (PKV_BF16, PKV_DENSE, PKV_EMPTY, PKV_F32, PKV_FACTOR, PKV_INT4, PKV_OP_ATTENTION,
-                   PKV_OP_COMPRESS, PKV_OP_IMPORT, PKV_OP_PREFILL, PuzzleKVError, check)
+from ._lib import (PKV_BF16, PKV_DENSE, PKV_EMPTY, PKV_F32, PKV_FACTOR, PKV_GLOBAL, PKV_INT4, PKV_OP_ATTENTION,
+                   PKV_OP_COMPRESS, PKV_OP_GLOBAL_ATTENTION, PKV_OP_GLOBAL_PREFILL, PKV_OP_IMPORT, PKV_OP_PREFILL,
+                   PuzzleKVError, check)
 
-__all__ = ["PuzzleKVCache", "plan_pages", "eligible_pages", "load_library", "PuzzleKVError",
-           "PKV_EMPTY", "PKV_DENSE", "PKV_FACTOR", "PKV_F32", "PKV_BF16", "PKV_INT4"]
+__all__ = ["PuzzleKVCache", "GlobalSVD", "plan_pages", "eligible_pages", "global_rank", "load_library",
+           "PuzzleKVError", "PKV_EMPTY", "PKV_DENSE", "PKV_FACTOR", "PKV_GLOBAL", "PKV_F32", "PKV_BF16", "PKV_INT4"]
 
 _DTYPES = {"f32": PKV_F32, "fp32": PKV_F32, "float32": PKV_F32, "bf16": PKV_BF16, "bfloat16": PKV_BF16,
            "int4": PKV_INT4}
@@ -51,6 +52,15 @@ def eligible_pages(T_prev: int, T_new: int, P: int, S: int, W: int) -> np.ndarra
     check(lib.pkv_eligible_pages(T_prev, T_new, P, S, W, _np_ptr(out), cap, ctypes.byref(cnt)),
           "pkv_eligible_pages")
     return out[:cnt.value].copy()
+
+
+def global_rank(T: int, P: int, S: int, W: int, d: int, rho: float) -> int:
+    """pkv_global_rank: Global SVD rank whose whole-head storage (dense tokens
+    included) fits rho times the raw cache."""
+    r = int(_lib.load().pkv_global_rank(T, P, S, W, d, float(rho)))
+    if r < 0:
+        raise ValueError("pkv_global_rank: invalid argument")
+    return r
 
 
 def _stream_handle(torch, stream=None):
@@ -271,3 +281,69 @@ class PuzzleKVCache:
         check(self.lib.pkv_device_status(_stream_handle(self.torch, stream), ctypes.byref(bits)),
               "pkv_device_status")
         return int(bits.value)
+
+
+class GlobalSVD:
+    """Global SVD factors beside a PuzzleKVCache (pkv_global): one rank-r basis
+    per (layer, sequence, KV head) and K/V, shared by the tokens of the
+    compressible region; the cache's dense pool and page table hold the dense
+    pages. Buffers are allocated with torch."""
+
+    def __init__(self, cache: PuzzleKVCache, rank: int, max_tokens: int):
+        torch = cache.torch
+        self.cache, self.torch, self.lib = cache, torch, cache.lib
+        g = _lib.PkvGlobal()
+        g.rank, g.max_tokens = int(rank), int(max_tokens)
+        nb = int(self.lib.pkv_global_basis_bytes(ctypes.byref(cache.c), ctypes.byref(g)))
+        nc = int(self.lib.pkv_global_coef_bytes(ctypes.byref(cache.c), ctypes.byref(g)))
+        if nb == 0 or nc == 0:
+            raise PuzzleKVError(_lib.PKV_E_ARG, "GlobalSVD", "invalid geometry for Global SVD (rank %d, "
+                                "max_tokens %d)" % (rank, max_tokens))
+        self.basis = torch.zeros(nb, dtype=torch.uint8, device=cache.device)
+        self.coef = torch.zeros(nc, dtype=torch.uint8, device=cache.device)
+        g.basis, g.coef = self.basis.data_ptr(), self.coef.data_ptr()
+        self.g = g
+
+    def workspace(self, op: int, n: int):
+        nb = self.cache.workspace_bytes(op, n)
+        return self.torch.zeros(max(nb, 1), dtype=self.torch.uint8, device=self.cache.device)
+
+    def prefill(self, layer, k, v, seq_len, workspace=None, stream=None):
+        """k, v: device (batch, n_kv_heads, src_tokens, d) bf16."""
+        c = self.cache
+        assert k.is_contiguous() and v.is_contiguous() and k.dtype == c.qdtype
+        seq = _i32(seq_len, c.c.batch)
+        if workspace is None:
+            workspace = self.workspace(PKV_OP_GLOBAL_PREFILL, int(seq.max()) if seq.size else 0)
+        check(self.lib.pkv_global_prefill(ctypes.byref(c.c), ctypes.byref(self.g), layer, k.data_ptr(),
+                                          v.data_ptr(), k.shape[2], _np_ptr(seq), workspace.data_ptr(),
+                                          workspace.numel(), _stream_handle(self.torch, stream)),
+              "pkv_global_prefill")
+
+    def attention(self, layer, q, seq_len, out=None, lse=None, workspace=None, stream=None):
+        torch, c = self.torch, self.cache.c
+        assert q.is_contiguous() and q.dtype == self.cache.qdtype
+        seq = _i32(seq_len, c.batch)
+        if out is None:
+            out = torch.empty((c.batch, c.n_q_heads, c.head_dim), dtype=torch.float32, device=self.cache.device)
+        if lse is None:
+            lse = torch.empty((c.batch, c.n_q_heads), dtype=torch.float32, device=self.cache.device)
+        need = self.cache.workspace_bytes(PKV_OP_GLOBAL_ATTENTION, int(seq.max()) if seq.size else 0)
+        if workspace is None or workspace.numel() < need:
+            workspace = torch.zeros(max(need, 1), dtype=torch.uint8, device=self.cache.device)
+        check(self.lib.pkv_global_attention(ctypes.byref(c), ctypes.byref(self.g), layer, q.data_ptr(), _np_ptr(seq),
+                                            out.data_ptr(), lse.data_ptr(), workspace.data_ptr(), workspace.numel(),
+                                            _stream_handle(torch, stream)), "pkv_global_attention")
+        return out, lse
+
+    def export(self, layer, b, h, n_rows, stream=None):
+        """(B_K, B_V, A_K, A_V) of one head as device fp32: (r, d), (r, d), (n_rows, r), (n_rows, r)."""
+        torch, c, r = self.torch, self.cache.c, self.g.rank
+        bk = torch.empty((r, c.head_dim), dtype=torch.float32, device=self.cache.device)
+        bv = torch.empty_like(bk)
+        ak = torch.empty((max(n_rows, 1), r), dtype=torch.float32, device=self.cache.device)
+        av = torch.empty_like(ak)
+        check(self.lib.pkv_global_export(ctypes.byref(c), ctypes.byref(self.g), layer, b, h, n_rows, bk.data_ptr(),
+                                         bv.data_ptr(), ak.data_ptr(), av.data_ptr(), _stream_handle(torch, stream)),
+              "pkv_global_export")
+        return bk, bv, ak[:n_rows], av[:n_rows]

@@ -11,8 +11,9 @@ PKV_OK, PKV_E_ARG, PKV_E_SHAPE, PKV_E_RANK, PKV_E_STATE, PKV_E_WORKSPACE, PKV_E_
 STATUS_NAMES = ["PKV_OK", "PKV_E_ARG", "PKV_E_SHAPE", "PKV_E_RANK", "PKV_E_STATE", "PKV_E_WORKSPACE",
                 "PKV_E_UNSUPPORTED", "PKV_E_HIP"]
 PKV_F32, PKV_BF16, PKV_INT4 = 0, 1, 2
-PKV_EMPTY, PKV_DENSE, PKV_FACTOR = 0, 1, 2
+PKV_EMPTY, PKV_DENSE, PKV_FACTOR, PKV_GLOBAL = 0, 1, 2, 3
 PKV_OP_ATTENTION, PKV_OP_COMPRESS, PKV_OP_PREFILL, PKV_OP_IMPORT = 0, 1, 2, 3
+PKV_OP_GLOBAL_PREFILL, PKV_OP_GLOBAL_ATTENTION = 4, 5
 PKV_DEV_NOT_DENSE, PKV_DEV_BAD_PAGE, PKV_DEV_RING_OVERRUN, PKV_DEV_NO_CONVERGE, PKV_DEV_BAD_RANK = (
     0x1, 0x2, 0x4, 0x8, 0x10)
 PKV_DEV_NOT_ELIGIBLE = 0x20
@@ -26,6 +27,8 @@ EXPORTS = [
     "pkv_import_pages",
     "pkv_export_block_elems", "pkv_export_pages", "pkv_int4_blob_bytes", "pkv_export_int4_pages",
     "pkv_device_status", "pkv_compress_sweeps", "pkv_cache_bytes", "pkv_last_error", "pkv_version",
+    "pkv_global_basis_bytes", "pkv_global_coef_bytes", "pkv_global_rank", "pkv_global_prefill",
+    "pkv_global_attention", "pkv_global_export",
 ]
 
 
@@ -51,6 +54,11 @@ class PkvCache(ctypes.Structure):
     ]
 
 
+class PkvGlobal(ctypes.Structure):
+    _fields_ = [("rank", ctypes.c_int32), ("max_tokens", ctypes.c_int32), ("basis", ctypes.c_void_p),
+                ("coef", ctypes.c_void_p)]
+
+
 _lib = None
 
 
@@ -65,6 +73,7 @@ def load():
     lib = ctypes.CDLL(LIB_PATH)
     i32, i64, u32, sz, vp = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint32, ctypes.c_size_t, ctypes.c_void_p
     cp = ctypes.POINTER(PkvCache)
+    gp = ctypes.POINTER(PkvGlobal)
     sig = {
         "pkv_cache_check": ([cp], i32),
         "pkv_dense_slots_per_head": ([cp], i64),
@@ -91,6 +100,12 @@ def load():
         "pkv_device_status": ([vp, ctypes.POINTER(u32)], i32),
         "pkv_compress_sweeps": ([vp, ctypes.POINTER(ctypes.c_uint64)], i32),
         "pkv_cache_bytes": ([cp, i32, vp, ctypes.POINTER(PkvFootprint), vp], i32),
+        "pkv_global_basis_bytes": ([cp, gp], sz),
+        "pkv_global_coef_bytes": ([cp, gp], sz),
+        "pkv_global_rank": ([i64, i32, i32, i32, i32, ctypes.c_double], i32),
+        "pkv_global_prefill": ([cp, gp, i32, vp, vp, i64, vp, vp, sz, vp], i32),
+        "pkv_global_attention": ([cp, gp, i32, vp, vp, vp, vp, vp, sz, vp], i32),
+        "pkv_global_export": ([cp, gp, i32, i32, i32, i64, vp, vp, vp, vp, vp], i32),
         "pkv_last_error": ([], ctypes.c_char_p),
         "pkv_version": ([], ctypes.c_char_p),
     }

@@ -126,7 +126,8 @@ template <typename TE>
 __global__ __launch_bounds__(256) void k_prefill_pages(Geo g, pkv_page *table, char *dense,
                                                        const TE *k, const TE *v, int64_t src_tokens,
                                                        SeqArgs seq, const uint8_t *rank_k,
-                                                       const uint8_t *rank_v, int def_rk, int def_rv) {
+                                                       const uint8_t *rank_v, int def_rk, int def_rv,
+                                                       int glob_r) {
     const int j = blockIdx.x, h = blockIdx.y, b = blockIdx.z;
     const int64_t T = seq.len[b];
     const int64_t head = g.head_index(b, h);
@@ -134,6 +135,12 @@ __global__ __launch_bounds__(256) void k_prefill_pages(Geo g, pkv_page *table, c
     const int kind = plan_kind(T, g.P, g.S, g.W, j);
     if (kind == PKV_EMPTY) {
         if (threadIdx.x == 0) write_entry(e, 0, PKV_EMPTY, 0, 0);
+        return;
+    }
+    if (kind == PKV_FACTOR && glob_r > 0) {
+        // Global SVD cache: the page's tokens are rows of the head's
+        // coefficients; slot = the row of its first token
+        if (threadIdx.x == 0) write_entry(e, (j - g.sink_pages) * g.P, PKV_GLOBAL, glob_r, glob_r);
         return;
     }
     if (kind == PKV_FACTOR) {
@@ -165,17 +172,17 @@ __global__ __launch_bounds__(256) void k_prefill_pages(Geo g, pkv_page *table, c
 
 hipError_t launch_prefill_pages(const LaunchCtx &L, const void *k, const void *v, int64_t src_tokens,
                                 const SeqArgs &seq, const uint8_t *rank_k, const uint8_t *rank_v,
-                                int def_rk, int def_rv, int max_pages_in_batch) {
+                                int def_rk, int def_rv, int max_pages_in_batch, int glob_r) {
     LayerPtrs p = layer_ptrs(L);
     dim3 grid(max_pages_in_batch, L.geo.Hkv, L.geo.B);
     if (L.geo.dense_dtype == PKV_BF16)
         hipLaunchKernelGGL(k_prefill_pages<uint16_t>, grid, dim3(256), 0, L.stream, L.geo, p.table,
                            p.dense, (const uint16_t *)k, (const uint16_t *)v, src_tokens, seq, rank_k,
-                           rank_v, def_rk, def_rv);
+                           rank_v, def_rk, def_rv, glob_r);
     else
         hipLaunchKernelGGL(k_prefill_pages<float>, grid, dim3(256), 0, L.stream, L.geo, p.table, p.dense,
                            (const float *)k, (const float *)v, src_tokens, seq, rank_k, rank_v, def_rk,
-                           def_rv);
+                           def_rv, glob_r);
     return hipGetLastError();
 }
 

@@ -220,6 +220,8 @@ size_t pkv_workspace_bytes(const pkv_cache *c, int32_t op, int64_t n) {
     case PKV_OP_COMPRESS: return 0;
     case PKV_OP_PREFILL: return 0;
     case PKV_OP_IMPORT: return 0;
+    case PKV_OP_GLOBAL_PREFILL: return (size_t)global_prefill_workspace_bytes(g, n);
+    case PKV_OP_GLOBAL_ATTENTION: return (size_t)global_attention_workspace_bytes(g, n);
     default: return 0;
     }
 }
@@ -555,6 +557,134 @@ pkv_status pkv_export_int4_pages(const pkv_cache *c, int32_t layer, int32_t n, c
             return st;
     }
     return PKV_OK;
+}
+
+// ---- Global SVD baseline ------------------------------------------------------
+
+namespace {
+
+pkv_status check_global(const pkv_cache *c, const pkv_global *gl, bool need_buffers) {
+    pkv_status st = check_cache(c, true);
+    if (st != PKV_OK) return st;
+    if (!gl) return fail(PKV_E_ARG, "global descriptor is NULL");
+    if (c->dense_dtype != PKV_BF16 || c->head_dim != 128 || (c->page_size != 32 && c->page_size != 64))
+        return fail(PKV_E_UNSUPPORTED, "Global SVD needs bf16 dense pages, head_dim 128 and P = 32 or 64");
+    if (gl->rank < 1 || gl->rank > 128) return fail(PKV_E_RANK, "global rank %d outside 1..128", gl->rank);
+    if (gl->max_tokens <= 0 || gl->max_tokens % 32)
+        return fail(PKV_E_SHAPE, "max_tokens %d: must be a positive multiple of 32", gl->max_tokens);
+    if (need_buffers && (!gl->basis || !gl->coef)) return fail(PKV_E_ARG, "basis or coef is NULL");
+    return PKV_OK;
+}
+
+GlobalGeo global_geo(const pkv_global *gl) {
+    GlobalGeo gg;
+    gg.r = gl->rank;
+    gg.r8 = (gl->rank + 7) & ~7;
+    gg.max_tokens = gl->max_tokens;
+    return gg;
+}
+
+int64_t region_rows(const Geo &g, int64_t T) {
+    const int64_t t0 = (int64_t)g.sink_pages * g.P;
+    const int64_t t1 = T - g.W >= 0 ? (T - g.W) / g.P * g.P : 0;
+    return std::max<int64_t>(0, t1 - t0);
+}
+
+pkv_status global_seq(const pkv_cache *c, const pkv_global *gl, const int32_t *seq_len, int64_t src_cap, SeqArgs &seq,
+                      int64_t &max_T) {
+    if (!seq_len) return fail(PKV_E_ARG, "seq_len is NULL");
+    const Geo g = make_geo(c);
+    seq = SeqArgs{};
+    seq.n = c->batch;
+    max_T = 0;
+    for (int b = 0; b < c->batch; ++b) {
+        if (seq_len[b] < 0 || seq_len[b] > src_cap || (int64_t)seq_len[b] > (int64_t)c->max_pages * c->page_size)
+            return fail(PKV_E_SHAPE, "seq_len[%d] = %d outside 0..max_pages * P (and the source)", b, seq_len[b]);
+        if (region_rows(g, seq_len[b]) > gl->max_tokens)
+            return fail(PKV_E_SHAPE, "sequence %d: %lld region rows above max_tokens %d", b,
+                        (long long)region_rows(g, seq_len[b]), gl->max_tokens);
+        seq.len[b] = seq_len[b];
+        max_T = std::max<int64_t>(max_T, seq_len[b]);
+    }
+    return PKV_OK;
+}
+
+}  // namespace
+
+size_t pkv_global_basis_bytes(const pkv_cache *c, const pkv_global *gl) {
+    if (check_global(c, gl, false) != PKV_OK) return 0;
+    const GlobalGeo gg = global_geo(gl);
+    return (size_t)c->n_layers * c->batch * c->n_kv_heads * 3 * gg.r8 * c->head_dim * 2;
+}
+
+size_t pkv_global_coef_bytes(const pkv_cache *c, const pkv_global *gl) {
+    if (check_global(c, gl, false) != PKV_OK) return 0;
+    const GlobalGeo gg = global_geo(gl);
+    return (size_t)c->n_layers * c->batch * c->n_kv_heads * 2 * gg.r8 * (int64_t)gg.max_tokens * 2;
+}
+
+int32_t pkv_global_rank(int64_t T, int32_t P, int32_t S, int32_t W, int32_t d, double rho) {
+    if (T < 0 || P <= 0 || S < 0 || W < 0 || d <= 0 || !(rho > 0.0)) return -1;
+    int64_t n_dense = 0, n_fact = 0;
+    for (int64_t j = 0; j * P < T; ++j) {
+        const int64_t rows = std::min<int64_t>(P, T - j * P);
+        if (plan_kind(T, P, S, W, j) == PKV_FACTOR) n_fact += rows;
+        else n_dense += rows;
+    }
+    const double budget = rho * 2.0 * (double)T * d;
+    int32_t best = 0;
+    for (int64_t r = 1; r <= std::min<int64_t>(n_fact, d); ++r)
+        if (2.0 * n_dense * d + 2.0 * r * (n_fact + d) <= budget) best = (int32_t)r;
+    return best;
+}
+
+pkv_status pkv_global_prefill(const pkv_cache *c, const pkv_global *gl, int32_t layer, const void *k, const void *v,
+                              int64_t src_tokens, const int32_t *seq_len, void *ws, size_t ws_bytes, pkv_stream s) {
+    pkv_status st = check_global(c, gl, true);
+    if (st != PKV_OK) return st;
+    if ((st = check_layer(c, layer)) != PKV_OK) return st;
+    if (!k || !v) return fail(PKV_E_ARG, "k or v is NULL");
+    SeqArgs seq;
+    int64_t max_T = 0;
+    if ((st = global_seq(c, gl, seq_len, src_tokens, seq, max_T)) != PKV_OK) return st;
+    LaunchCtx L = ctx(c, layer, s);
+    const size_t need = (size_t)global_prefill_workspace_bytes(L.geo, max_T);
+    if ((st = check_ws(ws, ws_bytes, need)) != PKV_OK) return st;
+    hipError_t e = launch_prefill_pages(L, k, v, src_tokens, seq, nullptr, nullptr, 1, 1, c->max_pages, gl->rank);
+    if ((st = check_launch(e, "pkv_global_prefill (pages)")) != PKV_OK) return st;
+    return check_launch(launch_global_prefill(L, global_geo(gl), gl, k, v, src_tokens, seq, max_T, ws),
+                        "pkv_global_prefill");
+}
+
+pkv_status pkv_global_attention(const pkv_cache *c, const pkv_global *gl, int32_t layer, const void *q,
+                                const int32_t *seq_len, float *out, float *lse, void *ws, size_t ws_bytes,
+                                pkv_stream s) {
+    pkv_status st = check_global(c, gl, true);
+    if (st != PKV_OK) return st;
+    if ((st = check_layer(c, layer)) != PKV_OK) return st;
+    if (!q || !out) return fail(PKV_E_ARG, "q or out is NULL");
+    SeqArgs seq;
+    int64_t max_T = 0;
+    if ((st = global_seq(c, gl, seq_len, INT64_MAX, seq, max_T)) != PKV_OK) return st;
+    LaunchCtx L = ctx(c, layer, s);
+    const size_t need = (size_t)global_attention_workspace_bytes(L.geo, max_T);
+    if ((st = check_ws(ws, ws_bytes, need)) != PKV_OK) return st;
+    return check_launch(launch_global_attention(L, global_geo(gl), gl, q, seq, max_T, out, lse, ws),
+                        "pkv_global_attention");
+}
+
+pkv_status pkv_global_export(const pkv_cache *c, const pkv_global *gl, int32_t layer, int32_t b, int32_t h,
+                             int64_t n_rows, float *basis_k, float *basis_v, float *coef_k, float *coef_v,
+                             pkv_stream s) {
+    pkv_status st = check_global(c, gl, true);
+    if (st != PKV_OK) return st;
+    if ((st = check_layer(c, layer)) != PKV_OK) return st;
+    if (b < 0 || b >= c->batch || h < 0 || h >= c->n_kv_heads) return fail(PKV_E_ARG, "head (%d, %d) out of range", b, h);
+    if (n_rows < 0 || n_rows > gl->max_tokens) return fail(PKV_E_ARG, "n_rows %lld outside 0..max_tokens", (long long)n_rows);
+    if (!basis_k || !basis_v || (n_rows > 0 && (!coef_k || !coef_v))) return fail(PKV_E_ARG, "NULL output");
+    LaunchCtx L = ctx(c, layer, s);
+    return check_launch(launch_global_export(L, global_geo(gl), gl, b, h, n_rows, basis_k, basis_v, coef_k, coef_v),
+                        "pkv_global_export");
 }
 
 pkv_status pkv_compress_sweeps(pkv_stream s, uint64_t *sweeps) {

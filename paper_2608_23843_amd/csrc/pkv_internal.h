@@ -183,7 +183,7 @@ struct SeqArgs {
 hipError_t launch_reset(const LaunchCtx &L, int64_t first_entry, int64_t n_entries);
 hipError_t launch_prefill_pages(const LaunchCtx &L, const void *k, const void *v, int64_t src_tokens,
                                 const SeqArgs &seq, const uint8_t *rank_k, const uint8_t *rank_v,
-                                int def_rk, int def_rv, int max_pages_in_batch);
+                                int def_rk, int def_rv, int max_pages_in_batch, int glob_r = 0);
 hipError_t launch_prefill_compress(const LaunchCtx &L, const void *k, const void *v,
                                    int64_t src_tokens, const int32_t *item_offsets, int64_t n_items,
                                    const uint8_t *rank_k, const uint8_t *rank_v, int def_rk, int def_rv);
@@ -202,6 +202,24 @@ __host__ __device__ inline int64_t int4_blob_bytes(int P, int d, int rk, int rv)
     return (int64_t)P * rk + (int64_t)rk * d + (int64_t)P * rv + (int64_t)rv * d +
            2LL * ((P / 32) * rk + d + P + d);
 }
+
+// Global SVD factors beside a cache: rank, padded rank, coefficient rows per head.
+struct GlobalGeo {
+    int r, r8, max_tokens;
+};
+struct GlobalLayer {
+    char *basis, *coef;   // this layer's factors
+};
+int global_gram_chunks(const Geo &g, int64_t max_T);
+int64_t global_prefill_workspace_bytes(const Geo &g, int64_t max_T);
+int global_attention_chunks(const Geo &g, int64_t max_T);
+int64_t global_attention_workspace_bytes(const Geo &g, int64_t max_T);
+hipError_t launch_global_prefill(const LaunchCtx &L, const GlobalGeo &gg, const pkv_global *gl, const void *k,
+                                 const void *v, int64_t src_tokens, const SeqArgs &seq, int64_t max_T, void *ws);
+hipError_t launch_global_attention(const LaunchCtx &L, const GlobalGeo &gg, const pkv_global *gl, const void *q,
+                                   const SeqArgs &seq, int64_t max_T, float *out, float *lse, void *ws);
+hipError_t launch_global_export(const LaunchCtx &L, const GlobalGeo &gg, const pkv_global *gl, int b, int h,
+                                int64_t n_rows, float *bk, float *bv, float *ak, float *av);
 
 struct AttnPlan {
     int pages_per_chunk;

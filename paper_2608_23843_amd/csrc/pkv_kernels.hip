@@ -18,3 +18,4 @@
 #include "attention.inl"
 #include "attention_mfma.inl"
 #include "attention_launch.inl"
+#include "global_svd.inl"

@@ -228,3 +228,14 @@ def test_cache_bytes_argument_errors(pk):
     big = np.array([64, 8 * 64 + 1], dtype=np.int32)
     assert lib.pkv_cache_bytes(c, 0, big.ctypes.data, ctypes.byref(f), None) == 2
     assert lib.pkv_last_error()
+
+
+@pytest.mark.parametrize("T,P,S,W,rho", [(16384, 32, 32, 32, 0.6), (16384, 32, 32, 32, 0.58755), (131072, 64, 64, 512, 0.5643),
+                                         (32768, 64, 64, 256, 0.6), (1000, 32, 32, 32, 0.6), (100, 64, 64, 512, 0.6),
+                                         (5000, 16, 40, 20, 0.3), (4096, 64, 0, 0, 0.05)])
+def test_global_rank_matches_oracle_accounting(pk, T, P, S, W, rho):
+    """pkv_global_rank (integer, host) against the oracle's accounting over the
+    oracle's page plan, bit for bit."""
+    kinds = oracle.plan_pages(T, P, S, W)
+    n_fact = int(sum(min(P, T - j * P) for j, k in enumerate(kinds) if k == oracle.FACTOR))
+    assert pk.global_rank(T, P, S, W, 128, rho) == accounting.global_rank(T - n_fact, n_fact, 128, rho)

@@ -671,10 +671,15 @@ def test_global_rank_budget():
             stored = 2 * n_dense * d + 2 * (A.size + B.size)
             assert (stored <= rho * raw) == fits, (rho, rr)
     # matched to PuzzleKV's own whole-cache ratio at the paper's default
-    # geometry (P = 32, (16, 14), d = 128, 16K tokens, 96 dense tokens: sink
-    # page and the last two pages), Global SVD gets rank 74
-    rho_pkv = accounting.cache_ratio(512, 3, 32, 16, 14, 128)
-    assert accounting.global_rank(96, 16384 - 96, 128, rho_pkv) == 74
+    # geometry (P = 32, (16, 14), d = 128, 16K tokens; the plan keeps the sink
+    # page and the last completed page dense, the 58.76% of Section 4.5),
+    # Global SVD gets rank 74
+    kinds = oracle.plan_pages(16384, 32, 32, 32)
+    n_dense_pages = int((kinds == oracle.DENSE).sum())
+    assert n_dense_pages == 2
+    rho_pkv = accounting.cache_ratio(512, n_dense_pages, 32, 16, 14, 128)
+    assert abs(rho_pkv - 0.5876) < 5e-5
+    assert accounting.global_rank(32 * n_dense_pages, 16384 - 32 * n_dense_pages, 128, rho_pkv) == 74
 
 
 def test_global_head_attention_full_rank_equals_dense():
