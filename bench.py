@@ -88,6 +88,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="CPU-baseline budget for the oracle (0 disables)")
     ap.add_argument("--workers", type=int, default=16, help="host threads for input generation")
+    ap.add_argument("--compare", action="store_true",
+                    help="Global SVD workloads: also compare its accuracy with PuzzleKV's at the same budget")
     return ap.parse_args()
 
 
@@ -202,6 +204,275 @@ def cpu_baseline(wl, seed, seq_T, K_dense, V_dense, q, budget_s, layers, ranks, 
     }
 
 
+def global_attention_bytes(P, d, g, r, seq_len, S, W):
+    """Algorithmic bytes of one Global SVD attention launch, per (sequence, KV
+    head): the coefficient rows of the region (r bf16 values for K and for V
+    per token), the two bases (r x d each), the dense pages up to the length
+    and their page-table entries. The caller adds the queries, out and lse."""
+    total = 0
+    for T in seq_len:
+        n_pages = -(-T // P)
+        sink_pages = -(-S // P)
+        t1 = (T - W) // P * P if T >= W else 0
+        n_reg = max(0, t1 - sink_pages * P)
+        total += 2 * n_reg * r * 2 + 2 * r * d * 2 + 2 * (T - n_reg) * d * 2 + (n_pages - n_reg // P) * 8
+    return total
+
+
+def _rel(a, b):
+    import numpy as np
+    return float(np.abs(a - b).sum() / max(np.abs(b).sum(), 1e-300))
+
+
+def global_comparison(wl, seed, settings, log_fn):
+    """Global SVD against PuzzleKV at one budget (Section 4.2 "Main Results",
+    a matched rho), on sequences whose planted subspace changes every
+    `segment_pages` pages: reconstruction error of the compressible region
+    and attention error against exact dense attention (the oracle, fp64) for
+    random queries and for retrieval queries (each query head points at one
+    random key of the region, so its softmax is peaked), both methods' factors
+    computed on the GPU."""
+    import dataclasses
+    import numpy as np
+    import torch
+    import oracle
+    import paper_2608_23843_amd as pk
+    import synth
+    P, d, S, W, T, B, Hkv, g = wl.page, wl.head_dim, wl.sink, wl.window, wl.tokens, wl.batch, wl.kv_heads, wl.group
+    rk, rv = wl.ranks[0], (wl.ranks_v or wl.ranks)[0]
+    kinds = oracle.plan_pages(T, P, S, W)
+    fac = [j for j, k in enumerate(kinds) if k == oracle.FACTOR]
+    rows = np.concatenate([np.arange(j * P, (j + 1) * P) for j in fac])
+    out = []
+    for seg in settings:
+        w = dataclasses.replace(wl, segment_pages=seg)
+        K, V = synth.kv_layer(w, seed, 0, T)
+        kt = torch.from_numpy(K).to("cuda", torch.bfloat16).contiguous()
+        vt = torch.from_numpy(V).to("cuda", torch.bfloat16).contiguous()
+        cache = pk.PuzzleKVCache(1, B, Hkv, w.q_heads, d, P, len(kinds), max(rk, rv), S, W, "bf16", "bf16")
+        cache.prefill(0, kt, vt, [T] * B, default_rank=(rk, rv))
+        fp = cache.footprint([T] * B, layer=0)
+        rho = (fp["dense_bytes"] + fp["factor_bytes"]) / fp["raw_bytes"]
+        r = pk.global_rank(T, P, S, W, d, rho)
+        gc = pk.PuzzleKVCache(1, B, Hkv, w.q_heads, d, P, len(kinds), 1, S, W, "bf16", "bf16")
+        gs = pk.GlobalSVD(gc, r, -(-len(rows) // 32) * 32)
+        gs.prefill(0, kt, vt, [T] * B)
+        torch.cuda.synchronize()
+        status = cache.device_status()
+        # reconstruction of the region
+        num = {"pkv": [0.0, 0.0], "global": [0.0, 0.0]}
+        den = [0.0, 0.0]
+        R = cache.c.max_rank
+        for b in range(B):
+            for h in range(Hkv):
+                blk = cache.export_pages(0, [b] * len(fac), [h] * len(fac), fac).cpu().numpy().astype(np.float64)
+                bk, bv, ak, av = (x.cpu().numpy().astype(np.float64) for x in gs.export(0, b, h, len(rows)))
+                for i, (X, Ag, Bg) in enumerate(((K[b, h][rows].astype(np.float64), ak, bk),
+                                                 (V[b, h][rows].astype(np.float64), av, bv))):
+                    den[i] += float(np.sum(X * X))
+                    Eg = X - Ag @ Bg
+                    num["global"][i] += float(np.sum(Eg * Eg))
+                    rr = rk if i == 0 else rv
+                    off = 0 if i == 0 else P * R + R * d
+                    Lp = blk[:, off:off + P * R].reshape(-1, P, R)[:, :, :rr]
+                    Rp = blk[:, off + P * R:off + P * R + R * d].reshape(-1, R, d)[:, :rr]
+                    Ep = X.reshape(-1, P, d) - np.matmul(Lp, Rp)
+                    num["pkv"][i] += float(np.sum(Ep * Ep))
+        rec = {m: [float(np.sqrt(num[m][i] / den[i])) for i in range(2)] for m in num}
+        # attention against dense attention
+        rng = np.random.default_rng(seed + 77)
+        q_rand = synth.queries(w, seed, 0)
+        q_ret = np.empty_like(q_rand)
+        for b in range(B):
+            for h in range(Hkv):
+                for i in range(g):
+                    kk = K[b, h][rows[rng.integers(len(rows))]].astype(np.float64)
+                    q_ret[b, h * g + i] = 12.0 * np.sqrt(d) * kk / np.sum(kk * kk)   # score of that key: 12
+        q_ret = synth.round_storage(q_ret, "bf16")
+        att = {}
+        for name, qv in (("random", q_rand), ("retrieval", q_ret)):
+            qt = torch.from_numpy(qv).to("cuda", torch.bfloat16).contiguous()
+            o_p, _ = cache.attention(0, qt, [T] * B)
+            o_g, _ = gs.attention(0, qt, [T] * B)
+            torch.cuda.synchronize()
+            o_p, o_g = o_p.cpu().numpy().astype(np.float64), o_g.cpu().numpy().astype(np.float64)
+            ref = np.zeros_like(o_p)
+            for b in range(B):
+                for h in range(Hkv):
+                    pages = []
+                    for j in range(len(kinds)):
+                        Kp = np.zeros((P, d)); Vp = np.zeros((P, d))
+                        n = min(P, T - j * P)
+                        Kp[:n] = K[b, h, j * P:j * P + n]; Vp[:n] = V[b, h, j * P:j * P + n]
+                        pages.append(("dense", Kp, Vp))
+                    ref[b, h * g:(h + 1) * g], _ = oracle.attention(oracle.HeadCache(T, P, d, pages),
+                                                                    qv[b, h * g:(h + 1) * g].astype(np.float64))
+            att[name] = {"pkv": _rel(o_p, ref), "global": _rel(o_g, ref)}
+        status |= cache.device_status() | gc.device_status()
+        rho_g = (2 * (T * B * Hkv - len(rows) * B * Hkv) * d + 2 * r * (len(rows) + d) * B * Hkv) / (2.0 * T * d * B * Hkv)
+        row = {"segment_pages": seg, "rho_pkv": round(rho, 5), "global_rank": r, "rho_global": round(rho_g, 5),
+               "recon_rel_err": {"pkv": [round(x, 5) for x in rec["pkv"]], "global": [round(x, 5) for x in rec["global"]]},
+               "attn_rel_err": {k: {m: round(v, 6) for m, v in d_.items()} for k, d_ in att.items()},
+               "device_status": status}
+        log_fn("comparison, segments of %s pages: %s" % (seg, json.dumps(row)))
+        out.append(row)
+        del cache, gc, gs, kt, vt
+        torch.cuda.empty_cache()
+    return out
+
+
+def global_cpu_baseline(wl, seed, T, r, budget_s, layers):
+    """The oracle's Global SVD attention (every factorized token rebuilt from
+    its coefficients and the basis, then textbook softmax) on whole heads of
+    one layer, coefficients and bases drawn by the generator, timed until the
+    budget is spent; extrapolated to the step."""
+    import numpy as np
+    import oracle
+    import synth
+    P, d, g = wl.page, wl.head_dim, wl.group
+    kinds = oracle.plan_pages(T, P, wl.sink, wl.window)
+    n_reg = int((kinds == oracle.FACTOR).sum()) * P
+    q = synth.queries(wl, seed, 0)
+    times = []
+    for b in range(wl.batch):
+        for h in range(wl.kv_heads):
+            K, V = synth.kv_head(wl, seed, 0, b, h, T)
+            A_K, B_K, A_V, B_V = synth.global_factors(wl, seed, 0, b, h, n_reg, r)
+            t = time.time()
+            head = oracle.global_head(T, P, d, kinds, K, V, A_K, B_K, A_V, B_V)
+            oracle.attention(head, q[b, h * g:(h + 1) * g].astype(np.float64))
+            times.append(time.time() - t)
+            if sum(times) >= budget_s:
+                break
+        if sum(times) >= budget_s:
+            break
+    per_head = sum(times) / len(times)
+    n_heads = wl.batch * wl.kv_heads
+    return {"value": per_head * n_heads * layers * 1e6, "unit": "us/step", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": "%d of %d (sequence, KV head) heads of one layer at T=%d (fp64 rebuild of %d factorized "
+                      "tokens at rank %d + softmax), %.2f s per head, extrapolated x%d heads x%d layers"
+                      % (len(times), n_heads, T, n_reg, r, per_head, n_heads, layers)}
+
+
+def run_global(args, wl):
+    """Global SVD baseline: prefill (Gram, eigenvectors, projection) timed on
+    layer 0, the layer copied into the others, then attention over every layer
+    per decode step. The baseline is built from the prompt and attended at
+    its length; decode steps re-attend the same cache with new queries."""
+    import numpy as np
+    import torch
+    import paper_2608_23843_amd as pk
+    import synth
+    layers = args.layers or wl.layers
+    B, Hkv, Hq, d, P, T = wl.batch, wl.kv_heads, wl.q_heads, wl.head_dim, wl.page, wl.tokens
+    S, W, g = wl.sink, wl.window, wl.group
+    n_steps = args.warmup + args.steps
+    kinds = pk.plan_pages(T, P, S, W)
+    n_reg = int((kinds == pk.PKV_FACTOR).sum()) * P
+    K, V = synth.kv_layer(wl, args.seed, 0, T, workers=args.workers)
+    kt = torch.from_numpy(K).to("cuda", torch.bfloat16)
+    vt = torch.from_numpy(V).to("cuda", torch.bfloat16)
+    del K, V
+    rho = wl.global_rho
+    if rho < 0:   # matched to PuzzleKV's realized ratio on the same inputs
+        pc = pk.PuzzleKVCache(1, B, Hkv, Hq, d, P, len(kinds), max(wl.ranks + wl.ranks_v), S, W, "bf16", "bf16")
+        pc.prefill(0, kt, vt, [T] * B, default_rank=(wl.ranks[0], (wl.ranks_v or wl.ranks)[0]))
+        fp = pc.footprint([T] * B, layer=0)
+        rho = (fp["dense_bytes"] + fp["factor_bytes"]) / fp["raw_bytes"]
+        del pc
+    r = pk.global_rank(T, P, S, W, d, rho)
+    log("workload %s: B=%d Hq=%d Hkv=%d d=%d P=%d T=%d layers=%d, Global SVD rank %d for ratio %.5f"
+        % (wl.name, B, Hq, Hkv, d, P, T, layers, r, rho))
+    cache = pk.PuzzleKVCache(layers, B, Hkv, Hq, d, P, len(kinds), 1, S, W, "bf16", "bf16")
+    gs = pk.GlobalSVD(cache, r, -(-n_reg // 32) * 32)
+    ws_p = gs.workspace(pk.PKV_OP_GLOBAL_PREFILL, T)
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    pre_ms = []
+    for rep in range(3):
+        torch.cuda.synchronize()
+        ev0.record()
+        gs.prefill(0, kt, vt, [T] * B, workspace=ws_p)
+        ev1.record()
+        torch.cuda.synchronize()
+        pre_ms.append(ev0.elapsed_time(ev1))
+    status = cache.device_status()
+    log("Global SVD prefill (Gram + eigenvectors + projection) of one layer: %.3f ms (best of 3), status %d"
+        % (min(pre_ms), status))
+    del kt, vt, ws_p
+    torch.cuda.empty_cache()
+    for buf in (cache.dense_pool, cache.table, gs.basis, gs.coef):
+        per = buf.numel() // layers
+        for layer in range(1, layers):
+            buf[layer * per:(layer + 1) * per].copy_(buf[:per])
+    torch.cuda.synchronize()
+    ws = gs.workspace(pk.PKV_OP_GLOBAL_ATTENTION, T)
+    out = torch.empty((B, Hq, d), dtype=torch.float32, device="cuda")
+    lse = torch.empty((B, Hq), dtype=torch.float32, device="cuda")
+    qs = [torch.from_numpy(synth.queries(wl, args.seed, s)).to("cuda", torch.bfloat16).contiguous()
+          for s in range(n_steps)]
+    stream = torch.cuda.current_stream()
+    pool = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+            for _ in range(args.steps * layers)]
+    marks = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    torch.cuda.synchronize()
+    import gc as _gc
+    _gc.collect()
+    _gc.disable()
+    calls = []
+    for s in range(n_steps):
+        timed = s >= args.warmup
+        if s == args.warmup:
+            torch.cuda.synchronize()
+            marks[0].record(stream)
+        for layer in range(layers):
+            if timed:
+                e0, e1 = pool[len(calls)]
+                e0.record(stream)
+            gs.attention(layer, qs[s], [T] * B, out=out, lse=lse, workspace=ws)
+            if timed:
+                e1.record(stream)
+                calls.append((e0, e1))
+    marks[1].record(stream)
+    torch.cuda.synchronize()
+    _gc.enable()
+    status |= cache.device_status()
+    ms_per_step = marks[0].elapsed_time(marks[1]) / args.steps
+    call_ms = np.array([a.elapsed_time(b) for a, b in calls])
+    attn_us = float(call_ms.mean() * 1e3)
+    if not np.isfinite(out.cpu().numpy()).all():
+        raise RuntimeError("non-finite attention output")
+    abytes = global_attention_bytes(P, d, g, r, [T] * B, S, W) * Hkv + B * Hq * (d * 2 + d * 4 + 4)
+    achieved = abytes / (attn_us * 1e-6) / 1e9
+    log("decode: %.3f ms/step, Global SVD attention %.1f us/layer (median %.1f), %.1f GB/s, status %d"
+        % (ms_per_step, attn_us, float(np.median(call_ms) * 1e3), achieved, status))
+    result = {
+        "metric": "Global SVD decode attention time per decode step (%d layers, %d/%d heads, %dK context, one "
+                  "rank-%d basis per KV head)" % (layers, Hq, Hkv, T // 1024, r),
+        "value": round(ms_per_step * 1e3, 2), "unit": "us/step", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4), "higher_is_better": False, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.name, "batch": B, "q_heads": Hq, "kv_heads": Hkv, "head_dim": d, "page": P,
+                   "tokens": T, "sink": S, "window": W, "global_rank": r, "storage_ratio": round(rho, 5),
+                   "segment_pages": wl.segment_pages, "layers": layers,
+                   "step": "Global SVD attention per layer (the baseline is not updated while decoding)"},
+        "attention_us_per_layer": round(attn_us, 2), "attention_algorithmic_bytes": int(abytes),
+        "attention_gbps": round(achieved, 1),
+        "global_prefill_ms_per_layer": round(min(pre_ms), 3),
+        "device_status": status,
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": measured_traffic(wl.name)},
+    }
+    del cache, gs, ws
+    torch.cuda.empty_cache()
+    if args.cpu_seconds > 0:
+        log("CPU baseline (oracle), budget %.0f s" % args.cpu_seconds)
+        result["cpu_baseline"] = global_cpu_baseline(wl, args.seed, T, r, args.cpu_seconds, layers)
+    if args.compare:
+        result["comparison"] = global_comparison(wl, args.seed, (1, 4, 16, 64, 0), log)
+    print(json.dumps(result), flush=True)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -225,6 +496,8 @@ def main():
     if args.tokens:
         import dataclasses
         wl = dataclasses.replace(wl, tokens=args.tokens, name=wl.name + "_T%d" % args.tokens)
+    if wl.global_rho != 0:
+        return run_global(args, wl)
     layers = args.layers or wl.layers
     B, Hkv, Hq, d, P, T = wl.batch, wl.kv_heads, wl.q_heads, wl.head_dim, wl.page, wl.tokens
     S, W = wl.sink, wl.window

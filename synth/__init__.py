@@ -31,7 +31,7 @@ import functools
 
 import numpy as np
 
-TAG_KEY, TAG_VALUE, TAG_OUTLIER, TAG_QUERY, TAG_RANK, TAG_FACTOR, TAG_TOKEN = range(7)
+TAG_KEY, TAG_VALUE, TAG_OUTLIER, TAG_QUERY, TAG_RANK, TAG_FACTOR, TAG_TOKEN, TAG_GLOBAL = range(8)
 
 
 @dataclasses.dataclass(frozen=True)
@@ -58,7 +58,8 @@ class Workload:
     rank_error: float = 0.0  # > 0: each page's rank chosen for this relative reconstruction error
     key_rope: bool = False   # keys handed over before RoPE (the cache rotates them at access)
     segment_pages: int = 1   # pages sharing one planted basis (0: the whole sequence)
-    global_rho: float = 0.0  # > 0: a Global SVD cache with its rank matched to this storage ratio
+    global_rho: float = 0.0  # != 0: a Global SVD cache, its rank matched to this storage ratio
+                             # (< 0: to the PuzzleKV ratio realized on the same inputs)
 
     @property
     def factors(self) -> str:
@@ -99,6 +100,20 @@ WORKLOADS = {
     # INT4 factors: Qwen3-32B heads, batch 8, T=128K.
     "qwen32b_int4": Workload("qwen32b_int4", 5, 8, 8, 64, 128, 64, 131072, 64, 512, 24,
                              (16, 24, 32), "bf16", 1.0e6, 4, factor_dtype="int4"),
+    # Global SVD baseline at the 128K Qwen3-32B-shaped layer: one basis per
+    # (sequence, KV head) over the compressible region, its rank matched to the
+    # whole-cache storage PuzzleKV reaches on the same layer (ranks U{16,24,32}
+    # pages, ratio 0.5643).
+    "qwen32b_128k_global": Workload("qwen32b_128k_global", 9, 4, 8, 64, 128, 64, 131072, 64, 512, 24,
+                                    (16, 24, 32), "bf16", 1.0e6, 4, layers=64, global_rho=0.5643),
+    # Global SVD against PuzzleKV at the paper's default configuration
+    # (Qwen3-8B heads, P = 32, (r_K, r_V) = (16, 14), S = W = 32, 16K,
+    # batch 1), the Global SVD rank matched to PuzzleKV's realized whole-cache
+    # ratio, on sequences whose planted subspace changes every
+    # segment_pages pages (the comparison sweeps several values).
+    "qwen8b_global": Workload("qwen8b_global", 10, 1, 8, 32, 128, 32, 16384, 32, 32, 24,
+                              (16,), "bf16", 1.0e6, 4, layers=36, ranks_v=(14,), segment_pages=16,
+                              global_rho=-1.0),
 }
 
 
@@ -285,3 +300,19 @@ def decode_kv(wl: Workload, seed: int, layer: int, pos: int):
         K[..., :half] = a * c - bb * s
         K[..., half:] = bb * c + a * s
     return round_storage(K, wl.dtype), round_storage(V, wl.dtype)
+
+
+def global_factors(wl: Workload, seed: int, layer: int, b: int, h: int, n_rows: int, r: int):
+    """Global SVD factors drawn directly (not from a decomposition),
+    storage-rounded: coefficients A (n_rows x r) ~ N(0, r0 / r * d) per entry
+    and a basis B (r x d) ~ N(0, 1/d), for K then V, so that A B has the
+    per-element scale of the planted pages. Used where a cache of the right
+    shape is needed without the GPU decomposition."""
+    g = rng(seed, wl.wid, TAG_GLOBAL, layer, b, h)
+    d = wl.head_dim
+    out = []
+    for _ in range(2):
+        A = g.standard_normal((n_rows, r)) * np.sqrt(wl.r0 * d / r)
+        B = g.standard_normal((r, d)) / np.sqrt(d)
+        out += [round_storage(A, wl.dtype), round_storage(B, wl.dtype)]
+    return tuple(out)
