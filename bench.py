@@ -93,10 +93,22 @@ def parse():
     return ap.parse_args()
 
 
-def attention_bytes(pk_cache, ranks_np, ranks_v_np, seq_len, P, d, B, Hkv, Hq, S, W):
-    """Algorithmic bytes one attention launch must move: every stored byte of
-    every page it reads (factor pairs at their ranks, dense pages up to the
-    sequence length), the page-table entries, the queries, out and lse."""
+def factor_logical_bytes(factors, P, d, rk, rv):
+    """Bytes of one factor page pair at its logical ranks (Eq. (3) storage):
+    (r_K + r_V)(P + d) elements; INT4 adds one fp16 scale per run of up to 32
+    elements along the paper's directions to its half-byte codes."""
+    if factors == "int4":
+        runs = lambda n: -(-n // 32)
+        scales = rk * runs(P) + d * runs(rk) + P * runs(rv) + d * runs(rv)
+        return (rk + rv) * (P + d) // 2 + 2 * scales
+    return (rk + rv) * (P + d) * (4 if factors == "f32" else 2)
+
+
+def attention_bytes(factors, ranks_np, ranks_v_np, seq_len, P, d, B, Hkv, Hq, S, W):
+    """Algorithmic bytes one attention launch must move: every factor page pair
+    at its logical ranks (padding the slot layout adds is not counted), the
+    dense pages up to the sequence length, the page-table entries, the
+    queries, out and lse."""
     total = 0
     fpb = {}
     for b in range(B):
@@ -109,7 +121,7 @@ def attention_bytes(pk_cache, ranks_np, ranks_v_np, seq_len, P, d, B, Hkv, Hq, S
                 if sink_pages <= j <= jmax:
                     r = (int(ranks_np[b, h, j]), int(ranks_v_np[b, h, j]))
                     if r not in fpb:
-                        fpb[r] = pk_cache.factor_page_bytes(*r)
+                        fpb[r] = factor_logical_bytes(factors, P, d, *r)
                     total += fpb[r]
                 else:
                     rows = min(P, T - j * P)
@@ -202,6 +214,87 @@ def cpu_baseline(wl, seed, seq_T, K_dense, V_dense, q, budget_s, layers, ranks, 
                   % (len(times), n_heads, seq_T, "INT4 dequantization + " if int4 else "",
                      "key RoPE + " if wl.key_rope else "", per_head, n_heads, layers),
     }
+
+
+def hbm_calibration(achieved_gbps):
+    """Streaming read and copy rates of this chip (pkv_bandwidth_probe over
+    2 GiB, beyond the 256 MB last-level cache; the best of a sweep of access
+    patterns and launch shapes), and the attention's rate against them."""
+    import torch
+    import paper_2608_23843_amd as pk
+    n = 2 << 30
+    src = torch.ones(n, dtype=torch.uint8, device="cuda")
+    dst = torch.empty(n, dtype=torch.uint8, device="cuda")
+    best = {"read": (0.0, ""), "copy": (0.0, "")}
+    for mode in (0, 2, 1, 3):
+        name = "copy" if mode & 1 else "read"
+        for threads in (256, 512):
+            for blocks in (256, 512, 1024, 2048, 4096):
+                gbps = pk.bandwidth_probe(src, dst, mode, reps=5, blocks=blocks, threads=threads)
+                if gbps > best[name][0]:
+                    best[name] = (gbps, "%s, %d x %d threads" % ("64 KB chunks per workgroup" if mode & 2 else
+                                                                 "grid-stride", blocks, threads))
+    del src, dst
+    torch.cuda.empty_cache()
+    out = {"read_gbps": round(best["read"][0], 1), "read_shape": best["read"][1],
+           "copy_gbps": round(best["copy"][0], 1), "copy_shape": best["copy"][1],
+           "attention_frac_of_read": round(achieved_gbps / best["read"][0], 4),
+           "attention_frac_of_copy": round(achieved_gbps / best["copy"][0], 4),
+           "probe": "pkv_bandwidth_probe over 2 GiB, 16-byte loads, best of 5 launches per shape"}
+    log("HBM calibration: read %.0f GB/s (%s), copy %.0f GB/s (%s); attention at %.3f of read"
+        % (best["read"][0], best["read"][1], best["copy"][0], best["copy"][1], achieved_gbps / best["read"][0]))
+    return out
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_extras(wl, seed, T, K_dense, V_dense, q, comp_X, ranks_np, ranks_v_np, comp_refs):
+    """The rest of the oracle baseline: one head's attention on a single
+    thread, and the oracle's decomposition (fp64 one-sided Jacobi) on a sample
+    of up to 4,096 of the prompt's factorizable page pairs on all threads and
+    on a single thread (a 64-pair slice)."""
+    import numpy as np
+    import oracle
+    threads = oracle.num_threads()
+    extras = {"cpu_model": cpu_model()}
+    oracle.set_num_threads(1)
+    try:
+        one = cpu_baseline(wl, seed, T, K_dense, V_dense, q, 0.0, 1, ranks_np, ranks_v_np)
+        n_heads = wl.batch * wl.kv_heads
+        extras["value_1thread"] = one["value"] * n_heads   # one layer, all heads, 1 thread
+        extras["unit_1thread"] = "us per layer (all heads), 1 thread, extrapolated from one head"
+        if comp_X is not None and wl.rank_error == 0:
+            n1 = min(64, len(comp_refs))
+            X1 = np.concatenate([comp_X[:n1], comp_X[len(comp_refs):len(comp_refs) + n1]])
+            r1 = np.array([ranks_np[b, h, j] for b, h, j in comp_refs[:n1]] +
+                          [ranks_v_np[b, h, j] for b, h, j in comp_refs[:n1]], dtype=np.int32)
+            t = time.time()
+            oracle.truncated_factors_batch(X1, r1)
+            extras["compress_page_pairs_per_s_1thread"] = round(n1 / (time.time() - t), 2)
+    finally:
+        oracle.set_num_threads(threads)
+    if comp_X is not None and wl.rank_error == 0:
+        n = len(comp_refs)
+        rk = np.array([ranks_np[b, h, j] for b, h, j in comp_refs] + [ranks_v_np[b, h, j] for b, h, j in comp_refs],
+                      dtype=np.int32)
+        t = time.time()
+        oracle.truncated_factors_batch(comp_X, rk)
+        dt = time.time() - t
+        extras["compress_page_pairs_per_s"] = round(n / dt, 2)
+        extras["compress_sample"] = ("%d page pairs (K and V, P=%d, d=%d) of the prompt's factorizable pages, "
+                                     "fp64 one-sided Jacobi, %d threads, %.1f s" % (n, wl.page, wl.head_dim,
+                                                                                     threads, dt))
+    log("CPU extras: %s" % json.dumps(extras))
+    return extras
 
 
 def global_attention_bytes(P, d, g, r, seq_len, S, W):
@@ -465,9 +558,11 @@ def run_global(args, wl):
     }
     del cache, gs, ws
     torch.cuda.empty_cache()
+    result["hbm_calibration"] = hbm_calibration(achieved)
     if args.cpu_seconds > 0:
         log("CPU baseline (oracle), budget %.0f s" % args.cpu_seconds)
         result["cpu_baseline"] = global_cpu_baseline(wl, args.seed, T, r, args.cpu_seconds, layers)
+        result["cpu_baseline"]["cpu_model"] = cpu_model()
     if args.compare:
         result["comparison"] = global_comparison(wl, args.seed, (1, 4, 16, 64, 0), log)
     print(json.dumps(result), flush=True)
@@ -515,6 +610,12 @@ def main():
                for b in range(B) for h in range(Hkv) for j in dense_idx}
     V_dense = {(b, h, j): V[b, h, j * P:(j + 1) * P].astype(np.float64)
                for b in range(B) for h in range(Hkv) for j in dense_idx}
+    # a sample of the prompt's factorizable pages for the oracle's decomposition
+    # baseline (up to 4,096 page pairs, taken in order over heads and pages)
+    fac_idx = [j for j, kd in enumerate(kinds) if kd == pk.PKV_FACTOR]
+    comp_refs = [(b, h, j) for b in range(B) for h in range(Hkv) for j in fac_idx][:4096]
+    comp_X = np.stack([K[b, h, j * P:(j + 1) * P] for b, h, j in comp_refs] +
+                      [V[b, h, j * P:(j + 1) * P] for b, h, j in comp_refs]).astype(np.float64) if comp_refs else None
     bf = torch.bfloat16
     kt = torch.from_numpy(K).to("cuda", bf)
     del K
@@ -592,6 +693,7 @@ def main():
     step_marks = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
     torch.cuda.synchronize()
     call_events = []
+    comp_events = []   # (start, end, page pairs) of the compress calls in the timed steps
     step_start = step_end = None
     compress_calls = 0
     # the host only enqueues in the timed loop; a garbage-collector pass there
@@ -613,7 +715,13 @@ def main():
                 bb, hh, jj = zip(*[(b, h, int(j)) for b in range(B) for h in range(Hkv) for j in new_pages])
                 rr = [int(req_np[b, h, j]) for b, h, j in zip(bb, hh, jj)]
                 rv = [int(req_v_np[b, h, j]) for b, h, j in zip(bb, hh, jj)]
+                if timed:
+                    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    c0.record(stream)
                 cache.compress_pages(layer, bb, hh, jj, rr, rv)
+                if timed:
+                    c1.record(stream)
+                    comp_events.append((c0, c1, len(bb)))
                 compress_calls += 1
             if timed:
                 e0, e1 = pool[len(call_events)]
@@ -642,10 +750,19 @@ def main():
     if not np.isfinite(out.float().cpu().numpy()).all():
         raise RuntimeError("non-finite attention output")
 
+    comp_decode = None
+    if comp_events:
+        cms = sum(a.elapsed_time(b) for a, b, _ in comp_events)
+        npairs = sum(n for _, _, n in comp_events)
+        comp_decode = {"calls": len(comp_events), "page_pairs": npairs, "ms_total": round(cms, 3),
+                       "page_pairs_per_s": round(npairs / (cms * 1e-3), 1)}
+        log("compress during the timed steps: %d calls, %d page pairs, %.3f ms, %.3g page pairs/s"
+            % (len(comp_events), npairs, cms, npairs / (cms * 1e-3)))
+
     if wl.rank_error > 0:   # ranks of the pages compressed during the decode steps too
         ranks_np, ranks_v_np = chosen_ranks(cache, pk.plan_pages(T + n_steps, P, S, W), max_pages, wl.rank_error)
     mid_T = T + args.warmup + args.steps // 2 + 1
-    abytes = attention_bytes(cache, ranks_np, ranks_v_np, [mid_T] * B, P, d, B, Hkv, Hq, S, W)
+    abytes = attention_bytes(wl.factors, ranks_np, ranks_v_np, [mid_T] * B, P, d, B, Hkv, Hq, S, W)
     achieved = abytes / (attn_us * 1e-6) / 1e9
     traffic = measured_traffic(wl.name)
     roofline = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
@@ -696,11 +813,16 @@ def main():
         "device_status": status,
         "roofline": roofline,
     }
+    if comp_decode:
+        result["compress_during_decode"] = comp_decode
+    result["hbm_calibration"] = hbm_calibration(achieved)
     if args.cpu_seconds > 0:
         log("CPU baseline (oracle), budget %.0f s" % args.cpu_seconds)
         q0 = synth.queries(wl, args.seed, 0)
         result["cpu_baseline"] = cpu_baseline(wl, args.seed, T, K_dense, V_dense, q0, args.cpu_seconds,
                                               layers, ranks_np, ranks_v_np)
+        result["cpu_baseline"].update(cpu_extras(wl, args.seed, T, K_dense, V_dense, q0, comp_X, req_np,
+                                                 req_v_np, comp_refs))
     print(json.dumps(result), flush=True)
 
 

@@ -434,6 +434,19 @@ pkv_status pkv_cache_bytes(const pkv_cache *c, int32_t layer, const int32_t *seq
 
 /* ---- diagnostics --------------------------------------------------------- */
 
+/* Bandwidth calibration: the best rate (GB/s, bytes moved per second) of
+ * `reps` timed launches (after one untimed) of a plain streaming kernel over
+ * `bytes` bytes of src (device, 16-byte aligned, bytes a multiple of 16),
+ * with `blocks` workgroups of `threads` (64..512, a multiple of 64) threads,
+ * 16-byte loads, four in flight per thread. mode 0: read, one grid-stride
+ * sweep; mode 2: read, each workgroup taking contiguous 64 KB chunks (dst
+ * receives one 4-byte word per thread in both); modes 1 and 3: copy src to
+ * dst with the same two patterns (bytes moved = 2 * bytes). Synchronizes the
+ * stream. It states the attention rates against what the chip's HBM gives a
+ * simple stream. */
+pkv_status pkv_bandwidth_probe(const void *src, void *dst, int64_t bytes, int32_t mode, int32_t reps,
+                               int32_t blocks, int32_t threads, double *gbps, pkv_stream s);
+
 /* Synchronizes the stream, then returns (and clears) the current device's
  * sticky status bits (PKV_DEV_*) in *bits. */
 pkv_status pkv_device_status(pkv_stream s, uint32_t *bits);

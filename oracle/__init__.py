@@ -71,6 +71,8 @@ def _load():
     lib.orc_attention_pagewise.restype = i32
     lib.orc_num_threads.argtypes = []
     lib.orc_num_threads.restype = i32
+    lib.orc_set_num_threads.argtypes = [i32]
+    lib.orc_set_num_threads.restype = None
     _ = dbl
     _lib = lib
     return lib
@@ -83,6 +85,11 @@ def _ptr(a: np.ndarray):
 def num_threads() -> int:
     """OpenMP threads the oracle's parallel loops use."""
     return int(_load().orc_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Sets the OpenMP threads of the oracle's parallel loops (timing only)."""
+    _load().orc_set_num_threads(int(n))
 
 
 # --------------------------------------------------------------------------

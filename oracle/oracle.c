@@ -483,3 +483,15 @@ int orc_num_threads(void)
     return 1;
 #endif
 }
+
+/* Sets the number of OpenMP threads of the parallel loops above (for timing
+ * the oracle on one core and on all of them); no effect without OpenMP. */
+void orc_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    extern void omp_set_num_threads(int);
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}

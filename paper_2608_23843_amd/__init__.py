@@ -63,6 +63,19 @@ def global_rank(T: int, P: int, S: int, W: int, d: int, rho: float) -> int:
     return r
 
 
+def bandwidth_probe(src, dst, mode: int, reps: int = 5, blocks: int = 2048, threads: int = 256, stream=None) -> float:
+    """pkv_bandwidth_probe over device tensors src (and dst): GB/s of a plain
+    streaming read (mode 0 grid-stride, 2 in 64 KB chunks per workgroup) or
+    copy (modes 1 and 3)."""
+    import torch
+    lib = _lib.load()
+    out = ctypes.c_double(0.0)
+    check(lib.pkv_bandwidth_probe(src.data_ptr(), dst.data_ptr(), src.numel() * src.element_size(), mode, reps,
+                                  blocks, threads, ctypes.byref(out), _stream_handle(torch, stream)),
+          "pkv_bandwidth_probe")
+    return float(out.value)
+
+
 def _stream_handle(torch, stream=None):
     s = stream if stream is not None else torch.cuda.current_stream()
     return ctypes.c_void_p(s.cuda_stream)

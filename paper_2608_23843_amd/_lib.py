@@ -28,7 +28,7 @@ EXPORTS = [
     "pkv_export_block_elems", "pkv_export_pages", "pkv_int4_blob_bytes", "pkv_export_int4_pages",
     "pkv_device_status", "pkv_compress_sweeps", "pkv_cache_bytes", "pkv_last_error", "pkv_version",
     "pkv_global_basis_bytes", "pkv_global_coef_bytes", "pkv_global_rank", "pkv_global_prefill",
-    "pkv_global_attention", "pkv_global_export",
+    "pkv_global_attention", "pkv_global_export", "pkv_bandwidth_probe",
 ]
 
 
@@ -106,6 +106,7 @@ def load():
         "pkv_global_prefill": ([cp, gp, i32, vp, vp, i64, vp, vp, sz, vp], i32),
         "pkv_global_attention": ([cp, gp, i32, vp, vp, vp, vp, vp, sz, vp], i32),
         "pkv_global_export": ([cp, gp, i32, i32, i32, i64, vp, vp, vp, vp, vp], i32),
+        "pkv_bandwidth_probe": ([vp, vp, i64, i32, i32, i32, i32, ctypes.POINTER(ctypes.c_double), vp], i32),
         "pkv_last_error": ([], ctypes.c_char_p),
         "pkv_version": ([], ctypes.c_char_p),
     }

@@ -14,7 +14,7 @@ LIB = os.path.join(HERE, "libpuzzlekv.so")
 
 SOURCES = ["pkv_kernels.hip", "pkv_host.cpp"]
 DEPS = ["pkv_internal.h", "cache_ops.inl", "int4.inl", "compress.inl", "compress_qr.inl", "attention.inl", "attention_mfma.inl", "attention_q4.inl",
-        "attention_launch.inl", "global_svd.inl"]
+        "attention_launch.inl", "global_svd.inl", "bandwidth.inl"]
 
 
 def hipcc() -> str:

@@ -755,6 +755,19 @@ pkv_status pkv_cache_bytes(const pkv_cache *c, int32_t layer, const int32_t *seq
     return PKV_OK;
 }
 
+pkv_status pkv_bandwidth_probe(const void *src, void *dst, int64_t bytes, int32_t mode, int32_t reps,
+                               int32_t blocks, int32_t threads, double *gbps, pkv_stream s) {
+    if (!src || !dst || !gbps) return fail(PKV_E_ARG, "src, dst or gbps is NULL");
+    if (bytes <= 0 || bytes % 16 || ((uintptr_t)src | (uintptr_t)dst) % 16)
+        return fail(PKV_E_ARG, "bytes must be a positive multiple of 16 and the buffers 16-byte aligned");
+    if (mode < 0 || mode > 3 || reps < 1 || blocks < 1 || blocks > (1 << 20) || threads < 64 || threads > 512 ||
+        threads % 64)
+        return fail(PKV_E_ARG, "mode %d, reps %d, blocks %d or threads %d out of range", mode, reps, blocks, threads);
+    hipError_t e = bandwidth_probe(src, dst, bytes, mode, reps, blocks, threads, gbps, (hipStream_t)s);
+    if (e != hipSuccess) return hip_fail(e, "pkv_bandwidth_probe");
+    return PKV_OK;
+}
+
 pkv_status pkv_device_status(pkv_stream s, uint32_t *bits) {
     if (!bits) return fail(PKV_E_ARG, "bits is NULL");
     hipError_t e = hipStreamSynchronize((hipStream_t)s);

@@ -221,6 +221,9 @@ hipError_t launch_global_attention(const LaunchCtx &L, const GlobalGeo &gg, cons
 hipError_t launch_global_export(const LaunchCtx &L, const GlobalGeo &gg, const pkv_global *gl, int b, int h,
                                 int64_t n_rows, float *bk, float *bv, float *ak, float *av);
 
+hipError_t bandwidth_probe(const void *src, void *dst, int64_t bytes, int mode, int reps, int blocks, int threads,
+                           double *gbps, hipStream_t stream);
+
 struct AttnPlan {
     int pages_per_chunk;
     int n_chunks;

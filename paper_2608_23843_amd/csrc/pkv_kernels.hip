@@ -19,3 +19,4 @@
 #include "attention_mfma.inl"
 #include "attention_launch.inl"
 #include "global_svd.inl"
+#include "bandwidth.inl"

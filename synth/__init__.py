@@ -74,8 +74,11 @@ WORKLOADS = {
     # 1 layer, 1 KV head, 1 query head, d=64, P=16, T=256, sink 16, window 32, r=4, fp32.
     "tiny": Workload("tiny", 1, 1, 1, 1, 64, 16, 256, 16, 32, 4, (4,), "f32", None, 0),
     # Llama-3-8B-shaped layer: 32 q / 8 kv heads, d=128, P=64, T=32K, batch 1, r=24, bf16.
+    # A decode step runs 32 such layers (Llama-3-8B's depth), each with its own
+    # buffers: 32 x 76 MB is far beyond the 256 MB last-level cache, so every
+    # layer's pages come from HBM.
     "llama8b_32k": Workload("llama8b_32k", 2, 1, 8, 32, 128, 64, 32768, 64, 256, 24, (24,),
-                            "bf16", 5.0e5, 4),
+                            "bf16", 5.0e5, 4, layers=32),
     # Qwen3-32B-shaped layer: 64 q / 8 kv heads, d=128, P=64, T=128K, batch 4,
     # r uniform over {16, 24, 32}; a decode step runs 64 such layers.
     "qwen32b_128k": Workload("qwen32b_128k", 3, 4, 8, 64, 128, 64, 131072, 64, 512, 24,

@@ -239,3 +239,15 @@ def test_global_rank_matches_oracle_accounting(pk, T, P, S, W, rho):
     kinds = oracle.plan_pages(T, P, S, W)
     n_fact = int(sum(min(P, T - j * P) for j, k in enumerate(kinds) if k == oracle.FACTOR))
     assert pk.global_rank(T, P, S, W, 128, rho) == accounting.global_rank(T - n_fact, n_fact, 128, rho)
+
+
+def test_bandwidth_probe_argument_errors(pk):
+    """pkv_bandwidth_probe checks its arguments before launching anything."""
+    lib = pk.load_library()
+    vp = ctypes.c_void_p
+    g = ctypes.c_double(0.0)
+    assert lib.pkv_bandwidth_probe(None, vp(0x1000), 1024, 0, 1, 64, 256, ctypes.byref(g), None) == 1
+    assert lib.pkv_bandwidth_probe(vp(0x1000), vp(0x2000), 1000, 0, 1, 64, 256, ctypes.byref(g), None) == 1
+    assert lib.pkv_bandwidth_probe(vp(0x1008), vp(0x2000), 1024, 0, 1, 64, 256, ctypes.byref(g), None) == 1
+    assert lib.pkv_bandwidth_probe(vp(0x1000), vp(0x2000), 1024, 4, 1, 64, 256, ctypes.byref(g), None) == 1
+    assert lib.pkv_bandwidth_probe(vp(0x1000), vp(0x2000), 1024, 0, 1, 64, 100, ctypes.byref(g), None) == 1
