@@ -455,6 +455,13 @@ def test_int4_zero_and_exact_grid():
     x = c * 0.25
     codes, sc = int4.quantize_lines(x, 0)
     assert np.array_equal(codes[:, 0], c[:, 0].astype(np.int8)) and sc[0, 0] == 0.25
+    # exact half steps round to the even code (reading: round half to even;
+    # rounding half away from zero would give 1, 3, -1, -3, 7 at 0.5, 2.5,
+    # -0.5, -2.5 and 6.5): the run's maximum 1.75 fixes s = 0.25 exactly
+    h = np.array([[7, 0.5, 1.5, 2.5, -0.5, -1.5, -2.5, 3.5, -3.5, 6.5, -6.5]], dtype=np.float64).T
+    codes, sc = int4.quantize_lines(h * 0.25, 0)
+    assert sc[0, 0] == 0.25
+    assert codes[:, 0].tolist() == [7, 0, 2, 2, 0, -2, -2, 4, -4, 6, -6]
 
 
 # --------------------------------------------------------------------------
