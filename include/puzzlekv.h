@@ -155,7 +155,11 @@ typedef struct {
      * RoPE applied at cache access (Section 4.2 "Main Results"; Appendix
      * "RoPE Key Analysis"). Factor slots then hold R_K transposed (B_Kt
      * above). Needs bf16 dense pages and factors, P = 32 or 64, head_dim =
-     * 64 or 128, max_rank <= 32 and positions below 2^24. */
+     * 64 or 128, max_rank <= 32 and positions below 2^24. The score product
+     * takes the rotated keys as fp16 hi/lo pairs (about 22 bits) and the
+     * queries in fp16, so query and rotated-key entries must stay below
+     * 65504 in magnitude; query entries below fp16's normal range (2^-14)
+     * keep an absolute error under 2^-25. */
     float key_rope_base;
 } pkv_cache;
 

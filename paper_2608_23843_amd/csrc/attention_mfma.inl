@@ -121,6 +121,25 @@ __device__ inline void split_tile(const f32x4 &x0, bf16x8 &hi, bf16x8 &lo) {
     lo = __builtin_bit_cast(bf16x8, u32x4{l0, l1, 0u, 0u});
 }
 
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
+
+__device__ inline f32x4 mfma_f16(const f16x8 &a, const f16x8 &b, const f32x4 &c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+// fp32 pair -> fp16 hi (toward zero) and lo (the remainder), as packed words.
+// The remainder a - hi is one mixed-precision fma with hi as its fp16
+// operand (the -1 is kept opaque so the compiler keeps the fma form); hi and
+// lo together keep about 22 bits.
+__device__ inline void split2_f16(float a, float b, uint32_t &hi, uint32_t &lo) {
+    const f16x2 h = __builtin_bit_cast(f16x2, __builtin_amdgcn_cvt_pkrtz(a, b));
+    float m1 = -1.f;
+    asm("" : "+v"(m1));
+    hi = __builtin_bit_cast(uint32_t, h);
+    lo = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(fmaf((float)h[0], m1, a), fmaf((float)h[1], m1, b)));
+}
+
 // Operand slices of one factor page held by one lane, in two halves: the key
 // factors feed phase 1 (scores and softmax), the value factors phase 2.
 template <int D, int P>
@@ -328,53 +347,35 @@ __device__ inline void unit_phase1(WaveState<D> &w, const KeyOps<D, P> &f, const
     page_softmax<D, P, false>(w, st, eh, el, P, q, c2);
 }
 
-// Rotation of frequency i at position t (rotate-half RoPE): the angle
-// t theta_i in revolutions, t w_i with w_i = theta_i / 2 pi held as
-// wh + wl; the product t wh is split exactly (fma) so that its integer part
-// drops out before the hardware sine and cosine, which take revolutions.
-__device__ inline void rope_cs(float t, float wh, float wl, float &c, float &s) {
-    const float p = t * wh;
-    const float e = fmaf(t, wh, -p);
-    const float r = __builtin_amdgcn_fractf(p) + fmaf(t, wl, e);
-    c = __builtin_amdgcn_cosf(r);
-    s = __builtin_amdgcn_sinf(r);
+// RoPE angles in revolutions: w_i = theta_i / 2 pi is held in LDS as
+// wh + wl (fp64 on the way). For a unit starting at position t0, each lane
+// computes the fraction of t0 w_i for one frequency (the product split
+// exactly with an fma, so the fraction is right to ~2^-24 at any position
+// below 2^24) into the wave's LDS row f0; the angle of position t0 + tau is
+// then frac(f0_i + tau wh_i), one fma and one fract, and the hardware sine and
+// cosine take revolutions. tau < 64 keeps the fma's rounding below 2^-20
+// revolutions.
+__device__ inline float rope_frac(float t0, float wh, float wl) {
+    const float p = t0 * wh;
+    const float e = fmaf(t0, wh, -p);
+    return __builtin_amdgcn_fractf(__builtin_amdgcn_fractf(p) + fmaf(t0, wl, e));
 }
 
-// Rotates the pairs (x[s][u], x[s + D/64][u]) of one lane's key row at
-// position t, x[s][u] being dim 32 s + 8 q + u (rw: wh[D/2] then wl[D/2]).
+// Rotates the pairs (x0[u], x1[u]) of one lane's key row at offset tau from
+// the unit's start: x0[u] is dim 32 s + 8 q + u, x1[u] its partner d/2 above
+// (rw: wh[D/2], f0: the wave's fractions for the unit).
 template <int D>
-__device__ inline void rope_row(float (&x)[D / 32][8], float t, int q, const float *rw) {
-#pragma unroll
-    for (int s = 0; s < D / 64; ++s)
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const int i0 = 32 * s + 8 * q + 4 * h;
-            const f32x4 wh = *(const f32x4 *)(rw + i0);
-            const f32x4 wl = *(const f32x4 *)(rw + D / 2 + i0);
-#pragma unroll
-            for (int v = 0; v < 4; ++v) {
-                float c, sn;
-                rope_cs(t, wh[v], wl[v], c, sn);
-                const float a = x[s][4 * h + v], b = x[s + D / 64][4 * h + v];
-                x[s][4 * h + v] = a * c - b * sn;
-                x[s + D / 64][4 * h + v] = fmaf(b, c, a * sn);
-            }
-        }
-}
-
-// Rotates the pairs (x0[u], x1[u]) of one lane's key row at position t:
-// x0[u] is dim 32 s + 8 q + u, x1[u] its partner d/2 above.
-template <int D>
-__device__ inline void rope_pair(float (&x0)[8], float (&x1)[8], float t, int s, int q, const float *rw) {
+__device__ inline void rope_pair(float (&x0)[8], float (&x1)[8], float tau, int s, int q, const float *rw,
+                                 const float *f0) {
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
         const int i0 = 32 * s + 8 * q + 4 * h;
         const f32x4 wh = *(const f32x4 *)(rw + i0);
-        const f32x4 wl = *(const f32x4 *)(rw + D / 2 + i0);
+        const f32x4 fr = *(const f32x4 *)(f0 + i0);
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-            float c, sn;
-            rope_cs(t, wh[v], wl[v], c, sn);
+            const float r = __builtin_amdgcn_fractf(fmaf(tau, wh[v], fr[v]));
+            const float c = __builtin_amdgcn_cosf(r), sn = __builtin_amdgcn_sinf(r);
             const float a = x0[4 * h + v], b = x1[4 * h + v];
             x0[4 * h + v] = a * c - b * sn;
             x1[4 * h + v] = fmaf(b, c, a * sn);
@@ -382,34 +383,54 @@ __device__ inline void rope_pair(float (&x0)[8], float (&x1)[8], float t, int s,
     }
 }
 
+// Rotated keys -> fp16 hi/lo A operands of the score product (K entries 8
+// dims of one chunk).
+__device__ inline void split8_f16(const float (&x)[8], f16x8 &hi, f16x8 &lo) {
+    uint32_t hd[4], ld[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) split2_f16(x[2 * u], x[2 * u + 1], hd[u], ld[u]);
+    hi = __builtin_bit_cast(f16x8, u32x4{hd[0], hd[1], hd[2], hd[3]});
+    lo = __builtin_bit_cast(f16x8, u32x4{ld[0], ld[1], ld[2], ld[3]});
+}
+
 // Phase 1 of a unit of a pre-RoPE cache. Factor page: per token tile,
 // K^T = R_K^T L_K^T, rotation, S^T = K Q^T; rank entries at or past r4(rk)
 // of the L_K operand are zeroed (the R_K^T operand holds the next row's
-// values there). Dense unit: the K rows are rotated, then S^T = K Q^T.
-// t0: position of the unit's first token.
+// values there). Dense unit: the K rows are rotated, then S^T = K Q^T. The
+// rotated keys enter the score product as fp16 hi/lo pairs against the query
+// group in fp16 (qh). t0: position of the unit's first token; f0: the wave's
+// LDS row of D/2 floats for the unit's angle fractions.
 template <int D, int P>
-__device__ inline void unit_phase1_rope(WaveState<D> &w, const KeyOps<D, P> &f, const bf16x8 (&qb)[D / 32],
+__device__ inline void unit_phase1_rope(WaveState<D> &w, const KeyOps<D, P> &f, const f16x8 (&qh)[D / 32],
                                         bool dense, int rows, bf16x8 (&eh)[(P + 31) / 32],
                                         bf16x8 (&el)[(P + 31) / 32], int n, int q, float c2, int64_t t0, int rk4,
-                                        const float *rw) {
+                                        const float *rw, float *f0) {
+    {
+        const int lane = q * 16 + n;
+        if (lane < D / 2) f0[lane] = rope_frac((float)t0, rw[lane], rw[D / 2 + lane]);
+        __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): the wave's row is written before it is read
+    }
     if (dense) {
         f32x4 z[2];
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt) {
-            float x[D / 32][8];
-#pragma unroll
-            for (int s = 0; s < D / 32; ++s)
-#pragma unroll
-                for (int u = 0; u < 8; ++u) x[s][u] = (float)f.bk[rt][s][u];
-            rope_row<D>(x, (float)(t0 + rank_row(rt, n)), q, rw);
+            const float tau = (float)rank_row(rt, n);
             z[rt] = zero_f4();
 #pragma unroll
-            for (int s = 0; s < D / 32; ++s) {
-                uint32_t hd[4], ld[4];
+            for (int s0 = 0; s0 < D / 64; ++s0) {
+                float x[2][8];
 #pragma unroll
-                for (int u = 0; u < 4; ++u) split2(x[s][2 * u], x[s][2 * u + 1], hd[u], ld[u]);
-                z[rt] = mfma_bf16(__builtin_bit_cast(bf16x8, u32x4{hd[0], hd[1], hd[2], hd[3]}), qb[s], z[rt]);
-                z[rt] = mfma_bf16(__builtin_bit_cast(bf16x8, u32x4{ld[0], ld[1], ld[2], ld[3]}), qb[s], z[rt]);
+                for (int k = 0; k < 2; ++k)
+#pragma unroll
+                    for (int u = 0; u < 8; ++u) x[k][u] = (float)f.bk[rt][s0 + k * (D / 64)][u];
+                rope_pair<D>(x[0], x[1], tau, s0, q, rw, f0);
+#pragma unroll
+                for (int k = 0; k < 2; ++k) {
+                    f16x8 hi, lo;
+                    split8_f16(x[k], hi, lo);
+                    z[rt] = mfma_f16(hi, qh[s0 + k * (D / 64)], z[rt]);
+                    z[rt] = mfma_f16(lo, qh[s0 + k * (D / 64)], z[rt]);
+                }
             }
         }
         bf16x8 eh1[1], el1[1];
@@ -426,7 +447,7 @@ __device__ inline void unit_phase1_rope(WaveState<D> &w, const KeyOps<D, P> &f, 
         if (!m_lo) am[0] = am[1] = 0u;
         if (!m_hi) am[2] = am[3] = 0u;
         const bf16x8 a = __builtin_bit_cast(bf16x8, am);
-        const float tpos = (float)(t0 + token_row<P>(tt, n));
+        const float tau = (float)token_row<P>(tt, n);
         st[tt] = zero_f4();
         // one rotate-half pair of 32-dim chunks (s, s + d/64) at a time
 #pragma unroll
@@ -440,15 +461,14 @@ __device__ inline void unit_phase1_rope(WaveState<D> &w, const KeyOps<D, P> &f, 
 #pragma unroll
                     for (int v = 0; v < 4; ++v) x[k][4 * hp + v] = kt[v];
                 }
-            rope_pair<D>(x[0], x[1], tpos, s0, q, rw);
+            rope_pair<D>(x[0], x[1], tau, s0, q, rw, f0);
 #pragma unroll
             for (int k = 0; k < 2; ++k) {
-                uint32_t hd[4], ld[4];
-#pragma unroll
-                for (int u = 0; u < 4; ++u) split2(x[k][2 * u], x[k][2 * u + 1], hd[u], ld[u]);
-                const bf16x8 qv = qb[s0 + k * (D / 64)];
-                st[tt] = mfma_bf16(__builtin_bit_cast(bf16x8, u32x4{hd[0], hd[1], hd[2], hd[3]}), qv, st[tt]);
-                st[tt] = mfma_bf16(__builtin_bit_cast(bf16x8, u32x4{ld[0], ld[1], ld[2], ld[3]}), qv, st[tt]);
+                f16x8 hi, lo;
+                split8_f16(x[k], hi, lo);
+                const f16x8 qv = qh[s0 + k * (D / 64)];
+                st[tt] = mfma_f16(hi, qv, st[tt]);
+                st[tt] = mfma_f16(lo, qv, st[tt]);
             }
         }
     }
@@ -710,8 +730,21 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
     // pre-RoPE keys: w_i = theta_i / 2 pi = base^(-2i/d) / 2 pi as wh + wl
     // (fp64 on the way), i < d/2, shared by the workgroup
     const float *rw = nullptr;
+    // pre-RoPE keys: the query group as fp16 B operands of the score product
+    // (exact from bf16 unless below fp16's normal range, where the absolute
+    // error stays under 2^-25)
+    f16x8 qh[KD];
+    if constexpr (ROPE) {
+#pragma unroll
+        for (int s = 0; s < KD; ++s)
+#pragma unroll
+            for (int u = 0; u < 8; ++u) qh[s][u] = (_Float16)(float)qb[s][u];
+    }
+    float *f0 = nullptr;
     if constexpr (ROPE) {
         __shared__ float s_rw[D];
+        __shared__ float s_f0[NW][D / 2];
+        f0 = s_f0[wave];
         if (threadIdx.x < D / 2) {
             const int i = (int)threadIdx.x;
             const double th = exp2(-(2.0 * i / D) * log2((double)g.rope_base));
@@ -846,8 +879,8 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
         const bool live = cur.e.kind != PKV_EMPTY, dns = cur.e.kind == PKV_DENSE;
         if (live) {
             if constexpr (ROPE)
-                unit_phase1_rope<D, P>(w, ko, qb, dns, rows, eh, el, n, q4, c2,
-                                       cur.j * P + (int64_t)UT * cur.half, r4(cur.e.rank_k), rw);
+                unit_phase1_rope<D, P>(w, ko, qh, dns, rows, eh, el, n, q4, c2,
+                                       cur.j * P + (int64_t)UT * cur.half, r4(cur.e.rank_k), rw, f0);
             else
                 unit_phase1<D, P>(w, ko, qb, dns, rows, eh, el, q4, c2);
         }

@@ -27,12 +27,6 @@
 
 namespace pkv {
 
-typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
-typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
-
-__device__ inline f32x4 mfma_f16(const f16x8 &a, const f16x8 &b, const f32x4 &c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
-}
 
 // Loop-invariant unpack constants, held in registers (kept opaque so the
 // compiler forms one v_and_or_b32 per pair of codes).
@@ -80,16 +74,6 @@ __device__ inline u32x4 q4_scale_div16(const u32x4 &sc) {
     o[1] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, s1) * r16);
     o[3] = __builtin_bit_cast(uint32_t, __builtin_bit_cast(f16x2, s3) * r16);
     return o;
-}
-// fp32 pair -> fp16 hi (toward zero) and lo (the remainder), as packed words.
-// The remainder a - hi is one mixed-precision fma with hi as its fp16
-// operand (the -1 is kept opaque so the compiler keeps the fma form).
-__device__ inline void split2_f16(float a, float b, uint32_t &hi, uint32_t &lo) {
-    const f16x2 h = __builtin_bit_cast(f16x2, __builtin_amdgcn_cvt_pkrtz(a, b));
-    float m1 = -1.f;
-    asm("" : "+v"(m1));
-    hi = __builtin_bit_cast(uint32_t, h);
-    lo = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_pkrtz(fmaf((float)h[0], m1, a), fmaf((float)h[1], m1, b)));
 }
 __device__ inline void split_tiles_f16(const f32x4 &x0, const f32x4 &x1, f16x8 &hi, f16x8 &lo) {
     uint32_t h0, h1, h2, h3, l0, l1, l2, l3;
