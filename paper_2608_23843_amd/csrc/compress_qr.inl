@@ -51,6 +51,41 @@ __device__ inline float cq_elem(const uint16_t *X, bool transposed, int P, int d
     return bf16_to_f32(transposed ? X[(int64_t)k * P + t] : X[(int64_t)t * d + k]);
 }
 
+typedef float cq_f32x2 __attribute__((ext_vector_type(2)));
+typedef __bf16 cq_bf16x2 __attribute__((ext_vector_type(2)));
+
+// Two fp32 values as a packed bf16 pair, rounded to nearest even.
+__device__ inline uint32_t cq_pack_bf16(float a, float b) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(cq_f32x2{a, b}, cq_bf16x2));
+}
+// Two fp32 values -> bf16 pair hi and bf16 pair lo of the remainders
+// (hi + lo carries 16 significant bits).
+__device__ inline void cq_split2(float a, float b, uint32_t &hi, uint32_t &lo) {
+    hi = cq_pack_bf16(a, b);
+    lo = cq_pack_bf16(a - __uint_as_float(hi << 16), b - __uint_as_float(hi & 0xffff0000u));
+}
+// Page dims k and k + 1 (k even) over tokens t0..t0+7 as two MFMA operands:
+// one 4-byte read per token row, split into its even and odd dim.
+__device__ inline void cq_load_dim_pair(const uint16_t *X, bool transposed, int P, int d, int k, int t0,
+                                        cq_bf16x8 &be, cq_bf16x8 &bo) {
+    if (transposed) {   // d x P: eight tokens of one dim are contiguous
+        be = __builtin_bit_cast(cq_bf16x8, *(const uint4 *)(X + (int64_t)k * P + t0));
+        bo = __builtin_bit_cast(cq_bf16x8, *(const uint4 *)(X + (int64_t)(k + 1) * P + t0));
+        return;
+    }
+    uint32_t w[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) w[i] = *(const uint32_t *)(X + (int64_t)(t0 + i) * d + k);
+    uint32_t e[4], o[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        e[i] = __builtin_amdgcn_perm(w[2 * i + 1], w[2 * i], 0x05040100u);   // low halves: dim k
+        o[i] = __builtin_amdgcn_perm(w[2 * i + 1], w[2 * i], 0x07060302u);   // high halves: dim k + 1
+    }
+    be = __builtin_bit_cast(cq_bf16x8, make_uint4(e[0], e[1], e[2], e[3]));
+    bo = __builtin_bit_cast(cq_bf16x8, make_uint4(o[0], o[1], o[2], o[3]));
+}
+
 __device__ inline float cq_f(int v) { return __int_as_float(v); }
 __device__ inline int cq_i(float v) { return __float_as_int(v); }
 
@@ -271,15 +306,15 @@ void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor, Comp
         float x[P];
 #pragma unroll
         for (int e = 0; e < P; ++e) x[e] = cq_group_bcast<P>(gc[e], piv0, piv1, grp);
-        float nx2a = 0.f, nx2b = 0.f, da = 0.f, db = 0.f;
+        float da = 0.f, db = 0.f;
 #pragma unroll
         for (int e = 0; e < P; e += 2) {
-            nx2a = fmaf(x[e], x[e], nx2a);
-            nx2b = fmaf(x[e + 1], x[e + 1], nx2b);
             da = fmaf(x[e], gc[e], da);
             db = fmaf(x[e + 1], gc[e + 1], db);
         }
-        const float nx2 = nx2a + nx2b, dot = da + db;
+        const float dot = da + db;
+        // the pivot's column is x, so its dot is |x|^2: no lane sums squares
+        const float nx2 = cq_group_bcast<P>(dot, piv0, piv1, grp);
         const float inv = nx2 > kCqTiny2 ? __builtin_amdgcn_rsqf(nx2) : 0.f;
         const float rk = done ? 0.f : dot * inv;          // R[k][c]
         const float f = done ? 0.f : rk * inv;            // projection coefficient
@@ -318,7 +353,7 @@ void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor, Comp
     // exactly what an fp32 cache stores), keep the tight one.
     constexpr float kTolFactor = std::is_same<TF, uint16_t>::value ? 100.f : 1.f;
     const float tol = kTolFactor * (float)P * 1.1920929e-7f;
-    const float stop_tol = sqrtf(tol);
+    const float tol2 = tol * tol;   // the tests compare squares: |gamma| > tol sqrt(a_lo a_hi)
     // requested rank, 0 for a rank chosen from the spectrum (adaptive ranks).
     // Then each sweep estimates that rank from the current column norms, and
     // the two columns after it are converged too (at most r_cap): a sweep
@@ -363,14 +398,15 @@ void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor, Comp
         const float gamma = gt * dsc * dp;
         const bool lo = c < partner;
         const float a_lo = lo ? alpha : beta, a_hi = lo ? beta : alpha;
-        const float norm_pair = sqrtf(a_lo * a_hi);
-        const bool rot = a_lo > kCqTiny2 && a_hi > kCqTiny2 && fabsf(gamma) > tol * norm_pair;
+        const float prod = a_lo * a_hi, g2 = gamma * gamma;
+        const bool rot = a_lo > kCqTiny2 && a_hi > kCqTiny2 && g2 > tol2 * prod;
         const float zeta = (a_hi - a_lo) * __builtin_amdgcn_rcpf(2.f * gamma);
         const float tz = __builtin_copysignf(
             __builtin_amdgcn_rcpf(fabsf(zeta) + __builtin_amdgcn_sqrtf(fmaf(zeta, zeta, 1.f))), zeta);
         const float t = rot ? tz : 0.f;
         const float cs = rot ? __builtin_amdgcn_rsqf(fmaf(t, t, 1.f)) : 1.f;
-        rotated |= (rot && ((tag | tag_p) >> 8) && fabsf(gamma) > stop_tol * norm_pair) ? 1 : 0;
+        // a rotation touching the top columns above sqrt(tol) in cosine
+        rotated |= (rot && ((tag | tag_p) >> 8) && g2 > tol * prod) ? 1 : 0;
         const float t_eff = lo ? -t : t;   // the lower column takes -sin
         const float mu = t_eff * (dp * __builtin_amdgcn_rcpf(dsc));
 #pragma unroll
@@ -565,7 +601,100 @@ void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor, Comp
     int8_t *sRc = (int8_t *)(cq_smem + 64 + 64 * 32 + 64 + 64);   // INT4 only: R~ codes (P = 64: one group per wave)
     Int4Layout f4{};
     if constexpr (kQ4) f4 = int4_layout(P, d, rk, rv);
-    for (int k0 = 0; k0 < d; k0 += kCols * P) {
+    // bf16 and INT4 factors at P = 64: the projection on the matrix cores.
+    // 32x32x16 bf16 products with A = L^T (rank lane % 32; tokens
+    // 16 s + 8 (lane / 32) + 0..7 of k-step s) split into bf16 hi + lo, so L
+    // enters with 16 significant bits, and B = X, exact. Lane (n, h) owns
+    // dims k = 64 J + 2 n and k + 1 in two accumulator tiles, so one
+    // 4-byte page read feeds both; accumulator register v holds rank
+    // 8 (v / 4) + 4 h + v % 4 of its dim. fp32 factors take the exact VALU
+    // loop below.
+    constexpr bool kMfmaProj = P == 64 && !std::is_same<TF, float>::value;
+    if constexpr (kMfmaProj) {
+        const int n = lane & 31, h = lane >> 5;
+        float isg[16];   // INT4: 1 / sigma of this lane's ranks
+        if constexpr (kQ4) {
+#pragma unroll
+            for (int v = 0; v < 16; ++v) isg[v] = sInvSig[8 * (v >> 2) + 4 * h + (v & 3)];
+        }
+        // one block of 64 dims at a time: two accumulator tiles
+#pragma unroll 1
+        for (int k = 2 * n; k - 2 * n < d; k += 64) {
+            cq_f32x16 ae = {}, ao = {};
+            const bool kin = k < d;
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                uint32_t hw[4], lw[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    cq_split2(sL[(16 * s + 8 * h + 2 * i) * 32 + n], sL[(16 * s + 8 * h + 2 * i + 1) * 32 + n], hw[i], lw[i]);
+                const cq_bf16x8 ahi = __builtin_bit_cast(cq_bf16x8, make_uint4(hw[0], hw[1], hw[2], hw[3]));
+                const cq_bf16x8 alo = __builtin_bit_cast(cq_bf16x8, make_uint4(lw[0], lw[1], lw[2], lw[3]));
+                cq_bf16x8 be = {}, bo = {};
+                if (kin) cq_load_dim_pair(X, ref.transposed, P, d, k, 16 * s + 8 * h, be, bo);
+                ae = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ahi, be, ae, 0, 0, 0);
+                ao = __builtin_amdgcn_mfma_f32_32x32x16_bf16(ahi, bo, ao, 0, 0, 0);
+                ae = __builtin_amdgcn_mfma_f32_32x32x16_bf16(alo, be, ae, 0, 0, 0);
+                ao = __builtin_amdgcn_mfma_f32_32x32x16_bf16(alo, bo, ao, 0, 0, 0);
+            }
+            if (!kin) continue;
+            if constexpr (kQ4) {
+                // R~ = Sigma^(-1/2) R (the products used L~ = L Sigma^(1/2));
+                // a dim's scale spans all ranks: this lane's 16 and lane ^ 32's
+#pragma unroll
+                for (int u = 0; u < 2; ++u) {
+                    cq_f32x16 &a = u == 0 ? ae : ao;
+                    float amax = 0.f;
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        a[v] *= isg[v];
+                        if (8 * (v >> 2) + 4 * h + (v & 3) < r) amax = fmaxf(amax, fabsf(a[v]));
+                    }
+                    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(amax), __float_as_uint(amax),
+                                                                     false, false);
+                    amax = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1]));   // the same in both lanes
+                    const uint16_t hs = f16_rne((double)amax / (double)kQ4Max);
+                    if (h == 0)
+                        *(uint16_t *)(factor + slot_off + (which == 0 ? q4_rk_scale(f4, k + u) : q4_rv_scale(f4, k + u))) = hs;
+                    const float sc = half_bits_to_f32(hs);
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        const int rr = 8 * (v >> 2) + 4 * h + (v & 3);
+                        const int8_t code = (int8_t)(rr < r ? q4_code(a[v], sc) : 0);
+                        if (which == 0) sRc[rr * d + k + u] = code;
+                        else sRc[(k + u) * 32 + rr] = code;
+                    }
+                }
+            } else {
+                const int rk4 = r4(rk), rv4 = r4(rv);
+                const FactorLayout fl = factor_layout(P, d, rk, rv, g.key_t != 0);
+                uint16_t *Ak = (uint16_t *)(factor + slot_off);
+                if (which == 0 && !g.key_t) {
+                    uint16_t *Bk = Ak + fl.bk;             // R_K, rk x d: dims k, k + 1 side by side
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        const int a = 8 * (v >> 2) + 4 * h + (v & 3);
+                        if (a < rk) *(uint32_t *)(Bk + (int64_t)a * d + k) = cq_pack_bf16(ae[v], ao[v]);
+                    }
+                } else {
+                    // R_K^T (d x r4(rk)) or R_V^T (d x r4(rv)), zero past the rank:
+                    // four consecutive ranks per 8-byte store
+                    const int rw = which == 0 ? rk4 : rv4;
+                    uint16_t *Bt = Ak + (which == 0 ? fl.bk : fl.bvt);
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int a0 = 8 * j + 4 * h;
+                        if (a0 >= rw) continue;
+                        *(uint2 *)(Bt + (int64_t)k * rw + a0) =
+                            make_uint2(cq_pack_bf16(ae[4 * j], ae[4 * j + 1]), cq_pack_bf16(ae[4 * j + 2], ae[4 * j + 3]));
+                        *(uint2 *)(Bt + (int64_t)(k + 1) * rw + a0) =
+                            make_uint2(cq_pack_bf16(ao[4 * j], ao[4 * j + 1]), cq_pack_bf16(ao[4 * j + 2], ao[4 * j + 3]));
+                    }
+                }
+            }
+        }
+    }
+    for (int k0 = 0; k0 < (kMfmaProj ? 0 : d); k0 += kCols * P) {
         const int k = k0 + kCols * c;
         const bool kin = k < d;
         float acc[kCols][32];
