@@ -25,8 +25,14 @@
 //     between groups of steps), without accumulating the rotations: at
 //     convergence the columns are lambda_c u_c with u_c the eigenvectors, so
 //     L is the normalized columns, orthonormal to the rotation threshold.
-//  4. Ranking and eigenvectors; then R = L^T X with L staged in LDS and
-//     each lane owning two output dims (coalesced page-row reads), stores.
+//  4. Ranking and eigenvectors; then R = L^T X with L staged in LDS: on
+//     32x32x16 bf16 matrix-core products at P = 64 (L as a bf16 hi + lo
+//     pair against the exact page) for bf16 and INT4 factors, otherwise
+//     fp32 fmas with each lane owning two output dims; stores.
+//     The page is read again here: holding it from phase 1 would take 64
+//     more registers per lane (two waves per SIMD instead of three) or 16 KB
+//     of LDS per wave, and the kernel is bound by its vector-ALU issue, not
+//     by the second read (about 0.2 TB/s).
 // Included by pkv_kernels.hip after compress.inl.
 
 namespace pkv {
@@ -384,17 +390,14 @@ void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor, Comp
             default: cq_swz<P, 31>(gc, pg, alpha, beta, dsc, dp, tag, tag_p); break;
 #undef PKV_CQ_CASE
         }
-        float ga = 0.f, gb = 0.f, gcc = 0.f, gd = 0.f;
+        // one accumulation chain (three fewer adds per step than four
+        // partial sums, and measured faster); the partner lane sums the same
+        // products in the same order, so both see the same gt
+        float gt = 0.f;
 #pragma unroll
-        for (int e = 0; e < P; e += 4) {
-            ga = fmaf(gc[e], pg[e], ga);
-            gb = fmaf(gc[e + 1], pg[e + 1], gb);
-            gcc = fmaf(gc[e + 2], pg[e + 2], gcc);
-            gd = fmaf(gc[e + 3], pg[e + 3], gd);
-        }
-        const float gt = (ga + gb) + (gcc + gd);
+        for (int e = 0; e < P; ++e) gt = fmaf(gc[e], pg[e], gt);
         const int partner = c ^ m;
-        larger += (beta > alpha || (beta == alpha && (tag_p & 255) < (tag & 255))) ? 1 : 0;
+        larger += (int)(beta > alpha) | ((int)(beta == alpha) & (int)((tag_p & 255) < (tag & 255)));
         const float gamma = gt * dsc * dp;
         const bool lo = c < partner;
         const float a_lo = lo ? alpha : beta, a_hi = lo ? beta : alpha;
