@@ -93,14 +93,23 @@ __device__ inline float ld_dev(const float *p) {
 }
 
 // Called by every thread of an NT-thread workgroup after its partial stores.
-// The workgroup that completes the head merges all of its chunks (Eq. (5)):
-// each thread owns a few (query, dim) outputs and folds the chunks in
-// groups of eight, issuing a group's loads (max, normalizer, output) at once
-// and rescaling its running state once per group.
+// The workgroup that completes the head merges all of its chunks (Eq. (5)).
+// Chunks are folded in groups of kMergeGroup. A group's maxima and
+// normalizers are read once, one or two per thread, and passed through LDS;
+// each thread's kMergeGroup partial outputs are in flight with them, so a
+// group costs one round trip to memory (kMergeGroup + 2 loads stay within a
+// wave's 63 outstanding vector loads). The loads are unconditional (a chunk
+// past the end reads the last one and is masked), which keeps this code
+// short: it runs once per launch, from a cold instruction cache.
+constexpr int kMergeGroup = 32;
+
 template <int NT>
 __device__ void publish_and_merge(const Geo &g, int64_t head, const Partials &pp, float *out, float *lse,
                                   int64_t T) {
+    constexpr int kMaxG = 16;                                      // the kernels' query-group limit
+    constexpr int MLT = (kMaxG * kMergeGroup + NT - 1) / NT;       // group maxima per thread
     __shared__ unsigned int s_prev;
+    __shared__ float s_mg[kMaxG * kMergeGroup], s_lg[kMaxG * kMergeGroup];
     const int tid = threadIdx.x;
     const int nc = pp.nc;
     __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0): this thread's partial stores have completed
@@ -111,39 +120,58 @@ __device__ void publish_and_merge(const Geo &g, int64_t head, const Partials &pp
 
     const int G = g.g, d = g.d;
     const int b = (int)(head / g.Hkv), h = (int)(head % g.Hkv);
-    for (int idx = tid; idx < G * d; idx += NT) {
+    // the same trip counts in every thread: the group loop holds barriers
+    for (int base = 0; base < G * d; base += NT) {
+        const int idx = min(base + tid, G * d - 1);   // threads past the end redo the last output, unstored
         const int qi = idx / d, k = idx % d;
-        const float *mp = pp.m + pp.mi(head, qi, 0), *lp = pp.l + pp.mi(head, qi, 0);
         const float *op = pp.o + pp.oi(head, qi, k, 0);
-        const int64_t cm = G, co = (int64_t)G * d;   // chunk strides
+        const int co = G * d;   // chunk stride of the outputs
         float M = -INFINITY, L = 0.f, A = 0.f;
-        for (int c0 = 0; c0 < nc; c0 += 8) {
-            float mv[8], lv[8], ov[8];
+        for (int c0 = 0; c0 < nc; c0 += kMergeGroup) {
+            float mreg[MLT], lreg[MLT];
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const bool ok = c0 + u < nc;
-                mv[u] = ok ? ld_dev(mp + (c0 + u) * cm) : -INFINITY;
-                lv[u] = ok ? ld_dev(lp + (c0 + u) * cm) : 0.f;
-                ov[u] = ok ? ld_dev(op + (c0 + u) * co) : 0.f;
+            for (int i = 0; i < MLT; ++i) {
+                const int t = tid + i * NT;
+                const int qm = min(t / kMergeGroup, G - 1), cu = min(c0 + t % kMergeGroup, nc - 1);
+                mreg[i] = ld_dev(pp.m + pp.mi(head, qm, cu));
+                lreg[i] = ld_dev(pp.l + pp.mi(head, qm, cu));
             }
+            float ov[kMergeGroup];
+#pragma unroll
+            for (int u = 0; u < kMergeGroup; ++u) ov[u] = ld_dev(op + (uint32_t)(min(c0 + u, nc - 1) * co));
+            __syncthreads();   // the previous group's maxima have been read
+#pragma unroll
+            for (int i = 0; i < MLT; ++i) {
+                const int t = tid + i * NT;
+                if (t < kMaxG * kMergeGroup) {
+                    s_mg[t] = (t % kMergeGroup) < nc - c0 ? mreg[i] : -INFINITY;
+                    s_lg[t] = lreg[i];
+                }
+            }
+            __syncthreads();
+            const float *mg = s_mg + qi * kMergeGroup, *lg = s_lg + qi * kMergeGroup;
             float Mg = M;
 #pragma unroll
-            for (int u = 0; u < 8; ++u) Mg = fmaxf(Mg, mv[u]);
+            for (int u = 0; u < kMergeGroup; ++u) Mg = fmaxf(Mg, mg[u]);
             if (Mg == -INFINITY) continue;   // no tokens in any chunk so far
-            const float sc = M == -INFINITY ? 0.f : exp2f(M - Mg);
+            // arguments <= 0 with Mg finite: the hardware exp2 gives 0 for -inf
+            // (an empty chunk, or no state yet) and needs no range fix-up
+            const float sc = __builtin_amdgcn_exp2f(M - Mg);
             L *= sc;
             A *= sc;
 #pragma unroll
-            for (int u = 0; u < 8; ++u) {
-                const float wgt = mv[u] == -INFINITY ? 0.f : exp2f(mv[u] - Mg);
-                L = fmaf(wgt, lv[u], L);
+            for (int u = 0; u < kMergeGroup; ++u) {
+                const float wgt = __builtin_amdgcn_exp2f(mg[u] - Mg);
+                L = fmaf(wgt, lg[u], L);
                 A = fmaf(wgt, ov[u], A);
             }
             M = Mg;
         }
-        const bool empty = T <= 0 || !(L > 0.f);
-        out[((int64_t)b * g.Hq + h * G + qi) * d + k] = empty ? 0.f : A / L;
-        if (lse && k == 0) lse[(int64_t)b * g.Hq + h * G + qi] = empty ? -INFINITY : (M + log2f(L)) * kLn2;
+        if (base + tid < G * d) {
+            const bool empty = T <= 0 || !(L > 0.f);
+            out[((int64_t)b * g.Hq + h * G + qi) * d + k] = empty ? 0.f : A / L;
+            if (lse && k == 0) lse[(int64_t)b * g.Hq + h * G + qi] = empty ? -INFINITY : (M + log2f(L)) * kLn2;
+        }
     }
     if (tid == 0) {
         __hip_atomic_store(&pp.counters[head], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

@@ -566,9 +566,9 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
         const uint16_t *qp = q + ((int64_t)b * g.Hq + (int64_t)h * G + n) * D + 8 * q4;
 #pragma unroll
         for (int s = 0; s < KD; ++s) qb[s] = n < G ? ld_b8(qp + 32 * s) : zero8();
-        // complete before the page loop: a load still pending on entry would
-        // make the first wait inside the loop body a full drain on every page
-        __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0)
+        // completed before the page loop (a load still pending on entry
+        // would make the first wait inside the loop body a full drain on
+        // every page); the bf16 path first issues its first table reads
     }
 
     // merge buffers; the INT4 kernel also keeps its O^T accumulators in s_o
@@ -626,6 +626,7 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
         // subnormal); one copy per workgroup (every wave serves this head),
         // read per page instead of held in registers
         __shared__ f16x8 s_qh[4][64];
+        __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0): the query
         if (threadIdx.x == 0) s_nd = 0u;
         if (wave == 0) {
 #pragma unroll
@@ -727,6 +728,67 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
     // at once. So all waves arrive at the same number of barriers, whatever
     // mix of factor pages and multi-unit dense pages each one streams.
     __shared__ unsigned int s_blk[4];
+    int round = 0;
+    bool blocks_done = false;
+    // Wave 0's block claim is issued at the top of a loop iteration and read
+    // at the bottom of the same iteration (the vector memory counter is in
+    // order: read later, its wait would also cover the loads issued after
+    // it); the value is held until take_page publishes it. A claim is taken
+    // synchronously only where none is held: the last rounds, when a wave's
+    // page is past the end.
+    unsigned int blk_next = 0u;
+    bool blk_ready = false, need_blk = false;   // wave 0 only
+    auto sync_claim = [&]() -> unsigned int {
+        unsigned int k = 0u;
+        if (lane == 0) k = __hip_atomic_fetch_add(pp.claim(head), (unsigned int)NW, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return (unsigned int)__builtin_amdgcn_readfirstlane((int)k);
+    };
+    auto needs_blk = [&]() -> bool { return wave == 0 && need_blk; };
+    auto issue_blk = [&]() -> unsigned int {
+        unsigned int k = 0u;
+        if (lane == 0) k = __hip_atomic_fetch_add(pp.claim(head), (unsigned int)NW, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return k;
+    };
+    auto take_blk = [&](unsigned int k) {
+        asm volatile("" : "+v"(k));
+        blk_next = (unsigned int)__builtin_amdgcn_readfirstlane((int)k);
+        blk_ready = true;
+        need_blk = false;
+    };
+    // Round 0 is static: workgroup c streams block c (pages c NW .. c NW +
+    // NW - 1) with no claim, and the head's counter hands out the blocks
+    // after the first n_chunks (a claim k is block n_chunks NW + k). The
+    // first table entries, wave 0's claim of the next block and the query
+    // are then in flight together: one memory round trip before the first
+    // page's loads instead of four in a row.
+    auto take_page = [&]() -> Claim {
+        unsigned int base;
+        if (round == 0) {
+            base = (unsigned int)chunk * (unsigned int)NW;
+            if (wave == 0) need_blk = true;
+        } else {
+            if (wave == 0) {
+                const unsigned int v = blk_ready ? blk_next : sync_claim();
+                if (lane == 0) s_blk[round & 3] = v + (unsigned int)n_chunks * (unsigned int)NW;
+                blk_ready = false;
+                need_blk = true;
+            }
+            // LDS write complete, then the round barrier; no vector-memory wait
+            // (loads of the units in flight stay in flight across it)
+            __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
+            asm volatile("s_barrier" ::: "memory");
+            base = (unsigned int)__builtin_amdgcn_readfirstlane((int)s_blk[round & 3]);
+        }
+        ++round;
+        if ((int64_t)base >= n_pages) blocks_done = true;
+        Claim c;
+        c.j = (int64_t)base + wave;
+        c.raw = c.j < n_pages ? tab[c.j] : make_uint2(0u, 0u);
+        return c;
+    };
+    Claim ahead = take_page();                              // round 0
+    const unsigned int pre0 = needs_blk() ? issue_blk() : 0u;   // round 1's block
+    __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0): query, first table entries, claim
     // pre-RoPE keys: w_i = theta_i / 2 pi = base^(-2i/d) / 2 pi as wh + wl
     // (fp64 on the way), i < d/2, shared by the workgroup
     const float *rw = nullptr;
@@ -756,63 +818,10 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
         __syncthreads();
         rw = s_rw;
     }
-    int round = 0;
-    bool blocks_done = false;
-    // Wave 0's block claim is issued at the top of a loop iteration and read
-    // at the bottom of the same iteration (the vector memory counter is in
-    // order: read later, its wait would also cover the loads issued after
-    // it); the value is held until take_page publishes it. A claim is taken
-    // synchronously only where none is held: the first two rounds and the
-    // last ones, when a wave's page is past the end.
-    unsigned int blk_next = 0u;
-    bool blk_ready = false, need_blk = false;   // wave 0 only
-    auto sync_claim = [&]() -> unsigned int {
-        unsigned int k = 0u;
-        if (lane == 0) k = __hip_atomic_fetch_add(pp.claim(head), (unsigned int)NW, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        return (unsigned int)__builtin_amdgcn_readfirstlane((int)k);
-    };
-    auto needs_blk = [&]() -> bool { return wave == 0 && need_blk; };
-    auto issue_blk = [&]() -> unsigned int {
-        unsigned int k = 0u;
-        if (lane == 0) k = __hip_atomic_fetch_add(pp.claim(head), (unsigned int)NW, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        return k;
-    };
-    auto take_blk = [&](unsigned int k) {
-        asm volatile("" : "+v"(k));
-        blk_next = (unsigned int)__builtin_amdgcn_readfirstlane((int)k);
-        blk_ready = true;
-        need_blk = false;
-    };
-    if (wave == 0) {
-        const unsigned int v = sync_claim();
-        if (lane == 0) s_blk[0] = v;
-    }
-    auto take_page = [&]() -> Claim {
-        if (wave == 0) {
-            if (round > 0) {
-                const unsigned int v = blk_ready ? blk_next : sync_claim();
-                if (lane == 0) s_blk[round & 3] = v;
-                blk_ready = false;
-            }
-            need_blk = true;
-        }
-        // LDS write complete, then the round barrier; no vector-memory wait
-        // (loads of the units in flight stay in flight across it)
-        __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0)
-        asm volatile("s_barrier" ::: "memory");
-        const unsigned int base = (unsigned int)__builtin_amdgcn_readfirstlane((int)s_blk[round & 3]);
-        ++round;
-        if ((int64_t)base >= n_pages) blocks_done = true;
-        Claim c;
-        c.j = (int64_t)base + wave;
-        c.raw = c.j < n_pages ? tab[c.j] : make_uint2(0u, 0u);
-        return c;
-    };
     Unit pending;                 // second and later units of a dense page
     pending.e.kind = PKV_EMPTY;
     pending.j = 0;
     pending.half = 0;
-    Claim ahead = take_page();
     // pre: wave 0's block claim issued at the top of this iteration (needs_blk held)
     auto next_unit = [&](unsigned int pre) -> Unit {
         if (needs_blk()) take_blk(pre);
@@ -870,7 +879,7 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
     cur.e.kind = PKV_EMPTY;
     cur.j = 0;
     cur.half = 0;
-    Unit nxt = next_unit(needs_blk() ? issue_blk() : 0u);
+    Unit nxt = next_unit(pre0);
     while (cur.e.kind != PKV_EMPTY || nxt.e.kind != PKV_EMPTY) {
         const unsigned int pre = needs_blk() ? issue_blk() : 0u;
         const PageRes nres = unit_res<D, P, ROPE>(factor, g.factor_slot_bytes, dense, g.dense_slot_bytes, nxt);
