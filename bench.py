@@ -34,7 +34,8 @@ if ROOT not in sys.path:
 
 HBM_PEAK_GBPS = 8000.0
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_2608_23843_amd", "csrc", f)
-                  for f in ("attention.inl", "attention_mfma.inl", "attention_q4.inl", "attention_launch.inl")]
+                  for f in ("attention.inl", "attention_mfma.inl", "attention_q4.inl", "attention_launch.inl",
+                            "global_svd.inl")]
 
 
 def log(msg: str) -> None:
@@ -88,6 +89,8 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0,
                     help="CPU-baseline budget for the oracle (0 disables)")
     ap.add_argument("--workers", type=int, default=16, help="host threads for input generation")
+    ap.add_argument("--no-calibration", action="store_true",
+                    help="skip the HBM read/copy bandwidth sweep (for short profiling runs)")
     ap.add_argument("--compare", action="store_true",
                     help="Global SVD workloads: also compare its accuracy with PuzzleKV's at the same budget")
     return ap.parse_args()
@@ -558,7 +561,8 @@ def run_global(args, wl):
     }
     del cache, gs, ws
     torch.cuda.empty_cache()
-    result["hbm_calibration"] = hbm_calibration(achieved)
+    if not args.no_calibration:
+        result["hbm_calibration"] = hbm_calibration(achieved)
     if args.cpu_seconds > 0:
         log("CPU baseline (oracle), budget %.0f s" % args.cpu_seconds)
         result["cpu_baseline"] = global_cpu_baseline(wl, args.seed, T, r, args.cpu_seconds, layers)
@@ -815,7 +819,8 @@ def main():
     }
     if comp_decode:
         result["compress_during_decode"] = comp_decode
-    result["hbm_calibration"] = hbm_calibration(achieved)
+    if not args.no_calibration:
+        result["hbm_calibration"] = hbm_calibration(achieved)
     if args.cpu_seconds > 0:
         log("CPU baseline (oracle), budget %.0f s" % args.cpu_seconds)
         q0 = synth.queries(wl, args.seed, 0)

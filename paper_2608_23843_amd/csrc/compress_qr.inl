@@ -625,12 +625,18 @@ void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor, Comp
         for (int k = 2 * n; k - 2 * n < d; k += 64) {
             cq_f32x16 ae = {}, ao = {};
             const bool kin = k < d;
+            // an offset the compiler cannot see is zero: the L operands are
+            // rebuilt from LDS in every block rather than hoisted out of the
+            // loop and held (32 more registers, spilled to scratch memory)
+            int z;
+            asm volatile("v_mov_b32 %0, 0" : "=v"(z));
+            const float *sLz = sL + z;
 #pragma unroll
             for (int s = 0; s < 4; ++s) {
                 uint32_t hw[4], lw[4];
 #pragma unroll
                 for (int i = 0; i < 4; ++i)
-                    cq_split2(sL[(16 * s + 8 * h + 2 * i) * 32 + n], sL[(16 * s + 8 * h + 2 * i + 1) * 32 + n], hw[i], lw[i]);
+                    cq_split2(sLz[(16 * s + 8 * h + 2 * i) * 32 + n], sLz[(16 * s + 8 * h + 2 * i + 1) * 32 + n], hw[i], lw[i]);
                 const cq_bf16x8 ahi = __builtin_bit_cast(cq_bf16x8, make_uint4(hw[0], hw[1], hw[2], hw[3]));
                 const cq_bf16x8 alo = __builtin_bit_cast(cq_bf16x8, make_uint4(lw[0], lw[1], lw[2], lw[3]));
                 cq_bf16x8 be = {}, bo = {};
