@@ -826,8 +826,9 @@ def main():
         q0 = synth.queries(wl, args.seed, 0)
         result["cpu_baseline"] = cpu_baseline(wl, args.seed, T, K_dense, V_dense, q0, args.cpu_seconds,
                                               layers, ranks_np, ranks_v_np)
-        result["cpu_baseline"].update(cpu_extras(wl, args.seed, T, K_dense, V_dense, q0, comp_X, req_np,
-                                                 req_v_np, comp_refs))
+        # the ranks the cache holds (requested, or chosen by the decomposition)
+        result["cpu_baseline"].update(cpu_extras(wl, args.seed, T, K_dense, V_dense, q0, comp_X, ranks_np,
+                                                 ranks_v_np, comp_refs))
     print(json.dumps(result), flush=True)
 
 
