@@ -334,9 +334,8 @@ __global__ __launch_bounds__(256) void k_global_project(Geo g, GlobalGeo gg, con
 //   dense pages (sink, window) of the chunk: S^T = K Q^T, O^T += V^T E^T;
 //   at the end O^T += B_V^T Y^T (M = dim, K = rank).
 // Ranks at or past r8 read as zero through buffer range checks, which zeroes
-// the matching rows of Z and Y; the A_K columns a lane reads past r8 (the
-// next row's values, or zero past the region's last row) multiply those
-// zeros. Waves merge in LDS; workgroups
+// the matching rows of Z and Y; the A_K rank blocks at or past r8 are not
+// read (they would hold the next row's values). Waves merge in LDS; workgroups
 // publish partials merged by Eq. (5) as in the page kernels.
 template <int KS>
 struct GWave {
@@ -389,8 +388,10 @@ __device__ inline void g_issue_unit(GUnitOps<KS> &f, __amdgpu_buffer_rsrc_t rak,
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt) {
         const uint32_t off = 2u * ((uint32_t)(u0 + token_row<32>(tt, n)) * (uint32_t)r8 + 8u * q);
+        // rank blocks at or past r8 read nothing: an offset past the
+        // resource returns zeros without a memory access
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) f.ak[tt][ks] = bld8(rak, off + 64u * ks, 0u);
+        for (int ks = 0; ks < KS; ++ks) f.ak[tt][ks] = bld8(rak, 32 * ks + 8 * q < r8 ? off + 64u * ks : kOOB, 0u);
     }
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks)

@@ -6,12 +6,12 @@ As in bench.py, the seeded generator draws the prompt K/V, the GPU
 decomposition builds the cache (per-page ranks drawn from {16, 24, 32}), and
 one attention call covers the whole batch. Checked on what the oracle can
 compute one head at a time:
-* attention: for every (sequence, KV head) of the 128K bf16 and INT4 layers,
-  the paper-default layer and the Llama-3-8B layer, and sampled ones of the
-  other variants, the oracle attends over that head's exported pages (dense
-  pages as stored, factor pages as the GPU stored them -- for INT4 the
-  dequantized balanced factors) with the same queries; bar max-abs <= 1e-2,
-  normwise mean-relative <= 1e-3;
+* attention: for every (sequence, KV head) of the 128K bf16, INT4, adaptive
+  and pre-RoPE layers, the paper-default layer and the Llama-3-8B layer, the
+  oracle attends over that head's exported pages (dense pages as stored,
+  factor pages as the GPU stored them -- for INT4 the dequantized balanced
+  factors) with the same queries; bar max-abs <= 1e-2, normwise
+  mean-relative <= 1e-3;
 * decomposition: sampled factor pages against the oracle's SVD of the stored
   page (sign-invariant checks, as in test_gpu_compress);
 * the page table: every entry's kind and ranks against the oracle's plan and
@@ -59,8 +59,11 @@ def _head_pages(cache, wl, b, h):
     return cache.export_pages(0, [b] * n, [h] * n, list(range(n))).cpu().numpy().astype(np.float64)
 
 
-def _run(name, heads, n_pages_checked):
+def _run(name, heads, n_pages_checked, deep=None):
+    """Attention of every head in `heads`; the chosen ranks (adaptive caches)
+    and sampled decompositions of the heads in `deep` (default: all of them)."""
     import torch
+    deep = set(heads if deep is None else deep)
     wl, cache, K, V, ranks, ranks_v = _build(name)
     B, Hkv, d, P, T = wl.batch, wl.kv_heads, wl.head_dim, wl.page, wl.tokens
     g, R = wl.group, max(wl.ranks + wl.ranks_v)
@@ -113,6 +116,8 @@ def _run(name, heads, n_pages_checked):
         assert ma <= MAX_ABS and mr <= MEAN_REL, (b, h, ma, mr)
         worst = [max(worst[0], ma), max(worst[1], mr)]
         assert np.abs(lse[b, h * g:(h + 1) * g] - rl).max() <= 1e-3
+        if (b, h) not in deep:
+            continue
         if wl.rank_error > 0:     # every factor page of this head: the chosen ranks
             for j in np.flatnonzero(fac):
                 for X, rr in ((K[b, h, j * P:(j + 1) * P], rk[b, h, j]), (V[b, h, j * P:(j + 1) * P], rv[b, h, j])):
@@ -141,18 +146,20 @@ def test_fullsize_qwen32b_128k_bf16():
 
 def test_fullsize_qwen32b_128k_adaptive_ranks():
     """The 128K layer with every page's ranks chosen by the decomposition for
-    relative Frobenius error 0.2 (cap 32): the chosen ranks of every factor
-    page of three heads against the oracle's singular values, attention and
-    sampled decompositions at those ranks."""
-    checked = _run("qwen32b_128k_adaptive", [(0, 0), (2, 3), (3, 7)], 4)
+    relative Frobenius error 0.2 (cap 32): attention of every (sequence, KV
+    head); the chosen ranks of every factor page of three heads against the
+    oracle's singular values, and sampled decompositions at those ranks."""
+    heads = [(b, h) for b in range(4) for h in range(8)]
+    checked = _run("qwen32b_128k_adaptive", heads, 4, deep=[(0, 0), (2, 3), (3, 7)])
     assert checked == 3 * 4 * 2
 
 
 def test_fullsize_qwen32b_128k_pre_rope():
     """The 128K layer with keys cached before RoPE (rotated at access, base
-    1e6): attention of three heads against the oracle's fp64 rotation, and
-    sampled decompositions of the pre-RoPE pages."""
-    checked = _run("qwen32b_128k_prerope", [(0, 0), (1, 6), (3, 2)], 4)
+    1e6): attention of every (sequence, KV head) against the oracle's fp64
+    rotation, and sampled decompositions of the pre-RoPE pages of three."""
+    heads = [(b, h) for b in range(4) for h in range(8)]
+    checked = _run("qwen32b_128k_prerope", heads, 4, deep=[(0, 0), (1, 6), (3, 2)])
     assert checked == 3 * 4 * 2
 
 
