@@ -322,8 +322,8 @@ __global__ __launch_bounds__(256) void k_global_project(Geo g, GlobalGeo gg, con
 // ---- decode attention over the global factors ------------------------------------
 //
 // Grid (chunk, head), eight waves per workgroup. The compressible region is
-// cut into 32-token units; chunk c takes a contiguous run of units and its
-// waves take every eighth one. Per wave:
+// cut into 32-token units; chunk c takes a contiguous run of an even number
+// of units and its waves take every eighth pair. Per wave:
 //   Z^T = B_K Q^T once (M = rank, K = d), as hi/lo bf16 B operands over KS
 //       32-rank steps (rank tile (ks, rt) row m -> rank 32 ks + rank_row(rt, m),
 //       so a lane's two tiles of a step hold ranks 32 ks + 8q .. +7);
@@ -483,7 +483,9 @@ __global__ __launch_bounds__(64 * kGAttnWaves, 1) void k_attn_global(Geo g, Glob
     int64_t t0, t1;
     global_range(g, T, t0, t1);
     const int64_t n_units = (t1 - t0) / 32;
-    const int64_t upc = ceil_div(n_units, n_chunks);
+    // chunks of an even number of units: a wave takes units in pairs (see
+    // below), and a pair is one 128-byte line of every A_V^T row
+    const int64_t upc = (ceil_div(n_units, n_chunks) + 1) & ~(int64_t)1;
     const int64_t ub = (int64_t)chunk * upc, ue = min<int64_t>(n_units, ub + upc);
 
     bf16x8 qb[4];
@@ -529,18 +531,23 @@ __global__ __launch_bounds__(64 * kGAttnWaves, 1) void k_attn_global(Geo g, Glob
             split_tiles(z[0], z[1], zh[ks], zl[ks]);
         }
         // the wave's units, each unit's operands loaded one step ahead (at
-        // ranks above 96 the second operand set would not fit the registers)
+        // ranks above 96 the second operand set would not fit the registers).
+        // Wave w takes the pairs of units (2 (w + NW i), +1): the two 64-byte
+        // halves of an A_V^T row's 128-byte line are then read by one wave a
+        // unit apart, rather than by two waves that drift apart and can each
+        // fetch the line from HBM.
+        auto unit_of = [&](int k) -> int64_t { return ub + 2 * (wave + (int64_t)NW * (k >> 1)) + (k & 1); };
         constexpr bool kAhead = KS <= 3;
         GUnitOps<KS> cur, nxt;
-        int64_t u = ub + wave;
-        if (kAhead && u < ue) g_issue_unit<KS>(cur, rak, ravt, u * 32, gg.r8, gg.max_tokens, n, q4);
-        for (; u < ue; u += NW) {
+        if (kAhead && unit_of(0) < ue) g_issue_unit<KS>(cur, rak, ravt, unit_of(0) * 32, gg.r8, gg.max_tokens, n, q4);
+        for (int k = 0; unit_of(k) < ue; ++k) {
             if (kAhead) {
-                if (u + NW < ue) g_issue_unit<KS>(nxt, rak, ravt, (u + NW) * 32, gg.r8, gg.max_tokens, n, q4);
+                const int64_t un = unit_of(k + 1);
+                if (un < ue) g_issue_unit<KS>(nxt, rak, ravt, un * 32, gg.r8, gg.max_tokens, n, q4);
                 g_unit<KS>(w, cur, zh, zl, q4, c2);
                 cur = nxt;
             } else {
-                g_issue_unit<KS>(cur, rak, ravt, u * 32, gg.r8, gg.max_tokens, n, q4);
+                g_issue_unit<KS>(cur, rak, ravt, unit_of(k) * 32, gg.r8, gg.max_tokens, n, q4);
                 g_unit<KS>(w, cur, zh, zl, q4, c2);
             }
         }
