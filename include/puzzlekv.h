@@ -355,11 +355,11 @@ pkv_status pkv_export_int4_pages(const pkv_cache *c, int32_t layer, int32_t n, c
  * KV head) in [n_layers][batch][n_kv_heads] order:
  *   basis: B_K (r8 x d), B_V (r8 x d), B_V^T (d x r8), row-major, entries
  *          past rank r zero
- *   coef:  A_K (m x r8) token-major, then A_V^T (r8 x m) rank-major, with
- *          m = max_tokens rounded up to a multiple of 64 (rows of A_V^T
- *          then start on 128-byte boundaries); row t of A_K (column t of
- *          A_V^T) is token t0 + t of the region, t0 = ceil(S / P) P;
- *          entries past rank r zero
+ *   coef:  A_K (max_tokens x r8) token-major, then A_V^T as max_tokens / 32
+ *          blocks of r8 x 32, one per 32-token unit, each rank-major (A_V^T
+ *          entry (a, t) at element (t - t mod 32) r8 + 32 a + t mod 32); row
+ *          t of A_K and column t of A_V^T are token t0 + t of the region,
+ *          t0 = ceil(S / P) P; entries past rank r zero
  */
 typedef struct {
     int32_t rank;        /* r: 1 .. 128 */

@@ -29,8 +29,10 @@
 // 8q..8q+7 of each 32-dim chunk over a pair of dim tiles (the rank-tile map
 // read as a dim map), which is the A operand layout of S^T = K Q^T. The
 // rotate-half pairs (i, i + d/2) sit in the same lane, so the rotation needs
-// no data movement; the rotated keys enter S^T as a bf16 hi/lo pair. Dense
-// keys are rotated the same way from their bf16 operands.
+// no data movement. Keys are rotated by their offset within the unit (a
+// table shared by every unit) and the query group by the unit's first
+// position, once per unit; both enter S^T as fp16 hi/lo pairs. Dense keys
+// are rotated the same way from their bf16 operands.
 //
 // Factor operands are read with buffer loads, one resource per section of the
 // slot sized to that section: rank rows past the page's rank fall outside it
@@ -216,17 +218,31 @@ __device__ inline PageRes unit_res(const char *factor, int64_t fslot_bytes, cons
     return r;
 }
 
-template <int D, int P, bool ROPE = false>
-__device__ inline void issue_key_loads(KeyOps<D, P> &f, const PageRes &r, const LaneOffs &lo, int n, int q) {
-    if constexpr (ROPE) {
-        // dense K: row rank_row(rt, n), columns 32 s + 8q..8q+7 (row length d);
-        // R_K^T: row 32 s + rank_row(rt, n), columns 8q..8q+7 (row length r4(rk))
+// Pre-RoPE caches: the key chunks of one rotate-half pair (s0, s0 + d/64).
+// Dense K: row rank_row(rt, n), columns 32 s + 8q..8q+7 (row length d);
+// R_K^T: row 32 s + rank_row(rt, n), columns 8q..8q+7 (row length r4(rk)).
+template <int D, int P>
+__device__ inline void issue_key_pair_rope(KeyOps<D, P> &f, const PageRes &r, int n, int q, int s0) {
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt) {
-            const uint32_t vb = 2u * ((uint32_t)rank_row(rt, n) * (uint32_t)r.kst + 8u * q);
+    for (int rt = 0; rt < 2; ++rt) {
+        const uint32_t vb = 2u * ((uint32_t)rank_row(rt, n) * (uint32_t)r.kst + 8u * q);
 #pragma unroll
-            for (int s = 0; s < D / 32; ++s) f.bk[rt][s] = bld8(r.bk, vb, (uint32_t)s * (uint32_t)r.kcs);
+        for (int k = 0; k < 2; ++k) {
+            const int s = s0 + k * (D / 64);
+            f.bk[rt][s] = bld8(r.bk, vb, (uint32_t)s * (uint32_t)r.kcs);
         }
+    }
+}
+
+// first_pair: pre-RoPE caches, the first rotate-half pair whose key chunks
+// are still to be loaded (the earlier ones were issued during phase 1)
+template <int D, int P, bool ROPE = false>
+__device__ inline void issue_key_loads(KeyOps<D, P> &f, const PageRes &r, const LaneOffs &lo, int n, int q,
+                                       int first_pair = 0) {
+    if constexpr (ROPE) {
+#pragma unroll
+        for (int s0 = 0; s0 < D / 64; ++s0)
+            if (s0 >= first_pair) issue_key_pair_rope<D, P>(f, r, n, q, s0);
     } else {
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt)
@@ -348,43 +364,39 @@ __device__ inline void unit_phase1(WaveState<D> &w, const KeyOps<D, P> &f, const
 }
 
 // RoPE angles in revolutions: w_i = theta_i / 2 pi is held in LDS as
-// wh + wl (fp64 on the way). For a unit starting at position t0, each lane
-// computes the fraction of t0 w_i for one frequency (the product split
-// exactly with an fma, so the fraction is right to ~2^-24 at any position
-// below 2^24) into the wave's LDS row f0; the angle of position t0 + tau is
-// then frac(f0_i + tau wh_i), one fma and one fract, and the hardware sine and
-// cosine take revolutions. tau < 64 keeps the fma's rounding below 2^-20
-// revolutions.
+// wh + wl (fp64 on the way). The rotation of position t0 + tau is split as
+// R(t0 + tau) = R(t0) R(tau), and q . R(t0) R(tau) k = (R(-t0) q) . (R(tau) k):
+// the keys of a unit are rotated by their offset tau from the unit's start
+// with cos / sin (tau theta_i) from a table shared by every unit, and the
+// query group is rotated once per unit by -t0 theta_i. Both angles come from
+// the fraction of their product with w_i (split exactly with an fma, right
+// to ~2^-24 revolutions at any position below 2^24), and the hardware sine
+// and cosine take revolutions.
 __device__ inline float rope_frac(float t0, float wh, float wl) {
     const float p = t0 * wh;
     const float e = fmaf(t0, wh, -p);
     return __builtin_amdgcn_fractf(__builtin_amdgcn_fractf(p) + fmaf(t0, wl, e));
 }
 
-// Rotates the pairs (x0[u], x1[u]) of one lane's key row at offset tau from
-// the unit's start: x0[u] is dim 32 s + 8 q + u, x1[u] its partner d/2 above
-// (rw: wh[D/2], f0: the wave's fractions for the unit).
-template <int D>
-__device__ inline void rope_pair(float (&x0)[8], float (&x1)[8], float tau, int s, int q, const float *rw,
-                                 const float *f0) {
+// Rotates the pairs (x0[u], x1[u]) of one lane's key row: x0[u] is dim
+// 32 s + 8 q + u, x1[u] its partner d/2 above; ct / st: cos and sin of
+// tau theta_i for the row's offset tau.
+__device__ inline void rope_pair(float (&x0)[8], float (&x1)[8], int s, int q, const float *ct, const float *st) {
 #pragma unroll
     for (int h = 0; h < 2; ++h) {
         const int i0 = 32 * s + 8 * q + 4 * h;
-        const f32x4 wh = *(const f32x4 *)(rw + i0);
-        const f32x4 fr = *(const f32x4 *)(f0 + i0);
+        const f32x4 c = *(const f32x4 *)(ct + i0);
+        const f32x4 sn = *(const f32x4 *)(st + i0);
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-            const float r = __builtin_amdgcn_fractf(fmaf(tau, wh[v], fr[v]));
-            const float c = __builtin_amdgcn_cosf(r), sn = __builtin_amdgcn_sinf(r);
             const float a = x0[4 * h + v], b = x1[4 * h + v];
-            x0[4 * h + v] = a * c - b * sn;
-            x1[4 * h + v] = fmaf(b, c, a * sn);
+            x0[4 * h + v] = fmaf(a, c[v], -b * sn[v]);
+            x1[4 * h + v] = fmaf(b, c[v], a * sn[v]);
         }
     }
 }
 
-// Rotated keys -> fp16 hi/lo A operands of the score product (K entries 8
-// dims of one chunk).
+// fp32 entries -> fp16 hi/lo operands (8 dims of one chunk).
 __device__ inline void split8_f16(const float (&x)[8], f16x8 &hi, f16x8 &lo) {
     uint32_t hd[4], ld[4];
 #pragma unroll
@@ -393,45 +405,88 @@ __device__ inline void split8_f16(const float (&x)[8], f16x8 &hi, f16x8 &lo) {
     lo = __builtin_bit_cast(f16x8, u32x4{ld[0], ld[1], ld[2], ld[3]});
 }
 
-// Phase 1 of a unit of a pre-RoPE cache. Factor page: per token tile,
-// K^T = R_K^T L_K^T, rotation, S^T = K Q^T; rank entries at or past r4(rk)
-// of the L_K operand are zeroed (the R_K^T operand holds the next row's
-// values there). Dense unit: the K rows are rotated, then S^T = K Q^T. The
-// rotated keys enter the score product as fp16 hi/lo pairs against the query
-// group in fp16 (qh). t0: position of the unit's first token; f0: the wave's
-// LDS row of D/2 floats for the unit's angle fractions.
+// LDS tables of a pre-RoPE cache: w_i as wh + wl (D floats); cos and sin of
+// tau theta_i for tau < P (rows of D/2 + 4 floats, padded against bank
+// conflicts); the query group in fp32 in the lanes' B operand layout
+// ([chunk][lane][8]); per wave, cos | sin of t0 theta_i of its current unit.
 template <int D, int P>
-__device__ inline void unit_phase1_rope(WaveState<D> &w, const KeyOps<D, P> &f, const f16x8 (&qh)[D / 32],
+struct RopeLds {
+    static constexpr int kRow = D / 2 + 4;
+    const float *rw, *ct, *st, *qf;
+    float *r0;
+};
+
+// One rotate-half pair of 32-dim chunks (s0, s0 + d/64) of the query group
+// rotated by -t0 theta_i, as fp16 hi/lo B operands of the score product
+// (about 22 bits): [0] chunk s0, [1] chunk s0 + d/64.
+template <int D, int P>
+__device__ inline void rope_query(const RopeLds<D, P> &L, int s0, int lane, int q, f16x8 (&qh)[2], f16x8 (&ql)[2]) {
+    float a[8], b[8];
+    const float *pa = L.qf + (s0 * 64 + lane) * 8, *pb = L.qf + ((s0 + D / 64) * 64 + lane) * 8;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+        const int i0 = 32 * s0 + 8 * q + 4 * h;
+        const f32x4 xa = *(const f32x4 *)(pa + 4 * h), xb = *(const f32x4 *)(pb + 4 * h);
+        const f32x4 c = *(const f32x4 *)(L.r0 + i0), sn = *(const f32x4 *)(L.r0 + D / 2 + i0);
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            a[4 * h + v] = fmaf(xa[v], c[v], xb[v] * sn[v]);
+            b[4 * h + v] = fmaf(xb[v], c[v], -xa[v] * sn[v]);
+        }
+    }
+    split8_f16(a, qh[0], ql[0]);
+    split8_f16(b, qh[1], ql[1]);
+}
+
+// Phase 1 of a unit of a pre-RoPE cache. Factor page: per token tile,
+// K^T = R_K^T L_K^T, rotation by the token's offset tau, S^T = K Q^T against
+// the query group rotated by -t0 theta_i; rank entries at or past r4(rk) of
+// the L_K operand are zeroed (the R_K^T operand holds the next row's values
+// there). Dense unit: the K rows are rotated, then the same product. Keys and
+// queries enter it as fp16 hi/lo pairs (three products: hi hi, lo hi, hi lo).
+// The loops take one rotate-half pair of 32-dim chunks at a time, outermost,
+// so only that pair of the rotated query is held, and a pair's key chunks are
+// free once it is done: pair_done(s0) is called then (but not after the last
+// pair), for the next unit's loads of those chunks. t0: position of the
+// unit's first token.
+template <int D, int P, typename PairDone>
+__device__ inline void unit_phase1_rope(WaveState<D> &w, const KeyOps<D, P> &f, const RopeLds<D, P> &L,
                                         bool dense, int rows, bf16x8 (&eh)[(P + 31) / 32],
                                         bf16x8 (&el)[(P + 31) / 32], int n, int q, float c2, int64_t t0, int rk4,
-                                        const float *rw, float *f0) {
-    {
-        const int lane = q * 16 + n;
-        if (lane < D / 2) f0[lane] = rope_frac((float)t0, rw[lane], rw[D / 2 + lane]);
-        __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): the wave's row is written before it is read
+                                        PairDone pair_done) {
+    constexpr int R = RopeLds<D, P>::kRow;
+    const int lane = q * 16 + n;
+    if (lane < D / 2) {
+        const float fr = rope_frac((float)t0, L.rw[lane], L.rw[D / 2 + lane]);
+        L.r0[lane] = __builtin_amdgcn_cosf(fr);
+        L.r0[D / 2 + lane] = __builtin_amdgcn_sinf(fr);
     }
+    __builtin_amdgcn_s_waitcnt(0xc07f);   // lgkmcnt(0): the wave's row is written before it is read
     if (dense) {
-        f32x4 z[2];
+        f32x4 z[2] = {zero_f4(), zero_f4()};
 #pragma unroll
-        for (int rt = 0; rt < 2; ++rt) {
-            const float tau = (float)rank_row(rt, n);
-            z[rt] = zero_f4();
+        for (int s0 = 0; s0 < D / 64; ++s0) {
+            f16x8 qh[2], ql[2];
+            rope_query<D, P>(L, s0, lane, q, qh, ql);
 #pragma unroll
-            for (int s0 = 0; s0 < D / 64; ++s0) {
+            for (int rt = 0; rt < 2; ++rt) {
+                const int tau = rank_row(rt, n);
                 float x[2][8];
 #pragma unroll
                 for (int k = 0; k < 2; ++k)
 #pragma unroll
                     for (int u = 0; u < 8; ++u) x[k][u] = (float)f.bk[rt][s0 + k * (D / 64)][u];
-                rope_pair<D>(x[0], x[1], tau, s0, q, rw, f0);
+                rope_pair(x[0], x[1], s0, q, L.ct + tau * R, L.st + tau * R);
 #pragma unroll
                 for (int k = 0; k < 2; ++k) {
                     f16x8 hi, lo;
                     split8_f16(x[k], hi, lo);
-                    z[rt] = mfma_f16(hi, qh[s0 + k * (D / 64)], z[rt]);
-                    z[rt] = mfma_f16(lo, qh[s0 + k * (D / 64)], z[rt]);
+                    z[rt] = mfma_f16(hi, qh[k], z[rt]);
+                    z[rt] = mfma_f16(lo, qh[k], z[rt]);
+                    z[rt] = mfma_f16(hi, ql[k], z[rt]);
                 }
             }
+            if (s0 + 1 < D / 64) pair_done(s0);
         }
         bf16x8 eh1[1], el1[1];
         page_softmax<D, 32, true>(w, z, eh1, el1, rows, q, c2);
@@ -440,37 +495,44 @@ __device__ inline void unit_phase1_rope(WaveState<D> &w, const KeyOps<D, P> &f, 
         return;
     }
     const bool m_lo = 8 * q < rk4, m_hi = 8 * q + 4 < rk4;
-    f32x4 st[P / 16];
+    bf16x8 a[P / 16];
 #pragma unroll
     for (int tt = 0; tt < P / 16; ++tt) {
         u32x4 am = __builtin_bit_cast(u32x4, f.ak[tt]);
         if (!m_lo) am[0] = am[1] = 0u;
         if (!m_hi) am[2] = am[3] = 0u;
-        const bf16x8 a = __builtin_bit_cast(bf16x8, am);
-        const float tau = (float)token_row<P>(tt, n);
-        st[tt] = zero_f4();
-        // one rotate-half pair of 32-dim chunks (s, s + d/64) at a time
+        a[tt] = __builtin_bit_cast(bf16x8, am);
+    }
+    f32x4 st[P / 16];
 #pragma unroll
-        for (int s0 = 0; s0 < D / 64; ++s0) {
+    for (int tt = 0; tt < P / 16; ++tt) st[tt] = zero_f4();
+#pragma unroll
+    for (int s0 = 0; s0 < D / 64; ++s0) {
+        f16x8 qh[2], ql[2];
+        rope_query<D, P>(L, s0, lane, q, qh, ql);
+#pragma unroll
+        for (int tt = 0; tt < P / 16; ++tt) {
+            const int tau = token_row<P>(tt, n);
             float x[2][8];
 #pragma unroll
             for (int k = 0; k < 2; ++k)
 #pragma unroll
                 for (int hp = 0; hp < 2; ++hp) {
-                    const f32x4 kt = mfma_bf16(f.bk[hp][s0 + k * (D / 64)], a, zero_f4());
+                    const f32x4 kt = mfma_bf16(f.bk[hp][s0 + k * (D / 64)], a[tt], zero_f4());
 #pragma unroll
                     for (int v = 0; v < 4; ++v) x[k][4 * hp + v] = kt[v];
                 }
-            rope_pair<D>(x[0], x[1], tau, s0, q, rw, f0);
+            rope_pair(x[0], x[1], s0, q, L.ct + tau * R, L.st + tau * R);
 #pragma unroll
             for (int k = 0; k < 2; ++k) {
                 f16x8 hi, lo;
                 split8_f16(x[k], hi, lo);
-                const f16x8 qv = qh[s0 + k * (D / 64)];
-                st[tt] = mfma_f16(hi, qv, st[tt]);
-                st[tt] = mfma_f16(lo, qv, st[tt]);
+                st[tt] = mfma_f16(hi, qh[k], st[tt]);
+                st[tt] = mfma_f16(lo, qh[k], st[tt]);
+                st[tt] = mfma_f16(hi, ql[k], st[tt]);
             }
         }
+        if (s0 + 1 < D / 64) pair_done(s0);
     }
     page_softmax<D, P, false>(w, st, eh, el, P, q, c2);
 }
@@ -543,7 +605,7 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
                                                                   const char *__restrict__ dense,
                                                                   const char *__restrict__ factor,
                                                                   const uint16_t *__restrict__ q, SeqArgs seq,
-                                                                  int /*ppc*/, int n_chunks, Partials pp, float *out,
+                                                                  int wave_claims_arg, int n_chunks, Partials pp, float *out,
                                                                   float *lse) {
     constexpr int KD = D / 32, DT = D / 16, KS = (P + 31) / 32;
     constexpr int NW = attn_waves<Q4>();
@@ -736,17 +798,28 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
     // it); the value is held until take_page publishes it. A claim is taken
     // synchronously only where none is held: the last rounds, when a wave's
     // page is past the end.
+    //
+    // With wave_claims (set by the host for pre-RoPE caches, and for streams
+    // of few pages per wave) each wave instead claims one page at a time after
+    // the same static round 0, with the same issue-ahead scheme and no
+    // barrier (a claim k is page n_chunks NW + k). The round barrier keeps the
+    // waves in step: the two waves of a SIMD then run the same phase of their
+    // pages at once, which costs compute-bound pages (pre-RoPE), and a round
+    // holding a two-unit dense page lasts twice as long for all eight waves,
+    // which costs a stream of few rounds.
+    const bool wave_claims = ROPE || wave_claims_arg != 0;
+    const unsigned int claim_step = wave_claims ? 1u : (unsigned int)NW;
     unsigned int blk_next = 0u;
-    bool blk_ready = false, need_blk = false;   // wave 0 only
+    bool blk_ready = false, need_blk = false;   // wave 0 only, unless wave_claims
     auto sync_claim = [&]() -> unsigned int {
         unsigned int k = 0u;
-        if (lane == 0) k = __hip_atomic_fetch_add(pp.claim(head), (unsigned int)NW, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (lane == 0) k = __hip_atomic_fetch_add(pp.claim(head), claim_step, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         return (unsigned int)__builtin_amdgcn_readfirstlane((int)k);
     };
-    auto needs_blk = [&]() -> bool { return wave == 0 && need_blk; };
+    auto needs_blk = [&]() -> bool { return (wave_claims || wave == 0) && need_blk; };
     auto issue_blk = [&]() -> unsigned int {
         unsigned int k = 0u;
-        if (lane == 0) k = __hip_atomic_fetch_add(pp.claim(head), (unsigned int)NW, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (lane == 0) k = __hip_atomic_fetch_add(pp.claim(head), claim_step, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         return k;
     };
     auto take_blk = [&](unsigned int k) {
@@ -765,7 +838,17 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
         unsigned int base;
         if (round == 0) {
             base = (unsigned int)chunk * (unsigned int)NW;
-            if (wave == 0) need_blk = true;
+            if (wave_claims || wave == 0) need_blk = true;
+        } else if (wave_claims) {
+            const unsigned int v = blk_ready ? blk_next : sync_claim();
+            blk_ready = false;
+            need_blk = true;
+            ++round;
+            Claim c;
+            c.j = (int64_t)v + (int64_t)n_chunks * NW;
+            if (c.j >= n_pages) blocks_done = true;
+            c.raw = c.j < n_pages ? tab[c.j] : make_uint2(0u, 0u);
+            return c;
         } else {
             if (wave == 0) {
                 const unsigned int v = blk_ready ? blk_next : sync_claim();
@@ -790,23 +873,15 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
     const unsigned int pre0 = needs_blk() ? issue_blk() : 0u;   // round 1's block
     __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0): query, first table entries, claim
     // pre-RoPE keys: w_i = theta_i / 2 pi = base^(-2i/d) / 2 pi as wh + wl
-    // (fp64 on the way), i < d/2, shared by the workgroup
-    const float *rw = nullptr;
-    // pre-RoPE keys: the query group as fp16 B operands of the score product
-    // (exact from bf16 unless below fp16's normal range, where the absolute
-    // error stays under 2^-25)
-    f16x8 qh[KD];
+    // (fp64 on the way), i < d/2; the table of cos / sin (tau theta_i) for
+    // tau < P; the query group in fp32. Shared by the workgroup.
+    RopeLds<D, P> rl{};
     if constexpr (ROPE) {
-#pragma unroll
-        for (int s = 0; s < KD; ++s)
-#pragma unroll
-            for (int u = 0; u < 8; ++u) qh[s][u] = (_Float16)(float)qb[s][u];
-    }
-    float *f0 = nullptr;
-    if constexpr (ROPE) {
+        constexpr int R = RopeLds<D, P>::kRow;
         __shared__ float s_rw[D];
-        __shared__ float s_f0[NW][D / 2];
-        f0 = s_f0[wave];
+        __shared__ float s_rt[2][P * R];
+        __shared__ float s_qf[KD * 64 * 8];
+        __shared__ float s_r0[NW][D];
         if (threadIdx.x < D / 2) {
             const int i = (int)threadIdx.x;
             const double th = exp2(-(2.0 * i / D) * log2((double)g.rope_base));
@@ -815,8 +890,25 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
             s_rw[i] = wh;
             s_rw[D / 2 + i] = (float)(wv - (double)wh);
         }
+        if (wave == 0) {
+#pragma unroll
+            for (int s = 0; s < KD; ++s)
+#pragma unroll
+                for (int u = 0; u < 8; ++u) s_qf[(s * 64 + lane) * 8 + u] = (float)qb[s][u];
+        }
         __syncthreads();
-        rw = s_rw;
+        for (int idx = (int)threadIdx.x; idx < P * (D / 2); idx += 64 * NW) {
+            const int tau = idx / (D / 2), i = idx % (D / 2);
+            const float fr = rope_frac((float)tau, s_rw[i], s_rw[D / 2 + i]);
+            s_rt[0][tau * R + i] = __builtin_amdgcn_cosf(fr);
+            s_rt[1][tau * R + i] = __builtin_amdgcn_sinf(fr);
+        }
+        __syncthreads();
+        rl.rw = s_rw;
+        rl.ct = s_rt[0];
+        rl.st = s_rt[1];
+        rl.qf = s_qf;
+        rl.r0 = s_r0[wave];
     }
     Unit pending;                 // second and later units of a dense page
     pending.e.kind = PKV_EMPTY;
@@ -888,12 +980,14 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
         const bool live = cur.e.kind != PKV_EMPTY, dns = cur.e.kind == PKV_DENSE;
         if (live) {
             if constexpr (ROPE)
-                unit_phase1_rope<D, P>(w, ko, qh, dns, rows, eh, el, n, q4, c2,
-                                       cur.j * P + (int64_t)UT * cur.half, r4(cur.e.rank_k), rw, f0);
+                unit_phase1_rope<D, P>(w, ko, rl, dns, rows, eh, el, n, q4, c2,
+                                       cur.j * P + (int64_t)UT * cur.half, r4(cur.e.rank_k),
+                                       [&](int s0) { issue_key_pair_rope<D, P>(ko, nres, n, q4, s0); });
             else
                 unit_phase1<D, P>(w, ko, qb, dns, rows, eh, el, q4, c2);
         }
-        issue_key_loads<D, P, ROPE>(ko, nres, lo, n, q4);
+        // pre-RoPE: the pairs but the last were issued during phase 1
+        issue_key_loads<D, P, ROPE>(ko, nres, lo, n, q4, ROPE && live ? D / 64 - 1 : 0);
         if (live) unit_phase2<D, P>(w, vo, dns, rows, eh, el, q4);
         issue_value_loads<D, P>(vo, nres, lo, n, q4);
         cur = nxt;
@@ -956,10 +1050,10 @@ hipError_t launch_attn_mfma(const LaunchCtx &L, const AttnPlan &plan, const uint
     dim3 grid(plan.n_chunks, g.B * g.Hkv);
 #define PKV_LAUNCH_MFMA(DD, PP)                                                                         \
     hipLaunchKernelGGL((k_attn_mfma<DD, PP, false>), grid, dim3(64 * kMfmaWaves), 0, L.stream, g, p.table,   \
-                       p.dense, p.factor, q, seq, plan.pages_per_chunk, plan.n_chunks, pp, out, lse)
+                       p.dense, p.factor, q, seq, plan.wave_claims, plan.n_chunks, pp, out, lse)
 #define PKV_LAUNCH_MFMA_ROPE(DD, PP)                                                                    \
     hipLaunchKernelGGL((k_attn_mfma<DD, PP, false, true>), grid, dim3(64 * kMfmaWaves), 0, L.stream, g,      \
-                       p.table, p.dense, p.factor, q, seq, plan.pages_per_chunk, plan.n_chunks, pp, out, lse)
+                       p.table, p.dense, p.factor, q, seq, plan.wave_claims, plan.n_chunks, pp, out, lse)
     if (g.key_t) {   // pre-RoPE keys (validated on the host: d = 64/128, P = 32/64)
         if (g.d == 128) {
             if (g.P == 64) PKV_LAUNCH_MFMA_ROPE(128, 64);
@@ -970,7 +1064,7 @@ hipError_t launch_attn_mfma(const LaunchCtx &L, const AttnPlan &plan, const uint
         }
     } else if (g.factor_dtype == PKV_INT4) {
         hipLaunchKernelGGL((k_attn_mfma<128, 64, true>), grid, dim3(64 * kMfmaWavesQ4), 0, L.stream, g, p.table,
-                           p.dense, p.factor, q, seq, plan.pages_per_chunk, plan.n_chunks, pp, out, lse);
+                           p.dense, p.factor, q, seq, plan.wave_claims, plan.n_chunks, pp, out, lse);
     } else if (g.d == 128) {
         if (g.P == 64) PKV_LAUNCH_MFMA(128, 64);
         else if (g.P == 32) PKV_LAUNCH_MFMA(128, 32);

@@ -264,7 +264,9 @@ __global__ __launch_bounds__(kGEigThreads) void k_global_eigen(Geo g, GlobalGeo 
 // 16x16x32 MFMA. Keys: C = B X^T (rank x token), lane (token, q) ends with
 // ranks 4q .. 4q+3 of each rank tile, stored to the token-major A_K. Values:
 // C = X B^T (token x rank), lane (rank, q) ends with tokens 4q .. 4q+3,
-// stored to the rank-major A_V^T.
+// stored to A_V^T, which is rank-major inside each 32-token unit: unit u's
+// block of r8 x 32 values is contiguous, so the attention reads a unit's
+// A_V^T as whole 128-byte lines, as it reads the unit's A_K rows.
 template <int RT>
 __global__ __launch_bounds__(256) void k_global_project(Geo g, GlobalGeo gg, const uint16_t *k, const uint16_t *v,
                                                         int64_t src_tokens, SeqArgs seq, const char *basis_layer,
@@ -312,7 +314,8 @@ __global__ __launch_bounds__(256) void k_global_project(Geo g, GlobalGeo gg, con
                 if (16 * rt + i < gg.r8) {
                     uint32_t lo = (uint32_t)f32_to_bf16(c[0]) | ((uint32_t)f32_to_bf16(c[1]) << 16);
                     uint32_t hi = (uint32_t)f32_to_bf16(c[2]) | ((uint32_t)f32_to_bf16(c[3]) << 16);
-                    *(uint2 *)(Avt + (int64_t)(16 * rt + i) * gg.max_tokens + tb + 4 * q) = make_uint2(lo, hi);
+                    *(uint2 *)(Avt + (tb & ~(int64_t)31) * gg.r8 + (16 * rt + i) * 32 + (tb & 31) + 4 * q) =
+                        make_uint2(lo, hi);
                 }
             }
         }
@@ -322,8 +325,8 @@ __global__ __launch_bounds__(256) void k_global_project(Geo g, GlobalGeo gg, con
 // ---- decode attention over the global factors ------------------------------------
 //
 // Grid (chunk, head), eight waves per workgroup. The compressible region is
-// cut into 32-token units; chunk c takes a contiguous run of an even number
-// of units and its waves take every eighth pair. Per wave:
+// cut into 32-token units; chunk c takes a contiguous run of units and its
+// waves take every eighth one. Per wave:
 //   Z^T = B_K Q^T once (M = rank, K = d), as hi/lo bf16 B operands over KS
 //       32-rank steps (rank tile (ks, rt) row m -> rank 32 ks + rank_row(rt, m),
 //       so a lane's two tiles of a step hold ranks 32 ks + 8q .. +7);
@@ -334,8 +337,9 @@ __global__ __launch_bounds__(256) void k_global_project(Geo g, GlobalGeo gg, con
 //   dense pages (sink, window) of the chunk: S^T = K Q^T, O^T += V^T E^T;
 //   at the end O^T += B_V^T Y^T (M = dim, K = rank).
 // Ranks at or past r8 read as zero through buffer range checks, which zeroes
-// the matching rows of Z and Y; the A_K rank blocks at or past r8 are not
-// read (they would hold the next row's values). Waves merge in LDS; workgroups
+// the matching rows of Z and Y; the A_K rank blocks and the A_V^T rank rows
+// at or past r8 are not read (they would hold the next token's or the next
+// unit's values). Waves merge in LDS; workgroups
 // publish partials merged by Eq. (5) as in the page kernels.
 template <int KS>
 struct GWave {
@@ -384,7 +388,7 @@ struct GUnitOps {
 
 template <int KS>
 __device__ inline void g_issue_unit(GUnitOps<KS> &f, __amdgpu_buffer_rsrc_t rak, __amdgpu_buffer_rsrc_t ravt,
-                                    int64_t u0, int r8, int max_tokens, int n, int q) {
+                                    int64_t u0, int r8, int n, int q) {
 #pragma unroll
     for (int tt = 0; tt < 2; ++tt) {
         const uint32_t off = 2u * ((uint32_t)(u0 + token_row<32>(tt, n)) * (uint32_t)r8 + 8u * q);
@@ -398,7 +402,7 @@ __device__ inline void g_issue_unit(GUnitOps<KS> &f, __amdgpu_buffer_rsrc_t rak,
 #pragma unroll
         for (int rt = 0; rt < 2; ++rt) {
             const uint32_t rank = 32u * ks + (uint32_t)rank_row(rt, n);
-            f.av[ks][rt] = bld8(ravt, 2u * (rank * (uint32_t)max_tokens + (uint32_t)u0 + 8u * q), 0u);
+            f.av[ks][rt] = bld8(ravt, rank < (uint32_t)r8 ? 2u * ((uint32_t)u0 * (uint32_t)r8 + 32u * rank + 8u * q) : kOOB, 0u);
         }
 }
 
@@ -483,9 +487,7 @@ __global__ __launch_bounds__(64 * kGAttnWaves, 1) void k_attn_global(Geo g, Glob
     int64_t t0, t1;
     global_range(g, T, t0, t1);
     const int64_t n_units = (t1 - t0) / 32;
-    // chunks of an even number of units: a wave takes units in pairs (see
-    // below), and a pair is one 128-byte line of every A_V^T row
-    const int64_t upc = (ceil_div(n_units, n_chunks) + 1) & ~(int64_t)1;
+    const int64_t upc = ceil_div(n_units, n_chunks);
     const int64_t ub = (int64_t)chunk * upc, ue = min<int64_t>(n_units, ub + upc);
 
     bf16x8 qb[4];
@@ -531,23 +533,18 @@ __global__ __launch_bounds__(64 * kGAttnWaves, 1) void k_attn_global(Geo g, Glob
             split_tiles(z[0], z[1], zh[ks], zl[ks]);
         }
         // the wave's units, each unit's operands loaded one step ahead (at
-        // ranks above 96 the second operand set would not fit the registers).
-        // Wave w takes the pairs of units (2 (w + NW i), +1): the two 64-byte
-        // halves of an A_V^T row's 128-byte line are then read by one wave a
-        // unit apart, rather than by two waves that drift apart and can each
-        // fetch the line from HBM.
-        auto unit_of = [&](int k) -> int64_t { return ub + 2 * (wave + (int64_t)NW * (k >> 1)) + (k & 1); };
+        // ranks above 96 the second operand set would not fit the registers)
         constexpr bool kAhead = KS <= 3;
         GUnitOps<KS> cur, nxt;
-        if (kAhead && unit_of(0) < ue) g_issue_unit<KS>(cur, rak, ravt, unit_of(0) * 32, gg.r8, gg.max_tokens, n, q4);
-        for (int k = 0; unit_of(k) < ue; ++k) {
+        int64_t u = ub + wave;
+        if (kAhead && u < ue) g_issue_unit<KS>(cur, rak, ravt, u * 32, gg.r8, n, q4);
+        for (; u < ue; u += NW) {
             if (kAhead) {
-                const int64_t un = unit_of(k + 1);
-                if (un < ue) g_issue_unit<KS>(nxt, rak, ravt, un * 32, gg.r8, gg.max_tokens, n, q4);
+                if (u + NW < ue) g_issue_unit<KS>(nxt, rak, ravt, (u + NW) * 32, gg.r8, n, q4);
                 g_unit<KS>(w, cur, zh, zl, q4, c2);
                 cur = nxt;
             } else {
-                g_issue_unit<KS>(cur, rak, ravt, unit_of(k) * 32, gg.r8, gg.max_tokens, n, q4);
+                g_issue_unit<KS>(cur, rak, ravt, u * 32, gg.r8, n, q4);
                 g_unit<KS>(w, cur, zh, zl, q4, c2);
             }
         }
@@ -722,7 +719,7 @@ __global__ void k_global_export(GlobalGeo gg, const char *basis_head, const char
     for (int64_t e = i0; e < n_rows * gg.r; e += stride) {
         const int64_t t = e / gg.r, a = e % gg.r;
         ak[e] = bf16_to_f32(Ak[t * gg.r8 + a]);
-        av[e] = bf16_to_f32(Avt[a * gg.max_tokens + t]);
+        av[e] = bf16_to_f32(Avt[(t & ~(int64_t)31) * gg.r8 + a * 32 + (t & 31)]);
     }
 }
 

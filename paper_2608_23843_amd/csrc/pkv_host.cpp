@@ -580,7 +580,7 @@ GlobalGeo global_geo(const pkv_global *gl) {
     GlobalGeo gg;
     gg.r = gl->rank;
     gg.r8 = (gl->rank + 7) & ~7;
-    gg.max_tokens = (gl->max_tokens + 63) & ~63;   // the pools' row stride: 128-byte rows of A_V^T
+    gg.max_tokens = gl->max_tokens;
     return gg;
 }
 

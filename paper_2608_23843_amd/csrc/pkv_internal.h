@@ -228,6 +228,7 @@ struct AttnPlan {
     int pages_per_chunk;
     int n_chunks;
     int use_mfma;
+    int wave_claims;   // matrix-core kernel: pages claimed per wave rather than per workgroup round
 };
 AttnPlan attention_plan(const Geo &g, int64_t max_T);
 int64_t attention_workspace_bytes(const Geo &g, int64_t max_T);
