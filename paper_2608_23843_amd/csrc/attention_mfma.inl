@@ -605,7 +605,7 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
                                                                   const char *__restrict__ dense,
                                                                   const char *__restrict__ factor,
                                                                   const uint16_t *__restrict__ q, SeqArgs seq,
-                                                                  int wave_claims_arg, int n_chunks, Partials pp, float *out,
+                                                                  int sched, int n_chunks, Partials pp, float *out,
                                                                   float *lse) {
     constexpr int KD = D / 32, DT = D / 16, KS = (P + 31) / 32;
     constexpr int NW = attn_waves<Q4>();
@@ -799,7 +799,7 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
     // synchronously only where none is held: the last rounds, when a wave's
     // page is past the end.
     //
-    // With wave_claims (set by the host for pre-RoPE caches, and for streams
+    // With wave_claims (kSchedWaveClaims, set by the host for pre-RoPE caches, and for streams
     // of few pages per wave) each wave instead claims one page at a time after
     // the same static round 0, with the same issue-ahead scheme and no
     // barrier (a claim k is page n_chunks NW + k). The round barrier keeps the
@@ -807,7 +807,12 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
     // pages at once, which costs compute-bound pages (pre-RoPE), and a round
     // holding a two-unit dense page lasts twice as long for all eight waves,
     // which costs a stream of few rounds.
-    const bool wave_claims = ROPE || wave_claims_arg != 0;
+    const bool wave_claims = ROPE || (sched & kSchedWaveClaims) != 0;
+    // With kSchedReverse the k-th page handed out is page n_pages - 1 - k:
+    // the window's dense pages (two units each) are taken first, and the last
+    // claims of every head are factor pages (set by the host for long streams).
+    const bool reverse = (sched & kSchedReverse) != 0;
+    auto page_of = [&](int64_t k) -> int64_t { return k >= n_pages ? n_pages : reverse ? n_pages - 1 - k : k; };
     const unsigned int claim_step = wave_claims ? 1u : (unsigned int)NW;
     unsigned int blk_next = 0u;
     bool blk_ready = false, need_blk = false;   // wave 0 only, unless wave_claims
@@ -845,7 +850,7 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
             need_blk = true;
             ++round;
             Claim c;
-            c.j = (int64_t)v + (int64_t)n_chunks * NW;
+            c.j = page_of((int64_t)v + (int64_t)n_chunks * NW);
             if (c.j >= n_pages) blocks_done = true;
             c.raw = c.j < n_pages ? tab[c.j] : make_uint2(0u, 0u);
             return c;
@@ -865,7 +870,7 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
         ++round;
         if ((int64_t)base >= n_pages) blocks_done = true;
         Claim c;
-        c.j = (int64_t)base + wave;
+        c.j = page_of((int64_t)base + wave);
         c.raw = c.j < n_pages ? tab[c.j] : make_uint2(0u, 0u);
         return c;
     };
@@ -1050,10 +1055,10 @@ hipError_t launch_attn_mfma(const LaunchCtx &L, const AttnPlan &plan, const uint
     dim3 grid(plan.n_chunks, g.B * g.Hkv);
 #define PKV_LAUNCH_MFMA(DD, PP)                                                                         \
     hipLaunchKernelGGL((k_attn_mfma<DD, PP, false>), grid, dim3(64 * kMfmaWaves), 0, L.stream, g, p.table,   \
-                       p.dense, p.factor, q, seq, plan.wave_claims, plan.n_chunks, pp, out, lse)
+                       p.dense, p.factor, q, seq, plan.sched, plan.n_chunks, pp, out, lse)
 #define PKV_LAUNCH_MFMA_ROPE(DD, PP)                                                                    \
     hipLaunchKernelGGL((k_attn_mfma<DD, PP, false, true>), grid, dim3(64 * kMfmaWaves), 0, L.stream, g,      \
-                       p.table, p.dense, p.factor, q, seq, plan.wave_claims, plan.n_chunks, pp, out, lse)
+                       p.table, p.dense, p.factor, q, seq, plan.sched, plan.n_chunks, pp, out, lse)
     if (g.key_t) {   // pre-RoPE keys (validated on the host: d = 64/128, P = 32/64)
         if (g.d == 128) {
             if (g.P == 64) PKV_LAUNCH_MFMA_ROPE(128, 64);
@@ -1064,7 +1069,7 @@ hipError_t launch_attn_mfma(const LaunchCtx &L, const AttnPlan &plan, const uint
         }
     } else if (g.factor_dtype == PKV_INT4) {
         hipLaunchKernelGGL((k_attn_mfma<128, 64, true>), grid, dim3(64 * kMfmaWavesQ4), 0, L.stream, g, p.table,
-                           p.dense, p.factor, q, seq, plan.wave_claims, plan.n_chunks, pp, out, lse);
+                           p.dense, p.factor, q, seq, plan.sched, plan.n_chunks, pp, out, lse);
     } else if (g.d == 128) {
         if (g.P == 64) PKV_LAUNCH_MFMA(128, 64);
         else if (g.P == 32) PKV_LAUNCH_MFMA(128, 32);

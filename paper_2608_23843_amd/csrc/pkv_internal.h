@@ -228,8 +228,11 @@ struct AttnPlan {
     int pages_per_chunk;
     int n_chunks;
     int use_mfma;
-    int wave_claims;   // matrix-core kernel: pages claimed per wave rather than per workgroup round
+    int sched;   // matrix-core kernel: kSched* bits
 };
+// Page schedule of the matrix-core kernel: pages claimed per wave rather
+// than per workgroup round; pages handed out last to first.
+constexpr int kSchedWaveClaims = 1, kSchedReverse = 2;
 AttnPlan attention_plan(const Geo &g, int64_t max_T);
 int64_t attention_workspace_bytes(const Geo &g, int64_t max_T);
 // Partial-state bytes the calls without a workspace can use, and the bytes
