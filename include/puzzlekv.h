@@ -246,7 +246,11 @@ pkv_status pkv_append_kv(const pkv_cache *c, int32_t layer, const void *k_new, c
  * the page is left untouched and PKV_DEV_NOT_DENSE (already factorized or
  * empty) or PKV_DEV_NOT_ELIGIBLE (incomplete, or still inside the window) is
  * raised. Duplicate pages in one call are rejected (PKV_E_ARG).
- * Workspace: pkv_workspace_bytes(PKV_OP_COMPRESS, n). */
+ * Workspace: optional. With ws (device) of at least
+ * pkv_workspace_bytes(PKV_OP_COMPRESS, n) bytes, the page list is copied
+ * there (an asynchronous host-to-device copy on s) and all n pages are
+ * factorized in one launch; calls that share a workspace must be ordered
+ * (one stream). With ws NULL or smaller, the pages go in launches of 96. */
 pkv_status pkv_compress_pages(const pkv_cache *c, int32_t layer, int32_t n, const int32_t *b,
                               const int32_t *kv_head, const int32_t *page, const uint8_t *rank_k,
                               const uint8_t *rank_v, void *ws, size_t ws_bytes, pkv_stream s);

@@ -185,13 +185,23 @@ class PuzzleKVCache:
         check(self.lib.pkv_append_kv(ctypes.byref(self.c), layer, k_new.data_ptr(), v_new.data_ptr(),
                                      _np_ptr(p), _stream_handle(self.torch, stream)), "pkv_append_kv")
 
-    def compress_pages(self, layer, b, h, page, rank_k, rank_v, stream=None):
+    def compress_pages(self, layer, b, h, page, rank_k, rank_v, stream=None, workspace=True):
+        """workspace: True (the cache's own, grown as needed: every page in one
+        launch), a device uint8 tensor, or None (launches of 96 pages)."""
         b, h, page = _i32(b), _i32(h), _i32(page)
         n = b.size
         rk = np.ascontiguousarray(np.broadcast_to(np.asarray(rank_k, dtype=np.uint8), (n,)))
         rv = np.ascontiguousarray(np.broadcast_to(np.asarray(rank_v, dtype=np.uint8), (n,)))
+        if workspace is True:
+            need = self.workspace_bytes(PKV_OP_COMPRESS, n)
+            ws = getattr(self, "_compress_ws", None)
+            if ws is None or ws.numel() < need:
+                ws = self._compress_ws = self.torch.empty(max(need, 256), dtype=self.torch.uint8,
+                                                          device=self.device)
+            workspace = ws
+        ws_ptr, ws_n = (None, 0) if workspace is None else (workspace.data_ptr(), workspace.numel())
         check(self.lib.pkv_compress_pages(ctypes.byref(self.c), layer, n, _np_ptr(b), _np_ptr(h),
-                                          _np_ptr(page), _np_ptr(rk), _np_ptr(rv), None, 0,
+                                          _np_ptr(page), _np_ptr(rk), _np_ptr(rv), ws_ptr, ws_n,
                                           _stream_handle(self.torch, stream)), "pkv_compress_pages")
 
     def attention(self, layer, q, seq_len, out=None, lse=None, workspace=None, stream=None):

@@ -246,10 +246,12 @@ hipError_t launch_append(const LaunchCtx &L, const void *k_new, const void *v_ne
 
 // ---- compress commit: DENSE -> FACTOR entries after the decompositions ------
 
-__global__ void k_compress_commit(Geo g, pkv_page *table, CompressItems items) {
-    const int i = threadIdx.x + blockIdx.x * blockDim.x;
-    if (i >= items.n) return;
-    const CompressItem it = items.it[i];
+// list: the items in device memory (n of them), or null for the launch's items.
+__global__ void k_compress_commit(Geo g, pkv_page *table, CompressItems items, const CompressItem *list,
+                                  int64_t n) {
+    const int64_t i = threadIdx.x + (int64_t)blockIdx.x * blockDim.x;
+    if (i >= (list ? n : (int64_t)items.n)) return;
+    const CompressItem it = list ? list[i] : items.it[i];
     const int64_t idx = g.head_index(it.b, it.h) * g.max_pages + it.j;
     // the same test the decompositions made: a refused page stays as it is
     if (compress_refusal(g, table, g.head_index(it.b, it.h), it.j) == 0u) {
@@ -261,7 +263,16 @@ __global__ void k_compress_commit(Geo g, pkv_page *table, CompressItems items) {
 
 hipError_t launch_compress_commit(const LaunchCtx &L, const CompressItems &items) {
     LayerPtrs p = layer_ptrs(L);
-    hipLaunchKernelGGL(k_compress_commit, dim3(1), dim3(128), 0, L.stream, L.geo, p.table, items);
+    hipLaunchKernelGGL(k_compress_commit, dim3(1), dim3(128), 0, L.stream, L.geo, p.table, items,
+                       (const CompressItem *)nullptr, (int64_t)0);
+    return hipGetLastError();
+}
+
+hipError_t launch_compress_commit_list(const LaunchCtx &L, const CompressItem *list, int64_t n) {
+    if (n <= 0) return hipSuccess;
+    LayerPtrs p = layer_ptrs(L);
+    hipLaunchKernelGGL(k_compress_commit, dim3((unsigned)ceil_div(n, 128)), dim3(128), 0, L.stream, L.geo, p.table,
+                       CompressItems{}, list, n);
     return hipGetLastError();
 }
 

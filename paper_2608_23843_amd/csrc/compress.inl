@@ -24,6 +24,7 @@ struct CompressSrc {
     SeqArgs off;              // prefill: item offset of sequence b (off.len[B] = total)
     const uint8_t *rank_k, *rank_v;
     int def_rk, def_rv;
+    const CompressItem *list;   // compress: the items in device memory, when set (else the launch's items)
 };
 
 __device__ inline float wave_shfl_xor(float v, int m) { return __shfl_xor(v, m, 64); }
@@ -56,7 +57,7 @@ __device__ inline DecompRef decode_decomp(const Geo &g, const pkv_page *table, c
     if (!r.active) return r;
     const int64_t item = q >> 1;
     if (src.mode == SRC_CACHE) {
-        const CompressItem it = items.it[item];
+        const CompressItem it = src.list ? src.list[item] : items.it[item];
         r.b = it.b; r.h = it.h; r.j = it.j; r.rk = it.rk; r.rv = it.rv;
         const int64_t head = g.head_index(r.b, r.h);
         const pkv_page e = table[head * g.max_pages + r.j];
@@ -348,6 +349,14 @@ hipError_t launch_compress(const LaunchCtx &L, const CompressItems &items) {
     CompressSrc src{};
     src.mode = SRC_CACHE;
     return launch_compress_any(L, items, src, 2LL * items.n);
+}
+
+hipError_t launch_compress_list(const LaunchCtx &L, const CompressItem *list, int64_t n) {
+    CompressItems items{};
+    CompressSrc src{};
+    src.mode = SRC_CACHE;
+    src.list = list;
+    return launch_compress_any(L, items, src, 2 * n);
 }
 
 hipError_t launch_prefill_compress(const LaunchCtx &L, const void *k, const void *v, int64_t src_tokens,

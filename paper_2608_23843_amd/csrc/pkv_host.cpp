@@ -217,7 +217,7 @@ size_t pkv_workspace_bytes(const pkv_cache *c, int32_t op, int64_t n) {
     Geo g = make_geo(c);
     switch (op) {
     case PKV_OP_ATTENTION: return (size_t)attention_workspace_bytes(g, n);
-    case PKV_OP_COMPRESS: return 0;
+    case PKV_OP_COMPRESS: return (size_t)((n * (int64_t)sizeof(CompressItem) + 255) / 256 * 256);
     case PKV_OP_PREFILL: return 0;
     case PKV_OP_IMPORT: return 0;
     case PKV_OP_GLOBAL_PREFILL: return (size_t)global_prefill_workspace_bytes(g, n);
@@ -343,7 +343,6 @@ pkv_status pkv_append_kv(const pkv_cache *c, int32_t layer, const void *k_new, c
 pkv_status pkv_compress_pages(const pkv_cache *c, int32_t layer, int32_t n, const int32_t *b,
                               const int32_t *kv_head, const int32_t *page, const uint8_t *rank_k,
                               const uint8_t *rank_v, void *ws, size_t ws_bytes, pkv_stream s) {
-    (void)ws; (void)ws_bytes;
     pkv_status st = check_cache(c, true);
     if (st != PKV_OK) return st;
     if ((st = check_layer(c, layer)) != PKV_OK) return st;
@@ -369,6 +368,26 @@ pkv_status pkv_compress_pages(const pkv_cache *c, int32_t layer, int32_t n, cons
     if (std::adjacent_find(sorted.begin(), sorted.end()) != sorted.end())
         return fail(PKV_E_ARG, "duplicate page in one compress call");
     LaunchCtx L = ctx(c, layer, s);
+    if (ws && ws_bytes >= (size_t)n * sizeof(CompressItem)) {
+        // the item list in the workspace: every page in one launch
+        std::vector<CompressItem> list((size_t)n);
+        for (int i = 0; i < n; ++i) {
+            CompressItem &it = list[(size_t)i];
+            it = CompressItem{};
+            it.b = b[i];
+            it.h = kv_head[i];
+            it.j = page[i];
+            it.rk = rank_k[i];
+            it.rv = rank_v[i];
+        }
+        const CompressItem *dl = (const CompressItem *)ws;
+        if ((st = check_launch(hipMemcpyAsync(ws, list.data(), (size_t)n * sizeof(CompressItem),
+                                              hipMemcpyHostToDevice, L.stream),
+                               "pkv_compress_pages (item list)")) != PKV_OK)
+            return st;
+        if ((st = check_launch(launch_compress_list(L, dl, n), "pkv_compress_pages")) != PKV_OK) return st;
+        return check_launch(launch_compress_commit_list(L, dl, n), "pkv_compress_pages (commit)");
+    }
     for (int base = 0; base < n; base += kCompressItemsPerLaunch) {
         CompressItems items{};
         items.n = std::min(kCompressItemsPerLaunch, n - base);

@@ -190,6 +190,9 @@ hipError_t launch_prefill_compress(const LaunchCtx &L, const void *k, const void
 hipError_t launch_append(const LaunchCtx &L, const void *k_new, const void *v_new, const SeqArgs &pos);
 hipError_t launch_compress(const LaunchCtx &L, const CompressItems &items);
 hipError_t launch_compress_commit(const LaunchCtx &L, const CompressItems &items);
+// The same with the n items in device memory, in one launch each.
+hipError_t launch_compress_list(const LaunchCtx &L, const CompressItem *list, int64_t n);
+hipError_t launch_compress_commit_list(const LaunchCtx &L, const CompressItem *list, int64_t n);
 hipError_t launch_import(const LaunchCtx &L, const CopyItems &items, const void *src);
 hipError_t launch_export(const LaunchCtx &L, const CopyItems &items, float *dst, int64_t block);
 hipError_t launch_export_int4(const LaunchCtx &L, const CopyItems &items, char *dst, int64_t block_bytes);

@@ -543,3 +543,50 @@ def test_import_refuses_two_dense_pages_on_one_slot():
     # the same page imported again replaces itself
     cache.import_pages(0, [0], [0], [1], [oracle.DENSE], [0], [0], bsrc, [0])
     assert cache.device_status() == 0
+
+
+def test_compress_page_list_in_workspace_matches_batches():
+    """pkv_compress_pages with a workspace (the page list copied to device
+    memory, every page in one launch) and without one (launches of 96 pages):
+    one window boundary of 128 (sequence, KV head) pairs, more than one
+    launch's worth. Factor pool, page table and device status equal byte for
+    byte between the two, and the factors agree with the oracle's SVD."""
+    import torch
+    import paper_2608_23843_amd as pk
+    B, Hkv, d, P, S, W, r = 16, 8, 64, 32, 32, 64, 12
+    T0 = 8 * P - 1
+    wl = synth.Workload("cw", 93, B, Hkv, Hkv, d, P, T0, S, W, 12, (r,), "bf16", 5e5, 4, decode_steps=P)
+    K, V = synth.kv_layer(wl, 0, 0)
+    max_pages = -(-(T0 + P) // P) + 1
+    caches = [pk.PuzzleKVCache(1, B, Hkv, Hkv, d, P, max_pages, 16, S, W, "bf16", "bf16") for _ in range(2)]
+    kt = torch.from_numpy(K[:, :, :T0]).to("cuda", torch.bfloat16).contiguous()
+    vt = torch.from_numpy(V[:, :, :T0]).to("cuda", torch.bfloat16).contiguous()
+    for c in caches:
+        c.dense_pool.zero_()
+        c.factor_pool.zero_()
+        c.prefill(0, kt, vt, [T0] * B, default_rank=(r, r))
+    refs = []
+    for t in range(T0, T0 + P):
+        kn = torch.from_numpy(K[:, :, t]).to("cuda", torch.bfloat16).contiguous()
+        vn = torch.from_numpy(V[:, :, t]).to("cuda", torch.bfloat16).contiguous()
+        for c in caches:
+            c.append(0, kn, vn, [t] * B)
+        new = oracle.eligible_pages(t, t + 1, P, S, W)
+        for j in new:
+            refs = [(b, h, int(j)) for b in range(B) for h in range(Hkv)]
+            bb, hh, jj = zip(*refs)
+            assert len(refs) > 96
+            caches[0].compress_pages(0, bb, hh, jj, [r] * len(refs), [8] * len(refs))
+            caches[1].compress_pages(0, bb, hh, jj, [r] * len(refs), [8] * len(refs), workspace=None)
+    torch.cuda.synchronize()
+    assert refs, "the run must cross a window boundary"
+    assert caches[0].device_status() == 0 and caches[1].device_status() == 0
+    assert torch.equal(caches[0].factor_pool, caches[1].factor_pool)
+    assert torch.equal(caches[0].table, caches[1].table)
+    assert torch.equal(caches[0].dense_pool, caches[1].dense_pool)
+    blocks = _export(caches[0], refs[::17])
+    R = caches[0].c.max_rank
+    for (b, h, j), blk in zip(refs[::17], blocks):
+        Lk, Rk, Lv, Rv = _unpack_factor(blk, P, d, R)
+        _check_factor(Lk[:, :r], Rk[:r], K[b, h, j * P:(j + 1) * P].astype(np.float64), r, 6e-3, 1e-2, 4e-3)
+        _check_factor(Lv[:, :8], Rv[:8], V[b, h, j * P:(j + 1) * P].astype(np.float64), 8, 6e-3, 1e-2, 4e-3)
