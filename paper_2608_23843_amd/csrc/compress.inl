@@ -24,7 +24,8 @@ struct CompressSrc {
     SeqArgs off;              // prefill: item offset of sequence b (off.len[B] = total)
     const uint8_t *rank_k, *rank_v;
     int def_rk, def_rv;
-    const CompressItem *list;   // compress: the items in device memory, when set (else the launch's items)
+    const CompressItem *list;   // compress: the items in device memory, when set (else the launch's items);
+                                // the matrix-core kernel takes it through its kList instantiation
 };
 
 __device__ inline float wave_shfl_xor(float v, int m) { return __shfl_xor(v, m, 64); }
@@ -46,7 +47,10 @@ struct DecompRef {
     bool transposed;   // X is V^T (d x P), the dense slot's value layout
 };
 
-template <typename TX>
+// kList: compress items come from src.list (device memory), else from the
+// launch's items (a template parameter: the runtime choice cost the
+// register-bound decomposition kernel a spill).
+template <typename TX, bool kList = false>
 __device__ inline DecompRef decode_decomp(const Geo &g, const pkv_page *table, const char *dense,
                                           const CompressItems &items, const CompressSrc &src, int64_t q,
                                           int64_t n_decomp, bool report) {
@@ -57,7 +61,7 @@ __device__ inline DecompRef decode_decomp(const Geo &g, const pkv_page *table, c
     if (!r.active) return r;
     const int64_t item = q >> 1;
     if (src.mode == SRC_CACHE) {
-        const CompressItem it = src.list ? src.list[item] : items.it[item];
+        const CompressItem it = kList ? src.list[item] : items.it[item];
         r.b = it.b; r.h = it.h; r.j = it.j; r.rk = it.rk; r.rv = it.rv;
         const int64_t head = g.head_index(r.b, r.h);
         const pkv_page e = table[head * g.max_pages + r.j];
@@ -109,7 +113,8 @@ __global__ __launch_bounds__(64) void k_compress(Geo g, pkv_page *table, const c
     TX *sX = sX_all + (int64_t)grp * P * ld_x;
 
     // ---- which page, which half (K or V), ranks, source --------------------
-    const DecompRef ref = decode_decomp<TX>(g, table, dense, items, src, q, n_decomp, c == 0);
+    const DecompRef ref = src.list ? decode_decomp<TX, true>(g, table, dense, items, src, q, n_decomp, c == 0)
+                                   : decode_decomp<TX, false>(g, table, dense, items, src, q, n_decomp, c == 0);
     bool active = ref.active;
     const int b = ref.b, h = ref.h, j = ref.j, rk = ref.rk, rv = ref.rv, which = ref.which;
     const TX *X = (const TX *)ref.X;

@@ -184,7 +184,7 @@ __device__ __forceinline__ int cq_rank(float key, int c, int grp) {
 // know K's rank before it stores: the two halves of the wavefront hold K and
 // V at P = 32, and at P = 64 the wavefront decomposes K, then V. With fixed
 // ranks every P = 64 decomposition is a wavefront of its own.
-template <typename TF, int P, bool kAdapt>
+template <typename TF, int P, bool kAdapt, bool kList = false>
 __global__ __launch_bounds__(64) __attribute__((amdgpu_waves_per_eu(3)))
 void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor, CompressItems items, CompressSrc src,
                    int64_t n_decomp) {
@@ -204,7 +204,7 @@ void k_compress_qr(Geo g, pkv_page *table, const char *dense, char *factor, Comp
     // a pass is active exactly when the other one is
     const int64_t q = ((int64_t)blockIdx.x * kPasses + kv) * D + grp;
 
-    const DecompRef ref = decode_decomp<uint16_t>(g, table, dense, items, src, q, n_decomp, c == 0);
+    const DecompRef ref = decode_decomp<uint16_t, kList>(g, table, dense, items, src, q, n_decomp, c == 0);
     const bool active = ref.active;
     const uint16_t *X = (const uint16_t *)ref.X;
 
@@ -825,8 +825,12 @@ hipError_t launch_compress_qr_a(const LaunchCtx &L, const CompressItems &items, 
     const size_t smem = (size_t)cq_wave_lds(L.geo.d, is_q4<TF>::value) * sizeof(float);
     const int64_t blocks = ceil_div(n_decomp, (int64_t)per_wave);
     LayerPtrs p = layer_ptrs(L);
-    hipLaunchKernelGGL((k_compress_qr<TF, P, kAdapt>), dim3((unsigned)blocks), dim3(64), smem, L.stream,
-                       L.geo, p.table, p.dense, p.factor, items, src, n_decomp);
+    if (src.list)
+        hipLaunchKernelGGL((k_compress_qr<TF, P, kAdapt, true>), dim3((unsigned)blocks), dim3(64), smem, L.stream,
+                           L.geo, p.table, p.dense, p.factor, items, src, n_decomp);
+    else
+        hipLaunchKernelGGL((k_compress_qr<TF, P, kAdapt>), dim3((unsigned)blocks), dim3(64), smem, L.stream,
+                           L.geo, p.table, p.dense, p.factor, items, src, n_decomp);
     return hipGetLastError();
 }
 
