@@ -600,7 +600,7 @@ __device__ inline pkv_page unpack_entry(uint2 ent) {
 // with page i+1's while phase 2 of page i reads the value operands, refilled
 // in turn with page i+1's. One operand set per wave keeps the register budget
 // at two waves per SIMD.
-template <int D, int P, bool Q4, bool ROPE = false>
+template <int D, int P, bool Q4, bool ROPE = false, bool FOLD = false>
 __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, const pkv_page *__restrict__ table,
                                                                   const char *__restrict__ dense,
                                                                   const char *__restrict__ factor,
@@ -683,10 +683,10 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
         // dense slots, which the host keeps within the queue) and done after.
         __shared__ int s_dense[kQ4DenseStage];
         __shared__ unsigned int s_nd;
-        // the query group as fp16 B operands, elements of pairs 1 and 3
-        // (e = 2, 3, 6, 7) divided by 16 for the raw key words (exact unless
-        // subnormal); one copy per workgroup (every wave serves this head),
-        // read per page instead of held in registers
+        // the query group times c2 (scores come out in log2 units) as fp16 B
+        // operands, elements of pairs 1 and 3 (e = 2, 3, 6, 7) also divided
+        // by 16 for the raw key words; one copy per workgroup (every wave
+        // serves this head), read per page instead of held in registers
         __shared__ f16x8 s_qh[4][64];
         __builtin_amdgcn_s_waitcnt(0x0f70);   // vmcnt(0): the query
         if (threadIdx.x == 0) s_nd = 0u;
@@ -695,7 +695,7 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
             for (int s = 0; s < 4; ++s) {
                 f16x8 h;
 #pragma unroll
-                for (int e = 0; e < 8; ++e) h[e] = (_Float16)((float)qb[s][e] * ((e & 2) ? 0.0625f : 1.0f));
+                for (int e = 0; e < 8; ++e) h[e] = (_Float16)((float)qb[s][e] * ((e & 2) ? 0.0625f * c2 : c2));
                 s_qh[s][lane] = h;
             }
         }
@@ -743,13 +743,14 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
             const bool live = cur.kind == PKV_FACTOR;
             if (live) {
                 f32x4 st[4];
-                q4_scores(ko, s_qh, lane, st, kq4);
+                // scores start from -(m_run + 2^4 units), or 0 on the first page
+                q4_scores(ko, s_qh, lane, st, kq4, w4.m_run == -INFINITY ? 0.f : -(w4.m_run + kQ4UnitLog2));
                 q4_issue_key_loads(ko, nres, n, q4);
-                q4_exp<D, 64, false>(w4, st, 64, q4, c2);
+                q4_exp_shifted<D, FOLD>(w4, st);
                 f16x8 yh, yl;
-                q4_values_y(vy, st, yh, yl, kq4);
+                q4_values_y<FOLD>(vy, st, yh, yl, kq4);
                 q4_issue_y_loads(vy, nres, n, q4);
-                q4_values_o<D>(w4, vo, yh, yl, kq4);
+                q4_values_o<D, FOLD>(w4, vo, yh, yl, kq4);
                 q4_issue_o_loads(vo, nres, n, q4);
             } else {
                 q4_issue_key_loads(ko, nres, n, q4);
@@ -770,7 +771,7 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
             bf16x8 qd[KD];
 #pragma unroll
             for (int s = 0; s < KD; ++s) qd[s] = n < G ? ld_b8(qp + 32 * s) : zero8();
-            q4_dense_page<D>(w4, qd, dense, g.dense_slot_bytes, e.slot, (int)min<int64_t>(P, T - j * P), n, q4, c2);
+            q4_dense_page<D, FOLD>(w4, qd, dense, g.dense_slot_bytes, e.slot, (int)min<int64_t>(P, T - j * P), n, q4, c2);
         }
         w.m_run = w4.m_run;
         w.l[0] = w4.l;
@@ -1026,7 +1027,8 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
 #pragma unroll
         for (int ww = 0; ww < NW; ++ww) {
             const float sc = s_m[ww][qi] == -INFINITY ? 0.f : exp2f(s_m[ww][qi] - M);
-            acc = fmaf(sc, s_o[ww][qi][k], acc);
+            // INT4 at <= 8 queries: rows 8-15 hold the lo parts of rows 0-7
+            acc = fmaf(sc, FOLD ? s_o[ww][qi][k] + s_o[ww][qi + 8][k] : s_o[ww][qi][k], acc);
             l = fmaf(sc, s_l[ww][qi], l);
         }
         if constexpr (Q4) {   // back from the INT4 kernel's units of 2^-4
@@ -1068,8 +1070,12 @@ hipError_t launch_attn_mfma(const LaunchCtx &L, const AttnPlan &plan, const uint
             else PKV_LAUNCH_MFMA_ROPE(64, 32);
         }
     } else if (g.factor_dtype == PKV_INT4) {
-        hipLaunchKernelGGL((k_attn_mfma<128, 64, true>), grid, dim3(64 * kMfmaWavesQ4), 0, L.stream, g, p.table,
-                           p.dense, p.factor, q, seq, plan.sched, plan.n_chunks, pp, out, lse);
+        if (g.g <= 8)   // padding columns 8-15 carry the lo half of the O^T update
+            hipLaunchKernelGGL((k_attn_mfma<128, 64, true, false, true>), grid, dim3(64 * kMfmaWavesQ4), 0, L.stream,
+                               g, p.table, p.dense, p.factor, q, seq, plan.sched, plan.n_chunks, pp, out, lse);
+        else
+            hipLaunchKernelGGL((k_attn_mfma<128, 64, true>), grid, dim3(64 * kMfmaWavesQ4), 0, L.stream, g, p.table,
+                               p.dense, p.factor, q, seq, plan.sched, plan.n_chunks, pp, out, lse);
     } else if (g.d == 128) {
         if (g.P == 64) PKV_LAUNCH_MFMA(128, 64);
         else if (g.P == 32) PKV_LAUNCH_MFMA(128, 32);

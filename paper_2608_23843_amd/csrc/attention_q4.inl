@@ -18,6 +18,12 @@
 //                        column scale of R~_V
 // The exp weights, l and O^T are kept in units of 2^-4 so every fp16 operand
 // stays in range and out of the subnormals.
+// With at most 8 queries per group, columns 8-15 of every 16x16 product are
+// padding; the O^T update then takes Y hi in columns 0-7 and Y lo in columns
+// 8-15 of one B operand (one product per dim tile instead of two), the lo
+// parts accumulate in the wave's rows 8-15 of O^T, and those rows are added
+// to rows 0-7 when the wave states are merged (lanes n and n + 8 keep the
+// same running max so both rows share every rescale).
 // Unpacking a word of eight nibbles n = c + 8 takes one and-or per pair of
 // codes: masked into the low mantissa of 1024.0 (fp16, quantum 1) a nibble
 // at bits 0-3 gives 1024 + n and one at bits 4-7 gives 1024 + 16 n, both
@@ -83,6 +89,24 @@ __device__ inline void split_tiles_f16(const f32x4 &x0, const f32x4 &x1, f16x8 &
     split2_f16(x1[2], x1[3], h3, l3);
     hi = __builtin_bit_cast(f16x8, u32x4{h0, h1, h2, h3});
     lo = __builtin_bit_cast(f16x8, u32x4{l0, l1, l2, l3});
+}
+
+// Within each 16-lane row, lanes 8-15 take `src` of lane n - 8 and lanes 0-7
+// keep `keep` (DPP row rotate by 8, written to banks 2 and 3 only).
+__device__ inline uint32_t row_hi_from_lo(uint32_t keep, uint32_t src) {
+    return (uint32_t)__builtin_amdgcn_update_dpp((int)keep, (int)src, 0x128, 0xf, 0xc, false);
+}
+__device__ inline float row_hi_from_lo(float keep, float src) {
+    return __uint_as_float(row_hi_from_lo(__float_as_uint(keep), __float_as_uint(src)));
+}
+// B operand of the folded O^T update: Y hi in lanes 0-7 of each row, Y lo of
+// lane n - 8 in lanes 8-15.
+__device__ inline f16x8 fold_hi_lo(const f16x8 &hi, const f16x8 &lo) {
+    const u32x4 h = __builtin_bit_cast(u32x4, hi), l = __builtin_bit_cast(u32x4, lo);
+    u32x4 o;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) o[i] = row_hi_from_lo(h[i], l[i]);
+    return __builtin_bit_cast(f16x8, o);
 }
 
 // Operand words of one INT4 factor page held by one lane.
@@ -184,7 +208,7 @@ __device__ inline void lds_st4(float *p, const f32x4 &v) { *(f32x4 *)p = v; }
 // lazy running max: it is raised (and O^T, l rescaled) only when a score
 // exceeds it by 2^4, so the exp weights, in units of 2^-4, stay at most 1.
 // Rows at or past `rows` are masked (dense pages).
-template <int D, int P, bool MASK>
+template <int D, int P, bool MASK, bool FOLD>
 __device__ inline void q4_exp(Q4State &w, f32x4 (&st)[P / 16], int rows, int q, float c2) {
     constexpr int TT = P / 16;
     float pm = -INFINITY;
@@ -195,6 +219,7 @@ __device__ inline void q4_exp(Q4State &w, f32x4 (&st)[P / 16], int rows, int q, 
             if (MASK && token_row<P>(tt, 4 * q + v) >= rows) st[tt][v] = -INFINITY;
             pm = fmaxf(pm, st[tt][v]);
         }
+    if constexpr (FOLD) pm = row_hi_from_lo(pm, pm);   // lanes n + 8 follow query n's max
     if (__builtin_amdgcn_ballot_w64(pm * c2 > w.m_run + kLazyLog2Q4) != 0) {
         pm = fmaxf(pm, __shfl_xor(pm, 16, 64));
         pm = fmaxf(pm, __shfl_xor(pm, 32, 64));
@@ -217,11 +242,53 @@ __device__ inline void q4_exp(Q4State &w, f32x4 (&st)[P / 16], int rows, int q, 
     w.l += sum;
 }
 
-// Scores of an INT4 factor page: Z^T, then S^T into st (raw, fp32). qh16
-// (LDS, [s][lane]): the query group as fp16 B operands, elements of pairs 1
-// and 3 divided by 16.
+// The same update for factor-page scores that arrive already in log2 units
+// and shifted: st = s c2 - (m_run + 2^4 units), or s c2 while the running max
+// is still -inf (the wave's first page). The shift came in through the score
+// accumulators' start, so the exponent needs no fma.
+template <int D, bool FOLD>
+__device__ inline void q4_exp_shifted(Q4State &w, f32x4 (&st)[4]) {
+    float pm = -INFINITY;
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) pm = fmaxf(pm, st[tt][v]);
+    if constexpr (FOLD) pm = row_hi_from_lo(pm, pm);   // lanes n + 8 follow query n's max
+    const bool first = w.m_run == -INFINITY;           // the same in every lane
+    // lazy max: raised only when a score passes it by 2^4 (kLazyLog2Q4 = kQ4UnitLog2)
+    if (first || __builtin_amdgcn_ballot_w64(pm > kLazyLog2Q4 - kQ4UnitLog2) != 0) {
+        pm = fmaxf(pm, __shfl_xor(pm, 16, 64));
+        pm = fmaxf(pm, __shfl_xor(pm, 32, 64));
+        const float top = first ? pm : w.m_run + kQ4UnitLog2 + pm;   // the page's largest s c2
+        const float m_new = fmaxf(w.m_run, top);
+        if (!first) {
+            const float alpha = exp2f(w.m_run - m_new);
+#pragma unroll
+            for (int dt = 0; dt < D / 16; ++dt) lds_st4(w.ol + 16 * dt, lds_ld4(w.ol + 16 * dt) * alpha);
+            w.l *= alpha;
+        }
+        const float sh = first ? -(m_new + kQ4UnitLog2) : w.m_run - m_new;
+#pragma unroll
+        for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) st[tt][v] += sh;
+        w.m_run = m_new;
+    }
+    float sum = 0.f;
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt) {
+#pragma unroll
+        for (int v = 0; v < 4; ++v) st[tt][v] = __builtin_amdgcn_exp2f(st[tt][v]);
+        sum += (st[tt][0] + st[tt][1]) + (st[tt][2] + st[tt][3]);
+    }
+    w.l += sum;
+}
+
+// Scores of an INT4 factor page: Z^T, then S^T into st (fp32, log2 units,
+// started from `shift` per query). qh16 (LDS, [s][lane]): the query group
+// times c2 as fp16 B operands, elements of pairs 1 and 3 divided by 16.
 __device__ inline void q4_scores(const Q4Key &f, const f16x8 (&qh16)[4][64], int lane, f32x4 (&st)[4],
-                                 const Q4Consts &k) {
+                                 const Q4Consts &k, float shift) {
     f16x8 qs[4];
 #pragma unroll
     for (int s = 0; s < 4; ++s) qs[s] = qh16[s][lane] * __builtin_bit_cast(f16x8, f.bks[s]);
@@ -260,7 +327,7 @@ __device__ inline void q4_scores(const Q4Key &f, const f16x8 (&qh16)[4][64], int
                 zs[rt][v + 1] = fmaf(z[rt][v + 1], (float)s2[1], zero);
             }
         split_tiles_f16(zs[0], zs[1], zh[u], zl[u]);
-        sb[u] = mfma_f16(nbeta, zh[u], zero_f4());
+        sb[u] = mfma_f16(nbeta, zh[u], f32x4{shift, shift, shift, shift});
         sb[u] = mfma_f16(nbeta, zl[u], sb[u]);
     }
 #pragma unroll
@@ -276,6 +343,7 @@ __device__ inline void q4_scores(const Q4Key &f, const f16x8 (&qh16)[4][64], int
 // returned as the fp16 hi/lo B operands of O^T, with the rows of ranks 2 and
 // 3 mod 4 (elements e = 2, 3, 6, 7 of each lane) divided by 16 for the raw
 // R~_V words, by the magic 64.0 in those lanes' A operand.
+template <bool FOLD>
 __device__ inline void q4_values_y(const Q4ValY &f, const f32x4 (&st)[4], f16x8 &yh, f16x8 &yl,
                                    const Q4Consts &k) {
     // E' (fp16): token 32 ks + 8q + e in element e of eb[ks]; tokens whose
@@ -312,22 +380,24 @@ __device__ inline void q4_values_y(const Q4ValY &f, const f32x4 (&st)[4], f16x8 
             y[rt] = mfma_f16(q4_frag_raw(f.avc[2 * rt + ks], k, k.h16y), eb[ks], y[rt]);
     }
     split_tiles_f16(y[0], y[1], yh, yl);
+    if constexpr (FOLD) yh = fold_hi_lo(yh, yl);
 }
 
 // O^T += s .* (R~_V^T Y^T) from raw R~_V^T code words, each dim tile started
 // from -beta x Y so the product is the codes' alone; output row c scaled by
 // the column scale of R~_V.
-template <int D>
+// With FOLD, yh is the folded operand (hi | lo by lane half) and yl unused.
+template <int D, bool FOLD>
 __device__ inline void q4_values_o(Q4State &w, const Q4ValO &f, const f16x8 &yh, const f16x8 &yl,
                                    const Q4Consts &k) {
     const f16x8 nbeta = f16x8{-1032, -1032, -1152, -1152, -1032, -1032, -1152, -1152};
     f32x4 ob = mfma_f16(nbeta, yh, zero_f4());
-    ob = mfma_f16(nbeta, yl, ob);
+    if constexpr (!FOLD) ob = mfma_f16(nbeta, yl, ob);
 #pragma unroll
     for (int dt = 0; dt < D / 16; ++dt) {
         const f16x8 a = q4_frag_raw(f.bvc[dt >> 2][dt & 3], k);
         f32x4 pr = mfma_f16(a, yh, ob);
-        pr = mfma_f16(a, yl, pr);
+        if constexpr (!FOLD) pr = mfma_f16(a, yl, pr);
         f32x4 o = lds_ld4(w.ol + 16 * dt);
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
@@ -341,7 +411,7 @@ __device__ inline void q4_values_o(Q4State &w, const Q4ValO &f, const f16x8 &yh,
 
 // A dense page, loaded and computed in place in units of 32 tokens (used for
 // the few dense pages after the INT4 stream).
-template <int D>
+template <int D, bool FOLD>
 __device__ inline void q4_dense_page(Q4State &w, const bf16x8 (&qb)[D / 32], const char *dense,
                                      int64_t slot_bytes, int slot, int rows_page, int n, int q, float c2) {
     const uint16_t *K = (const uint16_t *)(dense + slot * slot_bytes);
@@ -356,9 +426,13 @@ __device__ inline void q4_dense_page(Q4State &w, const bf16x8 (&qb)[D / 32], con
 #pragma unroll
             for (int s = 0; s < D / 32; ++s) st[tt] = mfma_bf16(ld_b8(kp + 32 * s), qb[s], st[tt]);
         }
-        q4_exp<D, 32, true>(w, st, rows, q, c2);
+        q4_exp<D, 32, true, FOLD>(w, st, rows, q, c2);
         bf16x8 eh, el;
         split_tiles(st[0], st[1], eh, el);
+        if (FOLD && n >= 8) {   // rows 8-15 of O^T hold the factor pages' lo parts
+            eh = zero8();
+            el = zero8();
+        }
 #pragma unroll
         for (int dt = 0; dt < D / 16; ++dt) {
             bf16x8 vv = ld_b8(Vt + (int64_t)(16 * dt + n) * 64 + 32 * half + 8 * q);

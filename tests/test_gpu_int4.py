@@ -160,6 +160,34 @@ def test_int4_attention_matches_oracle(seq_lens, ranks):
     assert ma <= MAX_ABS and mr <= MEAN_REL, (ma, mr)
 
 
+@pytest.mark.parametrize("g", [1, 5, 16])
+def test_int4_attention_query_groups(g):
+    """Query groups below, between and above 8: at most 8 queries the kernel
+    carries the lo half of the O^T update in the padding columns 8-15 and
+    folds those rows back at the merge; 16 queries use both halves of every
+    product for queries."""
+    import paper_2608_23843_amd as pk
+    seq_lens = [64 * 21 + 5, 64 * 9]
+    B, Hkv, S, W = len(seq_lens), 2, 64, 128
+    Tmax = max(seq_lens)
+    wl = _wl(B, Hkv, g, Tmax, S, W, seed_wid=96)
+    max_pages = -(-Tmax // P)
+    cache = pk.PuzzleKVCache(1, B, Hkv, Hkv * g, D, P, max_pages, 32, S, W, "bf16", "int4")
+    rng = np.random.default_rng(11)
+    heads = {}
+    for b, T in enumerate(seq_lens):
+        for h in range(Hkv):
+            K, V = synth.kv_head(wl, 0, 0, b, h, max_pages * P)
+            K, V = _bf16(K), _bf16(V)
+            rks = {j: tuple(int(x) for x in rng.choice([8, 17, 24, 32], 2)) for j in range(max_pages)}
+            pages, blobs = _encode_head(K, V, T, S, W, lambda j: rks[j])
+            _import(cache, b, h, pages, blobs)
+            heads[(b, h)] = oracle.HeadCache(T, P, D, pages)
+    out, ref = _attend(cache, wl, seq_lens, heads, g)
+    ma, mr = errors(out, ref)
+    assert ma <= MAX_ABS and mr <= MEAN_REL, (g, ma, mr)
+
+
 def _near_tie(x, s):
     qv = np.abs(x / np.where(s > 0, s, 1.0))
     return np.abs(qv - np.floor(qv) - 0.5) < 1e-3
