@@ -25,6 +25,8 @@ constexpr float kLn2 = 0.6931471805599453f;
 // contiguous block (whole cache lines written, no line shared between
 // workgroups) and the merge reads one chunk per load across consecutive
 // lanes. The partials are fully written by every call before they are read.
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+
 struct Partials {
     float *o, *m, *l;
     unsigned int *counters;  // chunks published, per head
@@ -103,9 +105,99 @@ __device__ inline float ld_dev(const float *p) {
 // short: it runs once per launch, from a cold instruction cache.
 constexpr int kMergeGroup = 32;
 
+// The fold of the last workgroup with 16-byte partial loads, for shapes whose
+// F = G d / 4 groups of four outputs divide the workgroup into R lanes each:
+// thread (f, r) folds chunks r, r + R, ... of output group f (one coherent
+// 16-byte load per chunk, J per group of kMergeGroup chunks, loads past the
+// last chunk read it again and are masked), every lane of a query uses the
+// same running max (the group's maxima through LDS), and the R partial sums
+// of an output group are added through LDS at the end. s_mg, s_lg: the
+// group maxima and normalizers (16 x kMergeGroup floats each); red: 5 NT
+// floats of LDS for the sums, 16-byte aligned.
+template <int NT, int R>
+__device__ void merge_vec(const Geo &g, int64_t head, const Partials &pp, float *out, float *lse, int64_t T,
+                          float *s_mg, float *s_lg, float *red) {
+    constexpr int J = (kMergeGroup + R - 1) / R;
+    constexpr int MLT = (16 * kMergeGroup + NT - 1) / NT;
+    f32x4 *s_ra = (f32x4 *)red;
+    float *s_rl = red + 4 * NT;
+    const int tid = threadIdx.x;
+    const int nc = pp.nc, G = g.g, d = g.d;
+    const int F = NT / R;
+    const int f = tid % F, r = tid / F;
+    const int q = (4 * f) / d, k = (4 * f) % d;
+    const uint32_t cs = (uint32_t)(G * d) * 4u;   // chunk stride in bytes
+    const __amdgpu_buffer_rsrc_t ro = __builtin_amdgcn_make_buffer_rsrc(
+        pp.o + pp.oi(head, 0, 0, 0), (short)0, (int)((uint32_t)pp.nc4 * cs), 0x00020000);
+    float M = -INFINITY, L = 0.f;
+    f32x4 A = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int c0 = 0; c0 < nc; c0 += kMergeGroup) {
+        float mreg[MLT], lreg[MLT];
+#pragma unroll
+        for (int i = 0; i < MLT; ++i) {
+            const int t = tid + i * NT;
+            const int qm = min(t / kMergeGroup, G - 1), cu = min(c0 + t % kMergeGroup, nc - 1);
+            mreg[i] = ld_dev(pp.m + pp.mi(head, qm, cu));
+            lreg[i] = ld_dev(pp.l + pp.mi(head, qm, cu));
+        }
+        f32x4 ov[J];
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            const uint32_t c = (uint32_t)min(c0 + r + R * j, nc - 1);
+            ov[j] = __builtin_bit_cast(f32x4, __builtin_amdgcn_raw_buffer_load_b128(ro, c * cs + 16u * (uint32_t)f, 0, 16));
+        }
+        __syncthreads();   // the previous group's maxima have been read
+#pragma unroll
+        for (int i = 0; i < MLT; ++i) {
+            const int t = tid + i * NT;
+            if (t < 16 * kMergeGroup) {
+                s_mg[t] = (t % kMergeGroup) < nc - c0 ? mreg[i] : -INFINITY;
+                s_lg[t] = lreg[i];
+            }
+        }
+        __syncthreads();
+        const float *mg = s_mg + q * kMergeGroup, *lg = s_lg + q * kMergeGroup;
+        float Mg = M;
+        for (int u = 0; u < kMergeGroup; u += 4) {
+            const f32x4 m4 = *(const f32x4 *)(mg + u);
+            Mg = fmaxf(Mg, fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3])));
+        }
+        if (Mg == -INFINITY) continue;   // no tokens in any chunk so far
+        const float sc = __builtin_amdgcn_exp2f(M - Mg);
+        L *= sc;
+        A *= sc;
+#pragma unroll
+        for (int j = 0; j < J; ++j) {
+            const int u = r + R * j;   // chunk c0 + u; at or past nc its maximum is -inf
+            const float wgt = u < kMergeGroup ? __builtin_amdgcn_exp2f(mg[u] - Mg) : 0.f;
+            if (u < kMergeGroup) L = fmaf(wgt, lg[u], L);
+            A += wgt * ov[j];
+        }
+        M = Mg;
+    }
+    s_ra[tid] = A;
+    s_rl[tid] = L;
+    __syncthreads();
+    if (r == 0) {
+#pragma unroll
+        for (int i = 1; i < R; ++i) {
+            A += s_ra[i * F + f];
+            L += s_rl[i * F + f];
+        }
+        const bool empty = T <= 0 || !(L > 0.f);
+        const int b = (int)(head / g.Hkv), h = (int)(head % g.Hkv);
+        float *o = out + ((int64_t)b * g.Hq + h * G + q) * d + k;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) o[i] = empty ? 0.f : A[i] / L;
+        if (lse && k == 0) lse[(int64_t)b * g.Hq + h * G + q] = empty ? -INFINITY : (M + log2f(L)) * kLn2;
+    }
+}
+
+// red: at least 5 NT floats of LDS the caller no longer needs (16-byte
+// aligned), or null: the fold with 16-byte loads needs them.
 template <int NT>
 __device__ void publish_and_merge(const Geo &g, int64_t head, const Partials &pp, float *out, float *lse,
-                                  int64_t T) {
+                                  int64_t T, float *red = nullptr) {
     constexpr int kMaxG = 16;                                      // the kernels' query-group limit
     constexpr int MLT = (kMaxG * kMergeGroup + NT - 1) / NT;       // group maxima per thread
     __shared__ unsigned int s_prev;
@@ -119,6 +211,24 @@ __device__ void publish_and_merge(const Geo &g, int64_t head, const Partials &pp
     if (s_prev != (unsigned int)(nc - 1)) return;
 
     const int G = g.g, d = g.d;
+    bool done = false;
+    // only where the per-output fold below would take several passes (G d >
+    // NT): at batch 1 (G d = NT, 32 chunks) that fold measured faster
+    if (red && G * d > NT && (G * d) % 4 == 0 && NT % (G * d / 4) == 0) {
+        switch (NT / (G * d / 4)) {
+        case 2: merge_vec<NT, 2>(g, head, pp, out, lse, T, s_mg, s_lg, red); done = true; break;
+        case 3: merge_vec<NT, 3>(g, head, pp, out, lse, T, s_mg, s_lg, red); done = true; break;
+        case 4: merge_vec<NT, 4>(g, head, pp, out, lse, T, s_mg, s_lg, red); done = true; break;
+        default: break;
+        }
+    }
+    if (done) {
+        if (tid == 0) {
+            __hip_atomic_store(&pp.counters[head], 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(pp.claim(head), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        return;
+    }
     const int b = (int)(head / g.Hkv), h = (int)(head % g.Hkv);
     // the same trip counts in every thread: the group loop holds barriers
     for (int base = 0; base < G * d; base += NT) {

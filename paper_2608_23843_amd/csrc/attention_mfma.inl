@@ -1041,7 +1041,8 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
             st_dev(&pp.l[pp.mi(head, qi, chunk)], l);
         }
     }
-    publish_and_merge<64 * NW>(g, head, pp, out, lse, T);
+    // the wave-state block is free once every thread has passed the publish barrier
+    publish_and_merge<64 * NW>(g, head, pp, out, lse, T, &s_o[0][0][0]);
 }
 
 inline bool mfma_supported(const Geo &g) {
