@@ -636,7 +636,7 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
     // merge buffers; the INT4 kernel also keeps its O^T accumulators in s_o
     // (rows padded to D + 4 floats against bank conflicts)
     __shared__ float s_m[NW][16], s_l[NW][16];
-    __shared__ float s_o[NW][16][D + 4];
+    __shared__ __align__(16) float s_o[NW][16][D + 4];
 
     WaveState<D> w;
 #pragma unroll

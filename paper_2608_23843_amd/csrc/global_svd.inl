@@ -586,7 +586,7 @@ __global__ __launch_bounds__(64 * kGAttnWaves, 1) void k_attn_global(Geo g, Glob
 
     // ---- merge the wave states (Eq. (5)) into the chunk's partial --------------
     __shared__ float s_m[NW][16], s_l[NW][16];
-    __shared__ float s_o[NW][16][D + 4];
+    __shared__ __align__(16) float s_o[NW][16][D + 4];
     if (q4 == 0) {
         s_m[wave][n] = w.m_run;
         s_l[wave][n] = w.l[0];
@@ -614,7 +614,8 @@ __global__ __launch_bounds__(64 * kGAttnWaves, 1) void k_attn_global(Geo g, Glob
             st_dev(&pp.l[pp.mi(head, qi, chunk)], l);
         }
     }
-    publish_and_merge<64 * NW>(g, head, pp, out, lse, T);
+    // the wave-state block is free once every thread has passed the publish barrier
+    publish_and_merge<64 * NW>(g, head, pp, out, lse, T, &s_o[0][0][0]);
 }
 
 // ---- launches -----------------------------------------------------------------------
