@@ -1018,24 +1018,30 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
             for (int v = 0; v < 4; ++v) s_o[wave][n][16 * dt + 4 * q4 + v] = w.o[dt][v];
     }
     __syncthreads();
-    for (int idx = threadIdx.x; idx < G * D; idx += 64 * NW) {
-        const int qi = idx / D, k = idx % D;
+    // four dims per thread: the wave weights once per query and dims, and one
+    // 16-byte store with the coherent cache policy of st_dev
+    const __amdgpu_buffer_rsrc_t rpo =
+        __builtin_amdgcn_make_buffer_rsrc(pp.o + pp.oi(head, 0, 0, chunk), (short)0, G * D * 4, kBufferDword3);
+    for (int f = threadIdx.x; f < G * D / 4; f += 64 * NW) {
+        const int qi = (4 * f) / D, k = (4 * f) % D;
         float M = -INFINITY;
 #pragma unroll
         for (int ww = 0; ww < NW; ++ww) M = fmaxf(M, s_m[ww][qi]);
-        float acc = 0.f, l = 0.f;
+        f32x4 acc = zero_f4();
+        float l = 0.f;
 #pragma unroll
         for (int ww = 0; ww < NW; ++ww) {
             const float sc = s_m[ww][qi] == -INFINITY ? 0.f : exp2f(s_m[ww][qi] - M);
             // INT4 at <= 8 queries: rows 8-15 hold the lo parts of rows 0-7
-            acc = fmaf(sc, FOLD ? s_o[ww][qi][k] + s_o[ww][qi + 8][k] : s_o[ww][qi][k], acc);
+            const f32x4 o = FOLD ? lds_ld4(&s_o[ww][qi][k]) + lds_ld4(&s_o[ww][qi + 8][k]) : lds_ld4(&s_o[ww][qi][k]);
+            acc += sc * o;
             l = fmaf(sc, s_l[ww][qi], l);
         }
         if constexpr (Q4) {   // back from the INT4 kernel's units of 2^-4
             acc *= kQ4Unit;
             l *= kQ4Unit;
         }
-        st_dev(&pp.o[pp.oi(head, qi, k, chunk)], acc);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc), rpo, 16u * (uint32_t)f, 0, 16);
         if (k == 0) {
             st_dev(&pp.m[pp.mi(head, qi, chunk)], M);
             st_dev(&pp.l[pp.mi(head, qi, chunk)], l);

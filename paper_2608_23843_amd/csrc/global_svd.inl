@@ -596,19 +596,23 @@ __global__ __launch_bounds__(64 * kGAttnWaves, 1) void k_attn_global(Geo g, Glob
 #pragma unroll
         for (int v = 0; v < 4; ++v) s_o[wave][n][16 * dt + 4 * q4 + v] = w.o[dt][v];
     __syncthreads();
-    for (int idx = threadIdx.x; idx < G * D; idx += 64 * NW) {
-        const int qi = idx / D, k = idx % D;
+    // four dims per thread, one 16-byte store with the coherent cache policy of st_dev
+    const __amdgpu_buffer_rsrc_t rpo =
+        __builtin_amdgcn_make_buffer_rsrc(pp.o + pp.oi(head, 0, 0, chunk), (short)0, G * D * 4, kBufferDword3);
+    for (int f = threadIdx.x; f < G * D / 4; f += 64 * NW) {
+        const int qi = (4 * f) / D, k = (4 * f) % D;
         float M = -INFINITY;
 #pragma unroll
         for (int ww = 0; ww < NW; ++ww) M = fmaxf(M, s_m[ww][qi]);
-        float acc = 0.f, l = 0.f;
+        f32x4 acc = zero_f4();
+        float l = 0.f;
 #pragma unroll
         for (int ww = 0; ww < NW; ++ww) {
             const float sc = s_m[ww][qi] == -INFINITY ? 0.f : exp2f(s_m[ww][qi] - M);
-            acc = fmaf(sc, s_o[ww][qi][k], acc);
+            acc += sc * lds_ld4(&s_o[ww][qi][k]);
             l = fmaf(sc, s_l[ww][qi], l);
         }
-        st_dev(&pp.o[pp.oi(head, qi, k, chunk)], acc);
+        __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc), rpo, 16u * (uint32_t)f, 0, 16);
         if (k == 0) {
             st_dev(&pp.m[pp.mi(head, qi, chunk)], M);
             st_dev(&pp.l[pp.mi(head, qi, chunk)], l);
