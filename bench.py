@@ -789,6 +789,9 @@ def main():
                                 "heads, 128K context, keys cached before RoPE and rotated at access)",
         "qwen32b_int4": "mixed-page decode attention time per decode step (INT4 factor pages, Qwen3-32B heads, "
                         "128K context, batch 8)",
+        "qwen32b_128k_tp8": "mixed-page decode attention time per decode step (64 layers, one GPU's share of "
+                            "Qwen3-32B heads under 8-way tensor parallelism: 1 KV head, 8 query heads, 128K "
+                            "context)",
     }
     result = {
         "metric": metrics.get(wl.name, "mixed-page decode attention time per decode step"),

@@ -18,17 +18,20 @@ AttnPlan attention_plan(const Geo &g, int64_t max_T) {
     p.n_chunks = (int)ceil_div(n_pages, p.pages_per_chunk);
     // Measured on one MI355X, each choice against the other:
     // - per-wave page claims (no round barrier) for pre-RoPE caches and for
-    //   streams of at most eight 64-token pages per wave: pre-RoPE 128K
-    //   layers 248 -> 221 us, a batch-1 32K layer 29.2 -> 27.1 us; the 128K
-    //   bf16 layers (32 pages per wave) and 32-token pages (no two-unit dense
-    //   pages) gain nothing or lose;
-    // - pages handed out last to first for streams of more than eight pages
-    //   per wave: 128K layers 209.2 -> 204.9 us (adaptive ranks 187.8 ->
-    //   182.9, pre-RoPE 223.5 -> 221.7); the batch-1 streams lose (27.9 ->
-    //   29.3 us), where the static first round gives the dense pages to a
-    //   few waves.
+    //   streams of at most two 64-token pages per wave: pre-RoPE 128K layers
+    //   248 -> 221 us, a batch-1 32K layer (two pages per wave) 29.2 -> 27.1
+    //   us; one GPU's tensor-parallel share of the 128K layers (four pages
+    //   per wave) loses (46.3 -> 52.3 us), as do the 128K bf16 layers (32
+    //   pages per wave) and 32-token pages (no two-unit dense pages);
+    // - pages handed out last to first, except for short streams with
+    //   per-wave claims: 128K layers 209.2 -> 204.9 us (adaptive ranks 187.8
+    //   -> 182.9, pre-RoPE 223.5 -> 221.7), the tensor-parallel share with
+    //   block claims 46.3 -> 42.4 us; the batch-1 32K layer (per-wave claims)
+    //   loses (27.9 -> 29.3 us), where the static first round gives the dense
+    //   pages to a few waves.
     const bool short_stream = p.pages_per_chunk <= 8 * kMfmaWaves;
-    p.sched = ((g.key_t || (g.P == 64 && short_stream)) ? kSchedWaveClaims : 0) | (short_stream ? 0 : kSchedReverse);
+    const bool wave_claims = g.key_t || (g.P == 64 && p.pages_per_chunk <= 2 * kMfmaWaves);
+    p.sched = (wave_claims ? kSchedWaveClaims : 0) | (short_stream && wave_claims ? 0 : kSchedReverse);
     return p;
 }
 

@@ -100,6 +100,12 @@ WORKLOADS = {
     # page model without the rotation; attention rotates keys at access.
     "qwen32b_128k_prerope": Workload("qwen32b_128k_prerope", 8, 4, 8, 64, 128, 64, 131072, 64, 512, 24,
                                      (16, 24, 32), "bf16", 1.0e6, 4, layers=64, key_rope=True),
+    # One GPU's share of the 128K Qwen3-32B-shaped layers under 8-way tensor
+    # parallelism by KV head: 1 kv head with its 8 q heads, batch 4, otherwise
+    # as qwen32b_128k; 64 layers of ~152 MB each, far beyond the 256 MB
+    # last-level cache.
+    "qwen32b_128k_tp8": Workload("qwen32b_128k_tp8", 11, 4, 1, 8, 128, 64, 131072, 64, 512, 24,
+                                 (16, 24, 32), "bf16", 1.0e6, 4, layers=64),
     # INT4 factors: Qwen3-32B heads, batch 8, T=128K.
     "qwen32b_int4": Workload("qwen32b_int4", 5, 8, 8, 64, 128, 64, 131072, 64, 512, 24,
                              (16, 24, 32), "bf16", 1.0e6, 4, factor_dtype="int4"),

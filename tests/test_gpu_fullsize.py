@@ -144,6 +144,13 @@ def test_fullsize_qwen32b_128k_bf16():
     assert checked == 32 * 2 * 2
 
 
+def test_fullsize_qwen32b_128k_tp8_share():
+    """One GPU's share of the 128K layer under 8-way tensor parallelism by KV
+    head (B=4, 1 kv head with 8 q heads): every sequence against the oracle."""
+    checked = _run("qwen32b_128k_tp8", [(b, 0) for b in range(4)], 2)
+    assert checked == 4 * 2 * 2
+
+
 def test_fullsize_qwen32b_128k_adaptive_ranks():
     """The 128K layer with every page's ranks chosen by the decomposition for
     relative Frobenius error 0.2 (cap 32): attention of every (sequence, KV
