@@ -207,6 +207,21 @@ def test_largest_batch():
     _assert_close(out, ref, lse, rl)
 
 
+def test_many_chunks_per_head_16byte_merge():
+    """Heads of 8 queries x 128 dims (more outputs than one pass of the
+    workgroup's threads, so the last workgroup folds with 16-byte loads) and
+    301 pages per sequence in a batch of two: 101 chunks per head (several
+    groups of 32, an odd count against two lanes per output group), the
+    shorter sequence leaving its last chunks empty."""
+    rng = np.random.default_rng(5)
+    T0 = 301 * 64 - 10
+    table = rng.choice([16, 24, 32], size=(2, 1, 301))
+    out, ref, lse, rl = run_case(2, 1, 8, 128, 64, [T0, 3000], 64, 512,
+                                 lambda b, h, j: (int(table[b, h, j]), int(table[b, h, j])),
+                                 r0=24, rope=1e6, outliers=4)
+    _assert_close(out, ref, lse, rl)
+
+
 @pytest.mark.parametrize("case", range(12))
 def test_random_geometries(case):
     """Seeded draws over the bf16 matrix-core kernel's geometry: (d, P)
