@@ -1018,6 +1018,9 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
             for (int v = 0; v < 4; ++v) s_o[wave][n][16 * dt + 4 * q4 + v] = w.o[dt][v];
     }
     __syncthreads();
+    // a head's only workgroup writes out and lse itself (no partial, counter
+    // or merge); otherwise the chunk's partial is published
+    const bool single = pp.nc == 1;
     // four dims per thread: the wave weights once per query and dims, and one
     // 16-byte store with the coherent cache policy of st_dev
     const __amdgpu_buffer_rsrc_t rpo =
@@ -1041,11 +1044,23 @@ __global__ __launch_bounds__(64 * attn_waves<Q4>(), 1) void k_attn_mfma(Geo g, c
             acc *= kQ4Unit;
             l *= kQ4Unit;
         }
+        if (single) {   // Eq. (5) with one partial: normalize
+            const bool empty = T <= 0 || !(l > 0.f);
+            float *o = out + ((int64_t)b * g.Hq + h * G + qi) * D + k;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) o[i] = empty ? 0.f : acc[i] / l;
+            if (lse && k == 0) lse[(int64_t)b * g.Hq + h * G + qi] = empty ? -INFINITY : (M + log2f(l)) * kLn2;
+            continue;
+        }
         __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, acc), rpo, 16u * (uint32_t)f, 0, 16);
         if (k == 0) {
             st_dev(&pp.m[pp.mi(head, qi, chunk)], M);
             st_dev(&pp.l[pp.mi(head, qi, chunk)], l);
         }
+    }
+    if (single) {   // every claim of this workgroup has returned: clear the head's claim word
+        if (threadIdx.x == 0) __hip_atomic_store(pp.claim(head), 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        return;
     }
     // the wave-state block is free once every thread has passed the publish barrier
     publish_and_merge<64 * NW>(g, head, pp, out, lse, T, &s_o[0][0][0]);
