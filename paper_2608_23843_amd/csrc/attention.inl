@@ -213,12 +213,12 @@ __device__ void publish_and_merge(const Geo &g, int64_t head, const Partials &pp
     const int G = g.g, d = g.d;
     bool done = false;
     // only where the per-output fold below would take several passes (G d >
-    // NT): at batch 1 (G d = NT, 32 chunks) that fold measured faster
+    // NT, so two or three lanes per output group): at batch 1 (G d = NT, 32
+    // chunks) that fold measured faster
     if (red && G * d > NT && (G * d) % 4 == 0 && NT % (G * d / 4) == 0) {
         switch (NT / (G * d / 4)) {
         case 2: merge_vec<NT, 2>(g, head, pp, out, lse, T, s_mg, s_lg, red); done = true; break;
         case 3: merge_vec<NT, 3>(g, head, pp, out, lse, T, s_mg, s_lg, red); done = true; break;
-        case 4: merge_vec<NT, 4>(g, head, pp, out, lse, T, s_mg, s_lg, red); done = true; break;
         default: break;
         }
     }

@@ -160,6 +160,31 @@ def test_int4_attention_matches_oracle(seq_lens, ranks):
     assert ma <= MAX_ABS and mr <= MEAN_REL, (ma, mr)
 
 
+def test_int4_attention_one_chunk_per_head():
+    """256 heads of six pages each (B=32, 8 KV heads): every head is one
+    workgroup's chunk, which normalizes its own output (no partial or merge);
+    pages 1 and 2 of every head are INT4 factor pages."""
+    import paper_2608_23843_amd as pk
+    B, Hkv, g, S, W = 32, 8, 8, 64, 128
+    T = 6 * 64 - 7
+    wl = _wl(B, Hkv, g, T, S, W, seed_wid=97)
+    cache = pk.PuzzleKVCache(1, B, Hkv, Hkv * g, D, P, 6, 32, S, W, "bf16", "int4")
+    rng = np.random.default_rng(13)
+    heads = {}
+    for b in range(B):
+        for h in range(Hkv):
+            K, V = synth.kv_head(wl, 0, 0, b, h, 6 * P)
+            K, V = _bf16(K), _bf16(V)
+            rks = {j: tuple(int(x) for x in rng.choice([16, 24, 32], 2)) for j in range(6)}
+            pages, blobs = _encode_head(K, V, T, S, W, lambda j: rks[j])
+            assert sorted(blobs) == [1, 2]
+            _import(cache, b, h, pages, blobs)
+            heads[(b, h)] = oracle.HeadCache(T, P, D, pages)
+    out, ref = _attend(cache, wl, [T] * B, heads, g)
+    ma, mr = errors(out, ref)
+    assert ma <= MAX_ABS and mr <= MEAN_REL, (ma, mr)
+
+
 @pytest.mark.parametrize("g", [1, 5, 16])
 def test_int4_attention_query_groups(g):
     """Query groups below, between and above 8: at most 8 queries the kernel
